@@ -1,0 +1,61 @@
+"""Statistics of the seeded synthetic inputs (they stand in for the paper's
+ReLU outputs on MNIST / CIFAR-10 / ImageNet, which are not available)."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import workloads
+
+
+def test_paper_table_transcription_consistent():
+    # Tab. 3's speedup column equals GEMM / ISC to the printed precision
+    tab = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_tables.json")))
+    assert len(tab["table2_layers"]) == len(tab["table3_cpu_ms"]) == 10
+    for row in tab["table3_cpu_ms"]:
+        assert abs(row["gemm_ms"] / row["isc_ms"] - row["speedup"]) < 0.03, row
+        assert row["sparsity"] >= 0.9   # the paper times only layers at >= 0.9
+
+
+def test_iid_sparsity_and_values():
+    layer = workloads.small_case(4, 8, 12, 12, 6, 3, 3, 1, 1, 0.9, seed=1)
+    x, w = workloads.make_inputs(layer, seed=1)
+    assert x.dtype == np.float32 and w.dtype == np.float32
+    s = np.mean(x == 0)
+    assert abs(s - 0.9) < 0.02
+    assert np.all(x >= 0)
+    assert abs(np.std(w) - 0.1) < 0.02
+
+
+def test_seeded_reproducible():
+    layer = workloads.WORKLOADS["lenet_conv2_tiny"].layers[0]
+    x1, w1 = workloads.make_inputs(layer)
+    x2, w2 = workloads.make_inputs(layer)
+    assert np.array_equal(x1, x2) and np.array_equal(w1, w2)
+    assert layer.seed == workloads.BASE_SEED + 1000
+
+
+def test_clustered_exact_zero_count():
+    layer = workloads.small_case(3, 5, 16, 16, 2, 3, 3, 1, 1, 0.9, seed=3, clustered=True)
+    x, _ = workloads.make_inputs(layer, seed=3)
+    assert int(np.sum(x == 0)) == int(np.ceil(0.9 * x.size))
+    # zeros cluster: a zero's 4-neighbours are zero more often than chance
+    z = x == 0
+    same = np.mean(z[:, :, 1:, :] & z[:, :, :-1, :]) / np.mean(z[:, :, 1:, :])
+    assert same > 0.92
+
+
+def test_workload_shapes():
+    names = set(workloads.WORKLOADS)
+    assert names == {"lenet_conv2_tiny", "lenet_conv2_batch", "alexnet_conv2",
+                     "alexnet_conv345", "inception_28"}
+    sweep = workloads.WORKLOADS["lenet_conv2_batch"].layers
+    assert [l.sparsity for l in sweep] == [0.5, 0.7, 0.9, 0.95, 0.99]
+    assert len({l.seed for l in sweep}) == 5
+
+
+def test_integer_case_bounds():
+    x, w = workloads.integer_case(2, 3, 5, 5, 2, 3, 3, seed=4)
+    assert set(np.unique(x)).issubset(set(range(0, 8)))
+    assert set(np.unique(w)).issubset(set(range(-4, 5)))
