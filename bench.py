@@ -1,0 +1,322 @@
+#!/usr/bin/env python3
+"""Benchmark of the sparse-input convolution on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--all --out FILE]
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: isc_conv2d on the AUTO path, i.e. compaction of the
+input (ISC step 1), the device-side sparse/dense decision, and the
+zero-skipping convolution with its transposed write-out (ISC steps 2-3); the
+dense kernels are launched too and exit on the decision.  Steps are replayed
+from a HIP graph (the layer is launch-bound at microseconds per step).
+
+Workload: LeNet conv2 (20 -> 50 maps, 12 x 12, 5 x 5, stride 1, no pad) at
+batch 256, input sparsity 0.9 (i.i.d. zeros, |N(0,1)| nonzeros, N(0, 0.1)
+weights), the sweep configuration whose 0.9 point the metric is quoted at.
+
+Prints ONE JSON line: value = dense-equivalent TFLOP/s of the step
+(2*N*K*C*R*S*Ho*Wo per step), speedup against the same GPU's dense path
+(im2col + fp32-MFMA GEMM), the sparsity sweep 0.5 .. 0.99, the roofline of
+the dominant kernel (timed with HIP events on the launch stream), and the
+CPU oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import workloads  # noqa: E402
+
+METRIC = "sparse-input conv: dense-equiv TFLOP/s & speedup vs dense at sparsity 0.9"
+HBM_PEAK_GBS = 8000.0
+# fp32 FMA on the vector ALUs without packed instructions (disabled in this
+# build): 256 CUs x 4 SIMDs x 16 lanes x 2 flop x 2.4 GHz
+VALU_F32_PEAK_TFLOPS = 78.6
+VALU_F32_PACKED_PEAK_TFLOPS = 157.3
+MFMA_F32_PEAK_TFLOPS = 157.3
+
+
+def dense_flops(layer, Ho, Wo) -> float:
+    return 2.0 * layer.N * layer.K * layer.C * layer.R * layer.S * Ho * Wo
+
+
+def taps_per_coord(n_in, k, pad, stride, n_out) -> np.ndarray:
+    """For each input coordinate u, how many filter offsets q put it on a
+    valid output ((u + pad - q) divisible by stride, quotient in range)."""
+    u = np.arange(n_in)[:, None]
+    q = np.arange(k)[None, :]
+    num = u + pad - q
+    ok = (num >= 0) & (num % stride == 0) & (num // stride < n_out)
+    return ok.sum(axis=1)
+
+
+def nonzero_macs(x, layer, Ho, Wo) -> int:
+    """Multiply-adds the zero-skipping convolution performs on x (bookkeeping
+    for the nonzero-MAC/s figure)."""
+    nzmask = (x.view(np.uint32) & np.uint32(0x7FFFFFFF)) != 0
+    per_pos = nzmask.sum(axis=(0, 1)).astype(np.int64)          # H x W counts
+    ty = taps_per_coord(layer.H, layer.R, layer.P, layer.T, Ho)
+    tx = taps_per_coord(layer.W, layer.S, layer.P, layer.T, Wo)
+    return int(layer.K * (per_pos * ty[:, None] * tx[None, :]).sum())
+
+
+def event_time_ms(torch, fn, reps: int, warm: int = 3) -> float:
+    """Average ms per call of fn, by HIP events on the current stream around
+    `reps` back-to-back calls."""
+    for _ in range(warm):
+        fn()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        fn()
+    e.record()
+    e.synchronize()
+    return s.elapsed_time(e) / reps
+
+
+def graph_of(torch, fn):
+    """Capture fn (which launches on the current stream) into a HIP graph."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    torch.cuda.synchronize()
+    return g
+
+
+class LayerRun:
+    """Device buffers and callables for one layer."""
+
+    def __init__(self, torch, isc, layer):
+        self.torch, self.isc, self.layer = torch, isc, layer
+        x, w = workloads.make_inputs(layer)
+        self.x_host = x
+        self.x = torch.from_numpy(x).cuda()
+        self.w = torch.from_numpy(w).cuda()
+        L = layer
+        self.desc = isc.make_desc(L.N, L.C, L.H, L.W, L.K, L.R, L.S, L.T, L.P)
+        self.Ho, self.Wo = isc.isc_out_shape(self.desc)
+        self.y = torch.empty((L.N, L.K, self.Ho, self.Wo), device="cuda")
+        self.ws = {p: isc.workspace(self.desc, p) for p in ("auto", "sparse", "dense")}
+        self.lists = isc.isc_compact(self.x)
+        self.wt = isc.isc_repack_filter(self.w)
+        self.col = torch.empty((L.C * L.R * L.S, L.N * self.Ho * self.Wo), device="cuda")
+        torch.cuda.synchronize()
+        self.nnz = int(self.lists[2].item())
+        self.sparsity = 1.0 - self.nnz / x.size
+        self.flops = dense_flops(L, self.Ho, self.Wo)
+        self.nz_macs = nonzero_macs(x, L, self.Ho, self.Wo)
+
+    def conv(self, path):
+        L = self.layer
+        return lambda: self.isc.isc_conv2d(self.x, self.w, L.T, L.P, path=path, out=self.y,
+                                           ws=self.ws[path])
+
+    def compact(self):
+        return lambda: self.isc.isc_compact(self.x, out=self.lists)
+
+    def sparse_kernel(self):
+        L = self.layer
+        return lambda: self.isc.isc_sparse_conv(self.x.shape, self.lists, self.wt, L.T, L.P,
+                                                out=self.y)
+
+    def im2col(self):
+        L = self.layer
+        return lambda: self.isc.isc_im2col(self.x, L.R, L.S, L.T, L.P)
+
+    def measure(self, steps, warmup, graphs=True):
+        torch = self.torch
+        res = {}
+        for path in ("auto", "sparse", "dense"):
+            fn = self.conv(path)
+            if graphs:
+                g = graph_of(torch, fn)
+                fn = g.replay
+            res["t_%s_ms" % path] = event_time_ms(torch, fn, steps, warmup)
+        reps = max(20, steps // 2)
+        res["t_compact_ms"] = event_time_ms(torch, self.compact(), reps)
+        res["t_sparse_kernel_ms"] = event_time_ms(torch, self.sparse_kernel(), reps)
+        res["t_im2col_ms"] = event_time_ms(torch, self.im2col(), max(5, reps // 4))
+        res["t_gemm_ms"] = max(0.0, res["t_dense_ms"] - res["t_im2col_ms"])
+        return res
+
+    def summary(self, res):
+        f, nzm = self.flops, self.nz_macs
+        L = self.layer
+        out = {
+            "workload": L.name, "N": L.N, "C": L.C, "H": L.H, "W": L.W, "K": L.K, "R": L.R,
+            "S": L.S, "stride": L.T, "pad": L.P, "target_sparsity": L.sparsity,
+            "measured_sparsity": round(self.sparsity, 6), "clustered": L.clustered,
+            "dense_gflop": round(f / 1e9, 4), "nonzero_macs": nzm,
+        }
+        for k, v in res.items():
+            out[k] = round(v, 6)
+        for path in ("auto", "sparse", "dense"):
+            out["tflops_%s" % path] = round(f / (res["t_%s_ms" % path] * 1e-3) / 1e12, 3)
+        out["nonzero_mac_per_s_auto"] = nzm / (res["t_auto_ms"] * 1e-3)
+        out["speedup_auto_vs_dense"] = round(res["t_dense_ms"] / res["t_auto_ms"], 3)
+        out["speedup_sparse_vs_dense"] = round(res["t_dense_ms"] / res["t_sparse_ms"], 3)
+        out["speedup_sparse_vs_gemm_only"] = round(res["t_gemm_ms"] / res["t_sparse_ms"], 3)
+        out["sparse_kernel_tflops_nonzero"] = round(2 * nzm / (res["t_sparse_kernel_ms"] * 1e-3) / 1e12, 3)
+        out["gemm_frac_mfma_peak"] = round(f / (res["t_gemm_ms"] * 1e-3) / 1e12 / MFMA_F32_PEAK_TFLOPS, 4) \
+            if res["t_gemm_ms"] > 0 else None
+        return out
+
+
+def cpu_baseline(layer, budget_s=10.0):
+    """The oracle (fp64 direct convolution, all host threads) on the first n
+    images of the workload, n sized for about budget_s seconds."""
+    import oracle
+    x, w = workloads.make_inputs(layer)
+    t0 = time.perf_counter()
+    oracle.conv2d_f64(x[:1], w, layer.T, layer.P)
+    t1 = time.perf_counter() - t0
+    n = int(max(1, min(layer.N, budget_s / max(t1, 1e-6))))
+    t0 = time.perf_counter()
+    out = oracle.conv2d_f64(x[:n], w, layer.T, layer.P)
+    dt = time.perf_counter() - t0
+    Ho, Wo = out.shape[2], out.shape[3]
+    flops = 2.0 * n * layer.K * layer.C * layer.R * layer.S * Ho * Wo
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": "first %d of %d images of %s at sparsity %g (fp64 direct convolution, "
+                      "%.2f s, dense-equivalent flops)" % (n, layer.N, layer.name, layer.sparsity, dt),
+            "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of graph replay")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--all", action="store_true", help="also measure every workload layer")
+    ap.add_argument("--out", default=None, help="JSONL file for --all rows")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the convolution would shard by batch; see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1704_07724_amd as isc
+    isc.lib()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+
+    sweep_layers = workloads.WORKLOADS["lenet_conv2_batch"].layers
+    head_layer = [l for l in sweep_layers if l.sparsity == 0.9][0]
+
+    # headline: whole hot path, AUTO, K timed steps bracketed by synchronize
+    head = LayerRun(torch, isc, head_layer)
+    step_fn = head.conv("auto")
+    if not args.no_graph:
+        step_fn = graph_of(torch, step_fn).replay
+    for _ in range(args.warmup):
+        step_fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step_fn()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = head.flops / (ms_per_step * 1e-3) / 1e12
+
+    res = head.measure(args.steps, args.warmup, graphs=not args.no_graph)
+    hs = head.summary(res)
+    t_kernel = res["t_sparse_kernel_ms"]
+    achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
+    roofline = {"bound": "alu", "kernel": "sparse_conv_kernel", "achieved": round(achieved, 3),
+                "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4), "traffic": None,
+                "per_launch": {"nonzero_macs": head.nz_macs, "flops": 2 * head.nz_macs,
+                               "avg_duration_ms": round(t_kernel, 6)},
+                "frac_vs_packed_peak": round(achieved / VALU_F32_PACKED_PEAK_TFLOPS, 4)}
+
+    sweep = []
+    if not args.no_sweep:
+        for layer in sweep_layers:
+            run = head if layer is head_layer else LayerRun(torch, isc, layer)
+            r = res if layer is head_layer else run.measure(max(50, args.steps // 2), 10,
+                                                            graphs=not args.no_graph)
+            s = run.summary(r)
+            sweep.append({k: s[k] for k in (
+                "target_sparsity", "measured_sparsity", "t_auto_ms", "t_sparse_ms", "t_dense_ms",
+                "t_compact_ms", "t_sparse_kernel_ms", "t_gemm_ms", "tflops_auto", "tflops_sparse",
+                "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense",
+                "speedup_sparse_vs_dense", "sparse_kernel_tflops_nonzero")})
+            if run is not head:
+                del run
+                torch.cuda.empty_cache()
+
+    line = {
+        "metric": METRIC, "value": round(value, 4), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "lenet_conv2_batch", "N": head_layer.N, "C": head_layer.C,
+                   "H": head_layer.H, "W": head_layer.W, "K": head_layer.K, "R": head_layer.R,
+                   "S": head_layer.S, "stride": head_layer.T, "pad": head_layer.P,
+                   "sparsity": head_layer.sparsity, "path": "auto", "threshold": 0.9,
+                   "launch": "eager" if args.no_graph else "hip_graph"},
+        "speedup_vs_dense": hs["speedup_auto_vs_dense"],
+        "speedup_vs_dense_gemm_only": round(res["t_gemm_ms"] / res["t_auto_ms"], 3),
+        "nonzero_mac_per_s": hs["nonzero_mac_per_s_auto"],
+        "measured_sparsity": hs["measured_sparsity"],
+        "dense_path_tflops": hs["tflops_dense"],
+        "roofline": roofline,
+        "timings_ms": {k: hs[k] for k in hs if k.startswith("t_")},
+        "sweep": sweep,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(head_layer)
+
+    if args.all:
+        rows = []
+        for wl in workloads.WORKLOADS.values():
+            for layer in wl.layers:
+                if wl.name == "lenet_conv2_batch":
+                    continue
+                run = LayerRun(torch, isc, layer)
+                s = run.summary(run.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph))
+                rows.append(s)
+                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx" % (
+                    layer.name, s["t_auto_ms"], s["t_sparse_ms"], s["t_dense_ms"],
+                    s["speedup_sparse_vs_dense"]), file=sys.stderr, flush=True)
+                del run
+                torch.cuda.empty_cache()
+        if args.out:
+            with open(args.out, "w") as f:
+                for r in rows:
+                    f.write(json.dumps(r) + "\n")
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

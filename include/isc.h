@@ -1,0 +1,195 @@
+/*
+ * isc.h -- C ABI of the sparse-input ("inverse sparse") convolution library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Method: Shi & Chu, "Speeding up Convolutional Neural Networks By Exploiting
+ * the Sparsity of Rectifier Units" (arXiv 1704.07724).  The input of a
+ * convolution is the output of a ReLU (Eq. 2), so most of its entries are
+ * zero; the sparse path lists the nonzero inputs (ISC step 1, Sec. "Sparse
+ * Convolution") and multiplies only those with K-contiguous weight vectors
+ * (ISC step 2), accumulating an output tile that is written out transposed
+ * to NCHW (ISC step 3).  The dense path is the matrix-multiplication
+ * formulation M_K x M_I = M_O of Fig. 3 (im2col followed by a GEMM), the
+ * paper's baseline.  A dispatcher picks one by measured input sparsity.
+ *
+ * Conventions shared by every entry point
+ *   - All tensors are fp32 (indices int32/uint32), dense and row-major:
+ *     input  x  N x C x H x W   (NCHW)
+ *     filter w  K x C x R x S   (KCRS)
+ *     output y  N x K x Ho x Wo (NCHW),
+ *     Ho = floor((H + 2P - R)/T) + 1, Wo = floor((W + 2P - S)/T) + 1.
+ *   - Device pointers are caller-owned HIP device allocations on the current
+ *     device; the library allocates no device memory.  Work is enqueued on the
+ *     given HIP stream (hipStream_t passed as void*, NULL = default stream)
+ *     and the call returns without waiting, unless stated otherwise.
+ *   - Return value: ISC_OK (0) or one of the positive status codes below.
+ *     Arguments are validated on the host before anything is enqueued; on a
+ *     validation error nothing is enqueued and no output is touched.  No C++
+ *     exception crosses the ABI and nothing is printed.
+ *   - Limits: every dimension >= 1, stride >= 1, pad >= 0, Ho and Wo >= 1,
+ *     H and W <= 65535, and N*C*H*W, N*K*Ho*Wo, K*C*R*S and the im2col
+ *     matrix (C*R*S rows of the padded column count) each below 2^31
+ *     elements.  Float pointers must be 4-byte aligned, workspaces 256-byte
+ *     aligned.
+ *   - Calls that share a workspace must not overlap in time (same stream, or
+ *     synchronised).
+ */
+#ifndef ISC_H
+#define ISC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Parameters of one convolution: the paper's Tab. 1 ("Parameters of
+ * Convolution") with the batch N added.  stride is T, pad is P (the same on
+ * both axes and on both sides). */
+typedef struct isc_conv_desc {
+    int32_t N;      /* images in the batch */
+    int32_t C;      /* input feature maps */
+    int32_t H, W;   /* input height and width (H_in, W_in) */
+    int32_t K;      /* output feature maps */
+    int32_t R, S;   /* filter height and width */
+    int32_t stride; /* T */
+    int32_t pad;    /* P, zero padding */
+} isc_conv_desc;
+
+/* Which path isc_conv2d runs. */
+typedef enum isc_path {
+    ISC_PATH_AUTO = 0,   /* compact, then sparse if sparsity >= threshold else dense */
+    ISC_PATH_SPARSE = 1, /* compaction + zero-skipping convolution */
+    ISC_PATH_DENSE = 2   /* im2col + MFMA GEMM */
+} isc_path;
+
+/* One entry of the nonzero list of ISC step 1: the value (bit-exact copy of
+ * the input) and its position in its plane, yx = (row << 16) | column. */
+typedef struct isc_nz {
+    float v;
+    uint32_t yx;
+} isc_nz;
+
+enum isc_status {
+    ISC_OK = 0,
+    ISC_ERR_NULL = 1,      /* a required pointer is NULL */
+    ISC_ERR_SHAPE = 2,     /* a dimension < 1, stride < 1, pad < 0, or Ho/Wo < 1 */
+    ISC_ERR_LIMIT = 3,     /* a size exceeds the int32 / 16-bit limits above */
+    ISC_ERR_WORKSPACE = 4, /* workspace smaller than isc_workspace_size */
+    ISC_ERR_ALIAS = 5,     /* output overlaps an input or the workspace */
+    ISC_ERR_PATH = 6,      /* path not an isc_path value */
+    ISC_ERR_DEVICE = 7,    /* no device, or the current device is not gfx950 */
+    ISC_ERR_HIP = 8,       /* a HIP runtime call failed */
+    ISC_ERR_ALIGN = 9,     /* pointer misaligned */
+    ISC_ERR_ARG = 10       /* other bad argument (threshold outside [0,1], ...) */
+};
+
+/* Output extent (Sec. "Sparsity of ReLUs" output-size formula, read as
+ * floor((H + 2P - R)/T) + 1; the printed (H + 2P - R + 1)/T agrees at T = 1).
+ * Host-only.  Ho/Wo receive the sizes.  Errors: NULL, SHAPE. */
+int isc_out_shape(const isc_conv_desc *d, int32_t *Ho, int32_t *Wo);
+
+/* Bytes of device workspace isc_conv2d needs for this descriptor and path
+ * (AUTO needs the sparse and dense buffers).  Host-only.  Errors: NULL,
+ * SHAPE, LIMIT, PATH. */
+int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes);
+
+/* The convolution of Eq. 1 (Sec. "Sparsity of ReLUs"), extended with batch,
+ * stride T and zero padding P, no bias and no activation:
+ *   y[n,k,i,j] = sum_{c,r,s} w[k,c,r,s] * x[n,c,i*T+r-P,j*T+s-P]
+ * (x taken as 0 outside the map).
+ *   x, w: device inputs (read only).  y: device output, fully written.
+ *   ws, ws_bytes: device workspace, at least isc_workspace_size(d, path)
+ *     bytes, 256-byte aligned; contents on entry are ignored.
+ *   path: isc_path.  threshold: the sparsity (fraction of zero inputs,
+ *     Sec. "Sparse Convolution") at or above which AUTO takes the sparse
+ *     path; the paper's experiments use 0.9 (Abstract, Sec. "Experiments").
+ *     The decision is made on the device from the compaction's count, with no
+ *     host synchronisation; isc_decision reads it back.
+ *   stream: hipStream_t or NULL.
+ * A value counts as zero iff its bits with the sign cleared are zero.
+ * fp32 throughout; the sparse path accumulates in fp32 in an order of its
+ * own, the dense path in MFMA order.  Errors: NULL, SHAPE, LIMIT, WORKSPACE,
+ * ALIAS, PATH, ARG, ALIGN, DEVICE, HIP. */
+int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
+               void *ws, size_t ws_bytes, int32_t path, float threshold,
+               void *stream);
+
+/* After isc_conv2d has completed on `stream` (this call synchronises the
+ * stream): the number of nonzero inputs the compaction counted (UINT64_MAX
+ * if the call ran the dense path only) and the path taken (ISC_PATH_SPARSE
+ * or ISC_PATH_DENSE).  ws/ws_bytes as passed to isc_conv2d.  Errors: NULL,
+ * WORKSPACE, HIP. */
+int isc_decision(const isc_conv_desc *d, const void *ws, size_t ws_bytes,
+                 uint64_t *nnz_total, int32_t *path_taken, void *stream);
+
+/* ISC step 1 (Sec. "Sparse Convolution"): list the nonzero inputs of every
+ * (n, c) plane with their row and column, in row-major order.
+ *   row_ptr: device int32[N*C*(H+1)]; row_ptr[p*(H+1) + y] = nonzeros of
+ *     plane p = n*C + c in rows < y (plane-relative), so row_ptr[p*(H+1)+H]
+ *     is the plane's count.
+ *   nz: device isc_nz[N*C*H*W]; entry e of plane p at nz[p*H*W + e]; slots
+ *     past the plane's count are not written.
+ *   nnz_total: device uint64, set to the total count (cleared by the call).
+ * The output is unique and bit-exact (values are bit copies).  Filter fields
+ * of d (K, R, S, stride, pad) must be valid but are otherwise unused.
+ * Errors: NULL, SHAPE, LIMIT, ALIAS, ALIGN, DEVICE, HIP. */
+int isc_compact(const isc_conv_desc *d, const float *x, int32_t *row_ptr,
+                isc_nz *nz, uint64_t *nnz_total, void *stream);
+
+/* ISC step 2's filter layout (Sec. "Sparse Convolution": the kernel matrix
+ * stored so that, for one input channel and tap, the weights of consecutive
+ * output maps are contiguous):
+ *   wt[((c*R + r)*S + s)*K + k] = w[k, c, r, s]
+ *   w: device K x C x R x S; wt: device float[K*C*R*S], must not overlap w.
+ * Only K, C, R, S of d are used (all must be valid).  Errors: NULL, SHAPE,
+ * LIMIT, ALIAS, ALIGN, DEVICE, HIP. */
+int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *stream);
+
+/* ISC steps 2 and 3 (Sec. "Sparse Convolution") on lists that isc_compact
+ * produced for the same input shape: for every nonzero x[n,c,y,x] and every
+ * filter tap (r, s) that reaches a valid output, add x * wt[c,r,s,k] to
+ * y[n, k, (y+P-r)/T, (x+P-s)/T]; then y holds the convolution of Eq. 1.
+ *   row_ptr, nz: as written by isc_compact for N, C, H, W of d (read only;
+ *     nz must have 64 readable entries past N*C*H*W -- isc_conv2d's
+ *     workspace does; a caller's own buffer of N*C*H*W + 64 entries does).
+ *   wt: the repacked filter of isc_repack_filter.
+ *   y: device output N x K x Ho x Wo, fully written, must not overlap the
+ *     inputs.
+ * One launch, no workspace, deterministic (each output is summed by one
+ * lane in list order).  Several convolutions of the same input (for example
+ * the branches of an inception block) can share one compaction.  Errors:
+ * NULL, SHAPE, LIMIT (no LDS tiling fits the shape), ALIAS, ALIGN, DEVICE,
+ * HIP. */
+int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz *nz,
+                    const float *wt, float *y, void *stream);
+
+/* The unrolled input matrix M_I of the matrix-multiplication formulation
+ * (Sec. "Sparse Convolution", Fig. 3), with the batch as extra columns:
+ *   col[(c*R + r)*S + s][(n*Ho + i)*Wo + j] = x[n, c, i*T + r - P, j*T + s - P]
+ * (0 outside the map), row stride ldc >= N*Ho*Wo elements; columns
+ * [N*Ho*Wo, ldc) of every row are set to 0.  Bit-exact copy.
+ * Errors: NULL, SHAPE, LIMIT, ALIAS, ALIGN, ARG (ldc too small), DEVICE, HIP. */
+int isc_im2col(const isc_conv_desc *d, const float *x, float *col, int64_t ldc,
+               void *stream);
+
+/* The GEMM of Fig. 3 on its own: c[m][n] = sum_k a[m][k] * b[k][n] for
+ * m < M, n < Ncols, k < Kd, fp32 inputs and accumulation on the fp32 matrix
+ * cores.  Row-major with leading dimensions lda >= Kd, ldb >= Ncols,
+ * ldc >= Ncols (elements).  Errors: NULL, SHAPE, LIMIT, ALIAS, ALIGN,
+ * DEVICE, HIP. */
+int isc_gemm_f32(int32_t M, int32_t Ncols, int32_t Kd, const float *a, int64_t lda,
+                 const float *b, int64_t ldb, float *c, int64_t ldc, void *stream);
+
+/* Short text for a status code (static storage). */
+const char *isc_status_str(int status);
+
+/* Library version, for logs. */
+const char *isc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISC_H */

@@ -65,6 +65,8 @@ def load_library(path: str):
     lib.oracle_nz_macs.restype = i64
     lib.oracle_im2col.argtypes = [vp] + [i32] * 8 + [i64, vp]
     lib.oracle_im2col.restype = None
+    lib.oracle_threads.argtypes = []
+    lib.oracle_threads.restype = i32
     return lib
 
 
@@ -92,6 +94,11 @@ def _f32(a) -> np.ndarray:
 
 def _ptr(a: np.ndarray):
     return ctypes.c_void_p(a.ctypes.data)
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().oracle_threads())
 
 
 def out_size(n_in: int, k: int, pad: int, stride: int) -> int:

@@ -28,6 +28,19 @@
  */
 #include <stdint.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* Threads the parallel loops below use (for reporting CPU-baseline runs). */
+int oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
 
 /* Output extent along one axis: floor((in + 2*pad - k) / stride) + 1, or 0
  * when the padded input is shorter than the filter. */

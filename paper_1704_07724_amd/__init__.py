@@ -1,0 +1,281 @@
+"""Python binding of libisc.so, the MI355X sparse-input convolution library.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C ABI declared in include/isc.h; torch supplies device
+memory and the current stream.  The binding refuses to work without the built
+library (there is no fallback of any kind).
+
+The functions carry the C names:
+    isc_out_shape, isc_workspace_size, isc_conv2d, isc_decision,
+    isc_compact, isc_im2col, isc_gemm_f32, isc_status_str, isc_version
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG_DIR = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG_DIR, "libisc.so")
+
+PATHS = {"auto": 0, "sparse": 1, "dense": 2}
+PATH_NAMES = {v: k for k, v in PATHS.items()}
+
+ISC_OK = 0
+STATUS = {
+    0: "ISC_OK", 1: "ISC_ERR_NULL", 2: "ISC_ERR_SHAPE", 3: "ISC_ERR_LIMIT",
+    4: "ISC_ERR_WORKSPACE", 5: "ISC_ERR_ALIAS", 6: "ISC_ERR_PATH", 7: "ISC_ERR_DEVICE",
+    8: "ISC_ERR_HIP", 9: "ISC_ERR_ALIGN", 10: "ISC_ERR_ARG",
+}
+EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
+           "isc_compact", "isc_repack_filter", "isc_sparse_conv", "isc_im2col", "isc_gemm_f32",
+           "isc_status_str", "isc_version")
+
+
+class IscError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (%s)" % (where, STATUS.get(status, status),
+                                          status_str(status)))
+
+
+class ConvDesc(ctypes.Structure):
+    """isc_conv_desc: Tab. 1 parameters plus the batch."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("N", "C", "H", "W", "K", "R", "S", "stride", "pad")]
+
+    def astuple(self):
+        return tuple(getattr(self, f) for f, _ in self._fields_)
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libisc.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libisc.so is not built (%s); run "
+                          "`python -m paper_1704_07724_amd.build`" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    i32, i64, sz, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+    dp = ctypes.POINTER(ConvDesc)
+    L.isc_out_shape.argtypes = [dp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    L.isc_workspace_size.argtypes = [dp, i32, ctypes.POINTER(sz)]
+    L.isc_conv2d.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, vp]
+    L.isc_decision.argtypes = [dp, vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(i32), vp]
+    L.isc_compact.argtypes = [dp, vp, vp, vp, vp, vp]
+    L.isc_repack_filter.argtypes = [dp, vp, vp, vp]
+    L.isc_sparse_conv.argtypes = [dp, vp, vp, vp, vp, vp]
+    L.isc_im2col.argtypes = [dp, vp, vp, i64, vp]
+    L.isc_gemm_f32.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
+    for name in EXPORTS[:9]:
+        getattr(L, name).restype = ctypes.c_int
+    L.isc_status_str.argtypes = [ctypes.c_int]
+    L.isc_status_str.restype = ctypes.c_char_p
+    L.isc_version.argtypes = []
+    L.isc_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str) -> None:
+    if status != ISC_OK:
+        raise IscError(status, where)
+
+
+def status_str(status: int) -> str:
+    return lib().isc_status_str(int(status)).decode()
+
+
+isc_status_str = status_str
+
+
+def isc_version() -> str:
+    return lib().isc_version().decode()
+
+
+def make_desc(N, C, H, W, K, R, S, stride=1, pad=0) -> ConvDesc:
+    return ConvDesc(N, C, H, W, K, R, S, stride, pad)
+
+
+def _desc_of(x_shape, w_shape, stride, pad) -> ConvDesc:
+    N, C, H, W = (int(v) for v in x_shape)
+    K, C2, R, S = (int(v) for v in w_shape)
+    if C != C2:
+        raise ValueError("input has %d channels, filter expects %d" % (C, C2))
+    return make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
+
+
+def isc_out_shape(desc: ConvDesc):
+    ho, wo = ctypes.c_int32(), ctypes.c_int32()
+    _check(lib().isc_out_shape(ctypes.byref(desc), ctypes.byref(ho), ctypes.byref(wo)),
+           "isc_out_shape")
+    return ho.value, wo.value
+
+
+def isc_workspace_size(desc: ConvDesc, path="auto") -> int:
+    n = ctypes.c_size_t()
+    _check(lib().isc_workspace_size(ctypes.byref(desc), _path(path), ctypes.byref(n)),
+           "isc_workspace_size")
+    return n.value
+
+
+def _path(path) -> int:
+    if isinstance(path, str):
+        return PATHS[path]
+    return int(path)
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(stream):
+    torch = _torch()
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev_f32(t, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32:
+        raise TypeError("%s must be a float32 CUDA/HIP tensor" % name)
+    return t.contiguous()
+
+
+def workspace(desc: ConvDesc, path="auto", device=None):
+    """A device workspace of isc_workspace_size bytes (256-byte aligned)."""
+    torch = _torch()
+    n = isc_workspace_size(desc, path)
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device or "cuda")
+
+
+def isc_conv2d(x, w, stride=1, pad=0, path="auto", threshold=0.9, out=None, ws=None,
+               stream=None):
+    """y = conv(x, w) (Eq. 1 with batch, stride, zero padding) on the GPU.
+
+    x: [N, C, H, W] float32, w: [K, C, R, S] float32 (device tensors).
+    path: "auto" | "sparse" | "dense"; threshold: sparsity at or above which
+    "auto" takes the sparse path.  Returns y [N, K, Ho, Wo] (``out`` if given).
+    """
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    w = _dev_f32(w, "w")
+    desc = _desc_of(x.shape, w.shape, stride, pad)
+    ho, wo = isc_out_shape(desc)
+    if out is None:
+        out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
+    elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
+        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+    if ws is None:
+        ws = workspace(desc, path, x.device)
+    _check(lib().isc_conv2d(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                            ws.data_ptr(), ws.numel() * ws.element_size(), _path(path),
+                            float(threshold), _stream(stream)), "isc_conv2d")
+    return out
+
+
+def isc_decision(desc: ConvDesc, ws, stream=None):
+    """(nnz_total, path_name) recorded by the last isc_conv2d on ``ws``;
+    synchronises the stream."""
+    nnz = ctypes.c_uint64()
+    path = ctypes.c_int32()
+    _check(lib().isc_decision(ctypes.byref(desc), ws.data_ptr(), ws.numel() * ws.element_size(),
+                              ctypes.byref(nnz), ctypes.byref(path), _stream(stream)),
+           "isc_decision")
+    return nnz.value, PATH_NAMES.get(path.value, path.value)
+
+
+NZ_TAIL = 64  # spare entries isc_sparse_conv may read past the last plane
+
+
+def isc_compact(x, stream=None, out=None):
+    """ISC step 1 on the GPU.
+
+    Returns (row_ptr [N*C, H+1] int32, entries [N*C, H*W, 2] int32 holding
+    (value bits, (row << 16) | column), nnz_total [1] int64), all on the
+    device; entries past a plane's count are left as allocated (zeros here).
+    The entries view sits in a buffer with NZ_TAIL spare entries, so it can
+    be passed to isc_sparse_conv.  ``out`` reuses (row_ptr, entries, total).
+    """
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    N, C, H, W = (int(v) for v in x.shape)
+    desc = make_desc(N, C, H, W, 1, 1, 1, 1, 0)
+    if out is None:
+        row_ptr = torch.empty((N * C, H + 1), dtype=torch.int32, device=x.device)
+        buf = torch.zeros((N * C * H * W + NZ_TAIL, 2), dtype=torch.int32, device=x.device)
+        nz = buf[:N * C * H * W].view(N * C, H * W, 2)
+        total = torch.empty(1, dtype=torch.int64, device=x.device)
+    else:
+        row_ptr, nz, total = out
+    _check(lib().isc_compact(ctypes.byref(desc), x.data_ptr(), row_ptr.data_ptr(), nz.data_ptr(),
+                             total.data_ptr(), _stream(stream)), "isc_compact")
+    return row_ptr, nz, total
+
+
+def isc_repack_filter(w, out=None, stream=None):
+    """ISC step 2's filter layout: wt [C, R, S, K] with K contiguous."""
+    torch = _torch()
+    w = _dev_f32(w, "w")
+    K, C, R, S = (int(v) for v in w.shape)
+    desc = make_desc(1, C, max(R, 1), max(S, 1), K, R, S, 1, 0)
+    if out is None:
+        out = torch.empty((C, R, S, K), dtype=torch.float32, device=w.device)
+    _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), out.data_ptr(),
+                                   _stream(stream)), "isc_repack_filter")
+    return out
+
+
+def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):
+    """ISC steps 2-3 from compacted lists (isc_compact's (row_ptr, entries,
+    ...)) and a repacked filter wt [C, R, S, K]; returns y [N, K, Ho, Wo]."""
+    torch = _torch()
+    N, C, H, W = (int(v) for v in x_shape)
+    C2, R, S, K = (int(v) for v in wt.shape)
+    if C != C2:
+        raise ValueError("channel mismatch")
+    row_ptr, nz = lists[0], lists[1]
+    desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
+    ho, wo = isc_out_shape(desc)
+    if out is None:
+        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=wt.device)
+    _check(lib().isc_sparse_conv(ctypes.byref(desc), row_ptr.data_ptr(), nz.data_ptr(),
+                                 wt.data_ptr(), out.data_ptr(), _stream(stream)),
+           "isc_sparse_conv")
+    return out
+
+
+def isc_im2col(x, R, S, stride=1, pad=0, ldc=None, stream=None):
+    """The unrolled input matrix M_I (Fig. 3) on the GPU: [C*R*S, ldc] float32."""
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    N, C, H, W = (int(v) for v in x.shape)
+    desc = make_desc(N, C, H, W, 1, int(R), int(S), int(stride), int(pad))
+    ho, wo = isc_out_shape(desc)
+    ldc = N * ho * wo if ldc is None else int(ldc)
+    col = torch.empty((C * R * S, ldc), dtype=torch.float32, device=x.device)
+    _check(lib().isc_im2col(ctypes.byref(desc), x.data_ptr(), col.data_ptr(), ldc,
+                            _stream(stream)), "isc_im2col")
+    return col
+
+
+def isc_gemm_f32(a, b, out=None, stream=None):
+    """c = a @ b on the fp32 matrix cores (a [M, Kd], b [Kd, N], row-major)."""
+    torch = _torch()
+    a = _dev_f32(a, "a")
+    b = _dev_f32(b, "b")
+    M, Kd = (int(v) for v in a.shape)
+    Kd2, N = (int(v) for v in b.shape)
+    if Kd != Kd2:
+        raise ValueError("inner dimensions differ")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=a.device)
+    _check(lib().isc_gemm_f32(M, N, Kd, a.data_ptr(), Kd, b.data_ptr(), N, out.data_ptr(), N,
+                              _stream(stream)), "isc_gemm_f32")
+    return out

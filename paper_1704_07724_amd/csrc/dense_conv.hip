@@ -1,0 +1,289 @@
+// Dense baseline: the matrix-multiplication formulation of convolution
+// (Sec. "Sparse Convolution", Fig. 3), M_K [K x RSC] * M_I [RSC x HoWo] =
+// M_O [K x HoWo], with the batch appended as extra columns of M_I.
+//
+// im2col writes M_I to the workspace (row (c, r, s), column (n, i, j)); the
+// GEMM multiplies the filter tensor, read in place as the row-major K x CRS
+// matrix M_K, by M_I on the fp32 matrix cores (v_mfma_f32_32x32x2_f32) and
+// scatters each output column back to NCHW in its epilogue.
+#include "isc_internal.hpp"
+
+#include <algorithm>
+
+namespace isc {
+namespace {
+
+// ----------------------------------------------------------------- im2col --
+
+constexpr int kIm2colRows = 8;  // rows of M_I per thread
+
+__global__ __launch_bounds__(256)
+void im2col_kernel(const float *__restrict__ x, int C, int H, int W, int R, int S, int T, int P,
+                   int Ho, int Wo, int ncols, float *__restrict__ col, int64_t ldc, int rows_total,
+                   Decision dec) {
+    if (!decision_says_run(dec)) return;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && dec.record) {
+        // dense-only call: no compaction ran, so there is no count
+        dec.record->nnz_total = ~0ull;
+        dec.record->path_taken = 2u;
+    }
+    const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (j >= ldc) return;
+    const bool real = j < ncols;
+    int n = 0, oy = 0, ox = 0;
+    if (real) {
+        const int hw = Ho * Wo;
+        n = static_cast<int>(j / hw);
+        const int p = static_cast<int>(j - static_cast<int64_t>(n) * hw);
+        oy = p / Wo;
+        ox = p - oy * Wo;
+    }
+    const int RS = R * S;
+    for (int q_begin = blockIdx.y * kIm2colRows; q_begin < rows_total;
+         q_begin += gridDim.y * kIm2colRows) {
+        const int q_end = min(rows_total, q_begin + kIm2colRows);
+        for (int q = q_begin; q < q_end; ++q) {
+            float v = 0.0f;
+            if (real) {
+                const int c = q / RS;
+                const int rs = q - c * RS;
+                const int r = rs / S;
+                const int s = rs - r * S;
+                const int iy = oy * T + r - P;
+                const int ix = ox * T + s - P;
+                if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+                    v = x[((static_cast<size_t>(n) * C + c) * H + iy) * W + ix];
+            }
+            col[static_cast<size_t>(q) * ldc + j] = v;
+        }
+    }
+}
+
+// ------------------------------------------------------------------- GEMM --
+//
+// Workgroup tile BM x BN = (WAVES_M * WM * 32) x (WAVES_N * WN * 32), four
+// wavefronts, each owning WM x WN blocks of 32 x 32 accumulated by
+// v_mfma_f32_32x32x2_f32.  K-slices of BK = 16 go through two LDS buffers;
+// the next slice's global loads are in flight while the current one feeds
+// the matrix cores.  A slices are stored transposed ([k][m]) so that both
+// operands are read by 32 consecutive lanes at consecutive addresses.
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int BK = 16;
+
+struct GemmArgs {
+    int M, N, Kd;
+    const float *a;
+    int64_t lda;
+    const float *b;
+    int64_t ldb;
+    float *c;
+    int64_t ldc;
+    int conv_hw;  // > 0: scatter column n to NCHW with Ho*Wo = conv_hw
+    Decision dec;
+};
+
+template <int WAVES_M, int WM, int WN, bool A_VEC, bool B_PADDED>
+__global__ __launch_bounds__(256)
+void gemm_f32_kernel(GemmArgs g) {
+    if (!decision_says_run(g.dec)) return;
+    constexpr int WAVES_N = 4 / WAVES_M;
+    constexpr int BM = WAVES_M * WM * 32;
+    constexpr int BN = WAVES_N * WN * 32;
+    constexpr int PADA = 4, PADB = 4;
+    __shared__ __align__(16) float As[2][BK][BM + PADA];
+    __shared__ __align__(16) float Bs[2][BK][BN + PADB];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave / WAVES_N;
+    const int wn = wave % WAVES_N;
+    const int m0 = blockIdx.y * BM;
+    const int n0 = blockIdx.x * BN;
+    const int M = g.M, N = g.N, Kd = g.Kd;
+
+    // global -> register staging
+    constexpr int A_F4 = BM * BK / 4;  // float4 per A slice
+    constexpr int B_F4 = BK * BN / 4;
+    constexpr int A_PER = (A_F4 + 255) / 256;
+    constexpr int B_PER = (B_F4 + 255) / 256;
+    float4 ra[A_PER];
+    float4 rb[B_PER];
+
+    auto load_slice = [&](int k0) {
+        const bool full_k = k0 + BK <= Kd;
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            const int idx = tid + i * 256;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (idx < A_F4) {
+                const int row = idx % BM;   // consecutive lanes: consecutive rows
+                const int kq = idx / BM;    // which 4-wide k group
+                const int m = m0 + row;
+                const int k = k0 + kq * 4;
+                if (m < M) {
+                    const float *src = g.a + static_cast<size_t>(m) * g.lda + k;
+                    if (A_VEC && full_k) {
+                        v = *reinterpret_cast<const float4 *>(src);
+                    } else {
+                        v.x = k + 0 < Kd ? src[0] : 0.f;
+                        v.y = k + 1 < Kd ? src[1] : 0.f;
+                        v.z = k + 2 < Kd ? src[2] : 0.f;
+                        v.w = k + 3 < Kd ? src[3] : 0.f;
+                    }
+                }
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < B_PER; ++i) {
+            const int idx = tid + i * 256;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (idx < B_F4) {
+                const int row = idx / (BN / 4);
+                const int nq = idx % (BN / 4);
+                const int k = k0 + row;
+                const int nn = n0 + nq * 4;
+                if (k < Kd) {
+                    const float *src = g.b + static_cast<size_t>(k) * g.ldb + nn;
+                    if (B_PADDED) {
+                        v = *reinterpret_cast<const float4 *>(src);
+                    } else {
+                        v.x = nn + 0 < N ? src[0] : 0.f;
+                        v.y = nn + 1 < N ? src[1] : 0.f;
+                        v.z = nn + 2 < N ? src[2] : 0.f;
+                        v.w = nn + 3 < N ? src[3] : 0.f;
+                    }
+                }
+            }
+            rb[i] = v;
+        }
+    };
+    auto store_slice = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i) {
+            const int idx = tid + i * 256;
+            if (idx < A_F4) {
+                const int row = idx % BM;
+                const int kq = idx / BM;
+                As[buf][kq * 4 + 0][row] = ra[i].x;
+                As[buf][kq * 4 + 1][row] = ra[i].y;
+                As[buf][kq * 4 + 2][row] = ra[i].z;
+                As[buf][kq * 4 + 3][row] = ra[i].w;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < B_PER; ++i) {
+            const int idx = tid + i * 256;
+            if (idx < B_F4) {
+                const int row = idx / (BN / 4);
+                const int nq = idx % (BN / 4);
+                *reinterpret_cast<float4 *>(&Bs[buf][row][nq * 4]) = rb[i];
+            }
+        }
+    };
+
+    floatx16 acc[WM][WN];
+#pragma unroll
+    for (int i = 0; i < WM; ++i)
+#pragma unroll
+        for (int j = 0; j < WN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const int nk = (Kd + BK - 1) / BK;
+    load_slice(0);
+    store_slice(0);
+    __syncthreads();
+    const int lrow = lane & 31;   // row (A) / column (B) within a 32-block
+    const int lk = lane >> 5;     // which of the two k of an MFMA step
+    for (int kt = 0; kt < nk; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < nk) load_slice((kt + 1) * BK);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            float av[WM], bv[WN];
+#pragma unroll
+            for (int i = 0; i < WM; ++i) av[i] = As[buf][kk + lk][(wm * WM + i) * 32 + lrow];
+#pragma unroll
+            for (int j = 0; j < WN; ++j) bv[j] = Bs[buf][kk + lk][(wn * WN + j) * 32 + lrow];
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+#pragma unroll
+                for (int j = 0; j < WN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+        }
+        if (kt + 1 < nk) store_slice(buf ^ 1);
+        __syncthreads();
+    }
+
+    // epilogue: accumulator register v of lane l holds row
+    // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32 x 32 block
+#pragma unroll
+    for (int j = 0; j < WN; ++j) {
+        const int nn = n0 + (wn * WN + j) * 32 + lrow;
+        if (nn >= N) continue;
+        size_t col_off;
+        size_t row_stride;
+        if (g.conv_hw > 0) {
+            const int img = nn / g.conv_hw;
+            const int p = nn - img * g.conv_hw;
+            col_off = static_cast<size_t>(img) * M * g.conv_hw + p;
+            row_stride = static_cast<size_t>(g.conv_hw);
+        } else {
+            col_off = static_cast<size_t>(nn);
+            row_stride = static_cast<size_t>(g.ldc);
+        }
+#pragma unroll
+        for (int i = 0; i < WM; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + (wm * WM + i) * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+                if (m < M) g.c[col_off + static_cast<size_t>(m) * row_stride] = acc[i][j][v];
+            }
+        }
+    }
+}
+
+template <int WAVES_M, int WM, int WN>
+hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, hipStream_t s) {
+    constexpr int BM = WAVES_M * WM * 32;
+    constexpr int BN = (4 / WAVES_M) * WN * 32;
+    dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
+    if (a_vec) {
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, true, true><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, true, false><<<grid, 256, 0, s>>>(g);
+    } else {
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, false, true><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false><<<grid, 256, 0, s>>>(g);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_im2col(const float *x, int N, int C, int H, int W, int R, int S, int T, int P,
+                         int Ho, int Wo, float *col, int64_t ldc, const Decision &dec, hipStream_t s) {
+    const int rows = C * R * S;
+    const int ncols = N * Ho * Wo;
+    const int row_groups = std::min((rows + kIm2colRows - 1) / kIm2colRows, 65535);
+    dim3 grid(static_cast<unsigned>((ldc + 255) / 256), static_cast<unsigned>(row_groups));
+    im2col_kernel<<<grid, 256, 0, s>>>(x, C, H, W, R, S, T, P, Ho, Wo, ncols, col, ldc, rows, dec);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda, const float *b,
+                           int64_t ldb, float *c, int64_t ldc, int conv_hw, bool b_padded,
+                           const Decision &dec, hipStream_t s) {
+    GemmArgs g{M, Ncols, Kd, a, lda, b, ldb, c, ldc, conv_hw, dec};
+    const bool a_vec = (lda % 4 == 0) && (reinterpret_cast<uintptr_t>(a) % 16 == 0);
+    const bool b_vec = b_padded && (ldb % 4 == 0) && (reinterpret_cast<uintptr_t>(b) % 16 == 0);
+    // tile height follows M: 32 (skinny), 64, or 128 rows per workgroup
+    if (M <= 32) return launch_gemm_t<1, 1, 2>(g, a_vec, b_vec, s);   // 32 x 256
+    if (M <= 64) return launch_gemm_t<2, 1, 2>(g, a_vec, b_vec, s);   // 64 x 128
+    return launch_gemm_t<2, 2, 2>(g, a_vec, b_vec, s);                // 128 x 128
+}
+
+}  // namespace isc

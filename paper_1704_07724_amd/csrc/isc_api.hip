@@ -1,0 +1,370 @@
+// C ABI of the library (include/isc.h): argument validation on the host,
+// workspace layout, and the launch sequences of the sparse path (ISC steps
+// 1-3), the dense path (Fig. 3) and the dispatcher between them.
+#include "isc.h"
+#include "isc_internal.hpp"
+
+#include <atomic>
+#include <cmath>
+#include <cstring>
+#include <limits>
+
+namespace isc {
+bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *ctiles, int *WA, int *hx);
+}
+
+namespace {
+
+using isc::Ctrl;
+using isc::NzEntry;
+
+constexpr int64_t kI32Max = std::numeric_limits<int32_t>::max();
+constexpr size_t kAlign = 256;
+constexpr int64_t kColPad = 256;   // im2col rows padded to this many columns
+constexpr int64_t kNzTail = 64;    // spare list entries after the last plane
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+struct Shape {
+    int64_t N, C, H, W, K, R, S, T, P, Ho, Wo;
+    int64_t in_elems() const { return N * C * H * W; }
+    int64_t out_elems() const { return N * K * Ho * Wo; }
+    int64_t filt_elems() const { return K * C * R * S; }
+    int64_t crs() const { return C * R * S; }
+    int64_t ncols() const { return N * Ho * Wo; }
+    int64_t ldcol() const { return (ncols() + kColPad - 1) / kColPad * kColPad; }
+};
+
+int64_t out_extent(int64_t in, int64_t k, int64_t pad, int64_t stride) {
+    const int64_t num = in + 2 * pad - k;
+    if (num < 0) return 0;
+    return num / stride + 1;
+}
+
+int check_desc(const isc_conv_desc *d, Shape *sh) {
+    if (!d) return ISC_ERR_NULL;
+    if (d->N < 1 || d->C < 1 || d->H < 1 || d->W < 1 || d->K < 1 || d->R < 1 || d->S < 1 ||
+        d->stride < 1 || d->pad < 0)
+        return ISC_ERR_SHAPE;
+    Shape s{d->N, d->C, d->H, d->W, d->K, d->R, d->S, d->stride, d->pad, 0, 0};
+    s.Ho = out_extent(s.H, s.R, s.P, s.T);
+    s.Wo = out_extent(s.W, s.S, s.P, s.T);
+    if (s.Ho < 1 || s.Wo < 1) return ISC_ERR_SHAPE;
+    if (s.H > 65535 || s.W > 65535) return ISC_ERR_LIMIT;
+    if (s.in_elems() > kI32Max || s.out_elems() > kI32Max || s.filt_elems() > kI32Max ||
+        s.ncols() > kI32Max || s.crs() * s.ldcol() > kI32Max || s.Ho > kI32Max || s.Wo > kI32Max)
+        return ISC_ERR_LIMIT;
+    if ((s.K + 31) / 32 > 65535) return ISC_ERR_LIMIT;  // GEMM grid rows
+    *sh = s;
+    return ISC_OK;
+}
+
+bool valid_path(int32_t p) { return p == ISC_PATH_AUTO || p == ISC_PATH_SPARSE || p == ISC_PATH_DENSE; }
+
+struct Layout {
+    size_t ctrl = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, total = 0;
+    bool sparse = false, dense = false;
+};
+
+Layout layout_for(const Shape &s, int32_t path) {
+    Layout L;
+    L.sparse = path != ISC_PATH_DENSE;
+    L.dense = path != ISC_PATH_SPARSE;
+    size_t off = align_up(sizeof(Ctrl), kAlign);
+    if (L.sparse) {
+        L.row_ptr = off;
+        off = align_up(off + sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1)), kAlign);
+        L.nz = off;
+        off = align_up(off + sizeof(NzEntry) * static_cast<size_t>(s.in_elems() + kNzTail), kAlign);
+        L.wt = off;
+        off = align_up(off + sizeof(float) * static_cast<size_t>(s.filt_elems()), kAlign);
+    }
+    if (L.dense) {
+        L.col = off;
+        off = align_up(off + sizeof(float) * static_cast<size_t>(s.crs() * s.ldcol()), kAlign);
+    }
+    L.total = off;
+    return L;
+}
+
+bool aligned(const void *p, size_t a) { return reinterpret_cast<uintptr_t>(p) % a == 0; }
+
+bool overlap(const void *a, size_t an, const void *b, size_t bn) {
+    const uintptr_t x0 = reinterpret_cast<uintptr_t>(a), y0 = reinterpret_cast<uintptr_t>(b);
+    return x0 < y0 + bn && y0 < x0 + an;
+}
+
+// The current device must be a gfx950; cached per device id.
+int check_device() {
+    static std::atomic<int> state[64];  // 0 unknown, 1 gfx950, 2 other
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return ISC_ERR_DEVICE;
+    if (dev < 64) {
+        const int st = state[dev].load(std::memory_order_relaxed);
+        if (st == 1) return ISC_OK;
+        if (st == 2) return ISC_ERR_DEVICE;
+    }
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return ISC_ERR_DEVICE;
+    const bool ok = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+    if (dev < 64) state[dev].store(ok ? 1 : 2, std::memory_order_relaxed);
+    return ok ? ISC_OK : ISC_ERR_DEVICE;
+}
+
+// Largest nonzero count n with 1 - n/total >= threshold (the sparsity test of
+// the dispatcher, evaluated in double exactly as written).
+unsigned long long nnz_limit_for(int64_t total, float threshold) {
+    const double th = static_cast<double>(threshold);
+    auto sparse_enough = [&](int64_t n) {
+        return 1.0 - static_cast<double>(n) / static_cast<double>(total) >= th;
+    };
+    int64_t n = static_cast<int64_t>(std::floor((1.0 - th) * static_cast<double>(total)));
+    n = std::max<int64_t>(-1, std::min<int64_t>(n, total));
+    while (n + 1 <= total && sparse_enough(n + 1)) ++n;
+    while (n >= 0 && !sparse_enough(n)) --n;
+    if (n < 0) return ~0ull;  // unreachable for threshold <= 1: n = 0 gives sparsity 1
+    return static_cast<unsigned long long>(n);
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? ISC_OK : ISC_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char *isc_version(void) { return "isc-mi355x 0.1 (gfx950)"; }
+
+const char *isc_status_str(int status) {
+    switch (status) {
+    case ISC_OK: return "ok";
+    case ISC_ERR_NULL: return "null pointer";
+    case ISC_ERR_SHAPE: return "invalid shape";
+    case ISC_ERR_LIMIT: return "size limit exceeded";
+    case ISC_ERR_WORKSPACE: return "workspace too small";
+    case ISC_ERR_ALIAS: return "output overlaps an input or the workspace";
+    case ISC_ERR_PATH: return "invalid path";
+    case ISC_ERR_DEVICE: return "no gfx950 device";
+    case ISC_ERR_HIP: return "HIP runtime error";
+    case ISC_ERR_ALIGN: return "misaligned pointer";
+    case ISC_ERR_ARG: return "invalid argument";
+    default: return "unknown status";
+    }
+}
+
+int isc_out_shape(const isc_conv_desc *d, int32_t *Ho, int32_t *Wo) {
+    if (!d || !Ho || !Wo) return ISC_ERR_NULL;
+    if (d->H < 1 || d->W < 1 || d->R < 1 || d->S < 1 || d->stride < 1 || d->pad < 0)
+        return ISC_ERR_SHAPE;
+    const int64_t ho = out_extent(d->H, d->R, d->pad, d->stride);
+    const int64_t wo = out_extent(d->W, d->S, d->pad, d->stride);
+    if (ho < 1 || wo < 1) return ISC_ERR_SHAPE;
+    *Ho = static_cast<int32_t>(ho);
+    *Wo = static_cast<int32_t>(wo);
+    return ISC_OK;
+}
+
+int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes) {
+    if (!bytes) return ISC_ERR_NULL;
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!valid_path(path)) return ISC_ERR_PATH;
+    *bytes = layout_for(s, path).total;
+    return ISC_OK;
+}
+
+int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
+               size_t ws_bytes, int32_t path, float threshold, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !w || !y || !ws) return ISC_ERR_NULL;
+    if (!valid_path(path)) return ISC_ERR_PATH;
+    if (!(threshold >= 0.0f && threshold <= 1.0f)) return ISC_ERR_ARG;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
+    const Layout L = layout_for(s, path);
+    if (ws_bytes < L.total) return ISC_ERR_WORKSPACE;
+    const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
+    if (overlap(y, ybytes, x, sizeof(float) * static_cast<size_t>(s.in_elems())) ||
+        overlap(y, ybytes, w, sizeof(float) * static_cast<size_t>(s.filt_elems())) ||
+        overlap(y, ybytes, ws, L.total))
+        return ISC_ERR_ALIAS;
+
+    isc::SparseShape sh{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
+                        static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
+                        static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
+                        static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
+    int th, bands, tw, ct, wa, hx;
+    const bool sparse_fits = isc::sparse_tiling(sh, &th, &bands, &tw, &ct, &wa, &hx);
+    if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
+    if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
+
+    st = check_device();
+    if (st) return st;
+
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(ws);
+    Ctrl *ctrl = reinterpret_cast<Ctrl *>(base);
+    hipError_t e = hipSuccess;
+
+    if (path != ISC_PATH_DENSE) {
+        int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
+        NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
+        float *wt = reinterpret_cast<float *>(base + L.wt);
+        // prologue: clear the counter, repack the filter to K-contiguous
+        if ((e = isc::launch_zero_counter(&ctrl->nnz_total, hs)) != hipSuccess) return hip_status(e);
+        if ((e = isc::launch_repack_filter(w, sh.K, static_cast<int>(s.crs()), wt, hs)) != hipSuccess)
+            return hip_status(e);
+        // step 1
+        if ((e = isc::launch_compact(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz,
+                                     &ctrl->nnz_total, hs)) != hipSuccess)
+            return hip_status(e);
+        // steps 2-3, gated by the device-side decision in AUTO
+        isc::Decision dec{ctrl, nnz_limit_for(s.in_elems(), threshold),
+                          path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways, ctrl};
+        if ((e = isc::launch_sparse_conv(sh, row_ptr, nz, wt, y, dec, hs)) != hipSuccess)
+            return hip_status(e);
+    }
+    if (path != ISC_PATH_SPARSE) {
+        float *col = reinterpret_cast<float *>(base + L.col);
+        isc::Decision dec{ctrl, nnz_limit_for(s.in_elems(), threshold),
+                          path == ISC_PATH_AUTO ? isc::kGateIfDense : isc::kGateAlways,
+                          path == ISC_PATH_DENSE ? ctrl : nullptr};
+        if ((e = isc::launch_im2col(x, sh.N, sh.C, sh.H, sh.W, sh.R, sh.S, sh.T, sh.P, sh.Ho, sh.Wo, col,
+                                    s.ldcol(), dec, hs)) != hipSuccess)
+            return hip_status(e);
+        dec.record = nullptr;
+        if ((e = isc::launch_gemm_f32(sh.K, static_cast<int>(s.ncols()), static_cast<int>(s.crs()), w,
+                                      s.crs(), col, s.ldcol(), y, 0, sh.Ho * sh.Wo, true, dec, hs)) !=
+            hipSuccess)
+            return hip_status(e);
+    }
+    return ISC_OK;
+}
+
+int isc_decision(const isc_conv_desc *d, const void *ws, size_t ws_bytes, uint64_t *nnz_total,
+                 int32_t *path_taken, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!ws || !nnz_total || !path_taken) return ISC_ERR_NULL;
+    if (ws_bytes < sizeof(Ctrl)) return ISC_ERR_WORKSPACE;
+    st = check_device();
+    if (st) return st;
+    Ctrl c;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(&c, ws, sizeof(Ctrl), hipMemcpyDeviceToHost, hs);
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return ISC_ERR_HIP;
+    *nnz_total = c.nnz_total;
+    *path_taken = static_cast<int32_t>(c.path_taken);
+    return ISC_OK;
+}
+
+int isc_compact(const isc_conv_desc *d, const float *x, int32_t *row_ptr, isc_nz *nz,
+                uint64_t *nnz_total, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !row_ptr || !nz || !nnz_total) return ISC_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(row_ptr, 4) || !aligned(nz, 8) || !aligned(nnz_total, 8))
+        return ISC_ERR_ALIGN;
+    const size_t xb = sizeof(float) * static_cast<size_t>(s.in_elems());
+    const size_t rb = sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1));
+    const size_t nb = sizeof(isc_nz) * static_cast<size_t>(s.in_elems());
+    if (overlap(row_ptr, rb, x, xb) || overlap(nz, nb, x, xb) || overlap(nz, nb, row_ptr, rb) ||
+        overlap(nnz_total, 8, x, xb) || overlap(nnz_total, 8, row_ptr, rb) || overlap(nnz_total, 8, nz, nb))
+        return ISC_ERR_ALIAS;
+    st = check_device();
+    if (st) return st;
+    static_assert(sizeof(isc_nz) == sizeof(NzEntry), "entry layout");
+    static_assert(sizeof(unsigned long long) == sizeof(uint64_t), "counter layout");
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    unsigned long long *counter = reinterpret_cast<unsigned long long *>(nnz_total);
+    hipError_t e = isc::launch_zero_counter(counter, hs);
+    if (e == hipSuccess)
+        e = isc::launch_compact(x, static_cast<int>(s.N * s.C), static_cast<int>(s.H), static_cast<int>(s.W),
+                                row_ptr, reinterpret_cast<NzEntry *>(nz), counter, hs);
+    return hip_status(e);
+}
+
+int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!w || !wt) return ISC_ERR_NULL;
+    if (!aligned(w, 4) || !aligned(wt, 4)) return ISC_ERR_ALIGN;
+    const size_t wb = sizeof(float) * static_cast<size_t>(s.filt_elems());
+    if (overlap(w, wb, wt, wb)) return ISC_ERR_ALIAS;
+    st = check_device();
+    if (st) return st;
+    return hip_status(isc::launch_repack_filter(w, static_cast<int>(s.K), static_cast<int>(s.crs()), wt,
+                                                static_cast<hipStream_t>(stream)));
+}
+
+int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz *nz, const float *wt,
+                    float *y, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!row_ptr || !nz || !wt || !y) return ISC_ERR_NULL;
+    if (!aligned(row_ptr, 4) || !aligned(nz, 8) || !aligned(wt, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
+    const size_t yb = sizeof(float) * static_cast<size_t>(s.out_elems());
+    if (overlap(y, yb, row_ptr, sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1))) ||
+        overlap(y, yb, nz, sizeof(isc_nz) * static_cast<size_t>(s.in_elems() + kNzTail)) ||
+        overlap(y, yb, wt, sizeof(float) * static_cast<size_t>(s.filt_elems())))
+        return ISC_ERR_ALIAS;
+    isc::SparseShape sh{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
+                        static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
+                        static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
+                        static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
+    int th, bands, tw, ct, wa, hx;
+    if (!isc::sparse_tiling(sh, &th, &bands, &tw, &ct, &wa, &hx)) return ISC_ERR_LIMIT;
+    st = check_device();
+    if (st) return st;
+    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    return hip_status(isc::launch_sparse_conv(sh, row_ptr, reinterpret_cast<const NzEntry *>(nz), wt, y, dec,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+int isc_im2col(const isc_conv_desc *d, const float *x, float *col, int64_t ldc, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !col) return ISC_ERR_NULL;
+    if (ldc < s.ncols() || s.crs() * ldc > kI32Max) return ISC_ERR_ARG;
+    if (!aligned(x, 4) || !aligned(col, 4)) return ISC_ERR_ALIGN;
+    if (overlap(col, sizeof(float) * static_cast<size_t>(s.crs() * ldc), x,
+                sizeof(float) * static_cast<size_t>(s.in_elems())))
+        return ISC_ERR_ALIAS;
+    st = check_device();
+    if (st) return st;
+    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    return hip_status(isc::launch_im2col(x, static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
+                                         static_cast<int>(s.W), static_cast<int>(s.R), static_cast<int>(s.S),
+                                         static_cast<int>(s.T), static_cast<int>(s.P), static_cast<int>(s.Ho),
+                                         static_cast<int>(s.Wo), col, ldc, dec,
+                                         static_cast<hipStream_t>(stream)));
+}
+
+int isc_gemm_f32(int32_t M, int32_t Ncols, int32_t Kd, const float *a, int64_t lda, const float *b,
+                 int64_t ldb, float *c, int64_t ldc, void *stream) {
+    if (M < 1 || Ncols < 1 || Kd < 1) return ISC_ERR_SHAPE;
+    if (!a || !b || !c) return ISC_ERR_NULL;
+    if (lda < Kd || ldb < Ncols || ldc < Ncols) return ISC_ERR_SHAPE;
+    if (static_cast<int64_t>(M) * lda > kI32Max || static_cast<int64_t>(Kd) * ldb > kI32Max ||
+        static_cast<int64_t>(M) * ldc > kI32Max || (M + 31) / 32 > 65535)
+        return ISC_ERR_LIMIT;
+    if (!aligned(a, 4) || !aligned(b, 4) || !aligned(c, 4)) return ISC_ERR_ALIGN;
+    const size_t cb = sizeof(float) * static_cast<size_t>((M - 1) * ldc + Ncols);
+    if (overlap(c, cb, a, sizeof(float) * static_cast<size_t>((M - 1) * lda + Kd)) ||
+        overlap(c, cb, b, sizeof(float) * static_cast<size_t>((Kd - 1) * ldb + Ncols)))
+        return ISC_ERR_ALIAS;
+    int st = check_device();
+    if (st) return st;
+    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    return hip_status(isc::launch_gemm_f32(M, Ncols, Kd, a, lda, b, ldb, c, ldc, 0, false, dec,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

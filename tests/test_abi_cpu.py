@@ -1,0 +1,121 @@
+"""The C-ABI library on the host: it loads, exports every symbol include/isc.h
+declares, and rejects bad arguments before touching any device (these run
+without a GPU; no compute call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_1704_07724_amd as isc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "isc.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(isc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_loads_and_exports_header_symbols():
+    L = isc.lib()
+    names = header_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(isc.EXPORTS)
+    assert "gfx950" in isc.isc_version()
+
+
+def test_status_strings():
+    for code in range(0, 11):
+        assert isc.status_str(code)
+    assert isc.status_str(99) == "unknown status"
+
+
+@pytest.mark.parametrize("H,R,P,T", [(12, 5, 0, 1), (27, 5, 2, 1), (13, 3, 1, 1), (11, 5, 1, 2),
+                                     (7, 7, 3, 2), (9, 2, 0, 3), (1, 1, 0, 1), (5, 7, 1, 1)])
+def test_out_shape_matches_oracle(H, R, P, T):
+    d = isc.make_desc(1, 1, H, H + 1, 1, R, R, T, P)
+    ho_o = oracle.out_size(H, R, P, T)
+    wo_o = oracle.out_size(H + 1, R, P, T)
+    if ho_o < 1 or wo_o < 1:
+        with pytest.raises(isc.IscError) as e:
+            isc.isc_out_shape(d)
+        assert e.value.status == 2
+    else:
+        assert isc.isc_out_shape(d) == (ho_o, wo_o)
+
+
+def test_workspace_sizes_ordered():
+    d = isc.make_desc(8, 20, 12, 12, 50, 5, 5, 1, 0)
+    sp = isc.isc_workspace_size(d, "sparse")
+    de = isc.isc_workspace_size(d, "dense")
+    au = isc.isc_workspace_size(d, "auto")
+    assert sp > 0 and de > 0
+    assert au >= max(sp, de)
+    # the dense path holds the unrolled matrix: C*R*S rows of >= N*Ho*Wo floats
+    assert de >= 20 * 25 * 8 * 8 * 8 * 4
+
+
+def _conv(desc, x=0x1000, w=0x200000, y=0x400000, ws=0x800000, ws_bytes=1 << 30, path=0,
+          th=0.9):
+    return isc.lib().isc_conv2d(ctypes.byref(desc) if desc is not None else None, x, w, y, ws,
+                                ws_bytes, path, ctypes.c_float(th), None)
+
+
+def test_conv2d_validation_errors():
+    good = isc.make_desc(2, 3, 8, 8, 4, 3, 3, 1, 1)
+    assert _conv(None) == 1                                    # NULL desc
+    assert _conv(good, x=0) == 1                               # NULL input
+    assert _conv(isc.make_desc(0, 3, 8, 8, 4, 3, 3, 1, 1)) == 2
+    assert _conv(isc.make_desc(2, 3, 8, 8, 4, 3, 3, 0, 1)) == 2  # stride 0
+    assert _conv(isc.make_desc(2, 3, 8, 8, 4, 3, 3, 1, -1)) == 2
+    assert _conv(isc.make_desc(2, 3, 2, 2, 4, 5, 5, 1, 0)) == 2  # filter larger than input
+    assert _conv(isc.make_desc(1, 1, 70000, 1, 1, 1, 1, 1, 0)) == 3   # H > 65535
+    assert _conv(isc.make_desc(4096, 512, 64, 64, 1, 1, 1, 1, 0)) == 3  # > 2^31 elements
+    assert _conv(good, path=7) == 6
+    assert _conv(good, th=1.5) == 10
+    assert _conv(good, th=float("nan")) == 10
+    assert _conv(good, x=0x1002) == 9                          # misaligned
+    assert _conv(good, ws=0x800010) == 9                       # workspace not 256-aligned
+    assert _conv(good, ws_bytes=16) == 4
+    assert _conv(good, y=0x1000) == 5                          # y overlaps x
+    assert _conv(good, y=0x800000) == 5                        # y overlaps the workspace
+
+
+def test_conv2d_without_device_reports_device():
+    # arguments valid, no GPU in this process -> ISC_ERR_DEVICE, nothing launched
+    try:
+        import torch
+        if torch.cuda.is_available():
+            pytest.skip("a GPU is present")
+    except Exception:
+        pass
+    good = isc.make_desc(2, 3, 8, 8, 4, 3, 3, 1, 1)
+    assert _conv(good) == 7
+
+
+def test_compact_im2col_gemm_validation():
+    L = isc.lib()
+    d = isc.make_desc(2, 3, 8, 8, 1, 1, 1, 1, 0)
+    assert L.isc_compact(ctypes.byref(d), 0, 0x1000, 0x2000, 0x3000, None) == 1
+    assert L.isc_compact(ctypes.byref(d), 0x100000, 0x100000, 0x200000, 0x300000, None) == 5
+    assert L.isc_compact(ctypes.byref(d), 0x100000, 0x200000, 0x300004, 0x400000, None) == 9
+    assert L.isc_im2col(ctypes.byref(d), 0x100000, 0x200000, 10, None) == 10  # ldc < N*Ho*Wo
+    assert L.isc_im2col(ctypes.byref(d), 0x100000, 0x100000, 128, None) == 5
+    assert L.isc_gemm_f32(0, 4, 4, 0x1000, 4, 0x2000, 4, 0x3000, 4, None) == 2
+    assert L.isc_gemm_f32(4, 4, 4, 0x1000, 3, 0x2000, 4, 0x3000, 4, None) == 2  # lda < Kd
+    assert L.isc_gemm_f32(4, 4, 4, 0x1000, 4, 0x2000, 4, 0x1000, 4, None) == 5  # c overlaps a
+
+
+def test_dispatch_threshold_reading():
+    # the AUTO decision is "sparsity = 1 - nnz/total >= threshold"; the
+    # default threshold follows the abstract's "not less than 0.9"
+    import inspect
+    sig = inspect.signature(isc.isc_conv2d)
+    assert sig.parameters["threshold"].default == 0.9
+    assert sig.parameters["path"].default == "auto"

@@ -1,0 +1,381 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars:
+  - compaction (ISC step 1) and im2col: bit-exact;
+  - convolution outputs (sparse and dense paths): elementwise
+    |gpu - oracle| <= 1e-4 * (1 + |oracle|);
+  - integer-valued inputs: every fp32 partial sum is exact, so both paths
+    must equal the oracle bitwise;
+  - the dispatcher's choice is the sparsity test 1 - nnz/total >= threshold
+    evaluated in double, the same as here.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available()
+    return t
+
+
+@pytest.fixture(scope="module")
+def isc(torch):
+    import paper_1704_07724_amd as m
+    m.lib()  # raises if the library is not built
+    return m
+
+
+def note(*parts):
+    print("[case]", *parts, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def assert_conv_close(got, want, what):
+    got = got.astype(np.float64)
+    err = np.abs(got - want)
+    bound = TOL * (1.0 + np.abs(want))
+    bad = err > bound
+    if bad.any():
+        i = np.flatnonzero(bad.ravel())[0]
+        raise AssertionError("%s: %d of %d outputs out of tolerance; first at flat %d: gpu %r "
+                             "oracle %r" % (what, int(bad.sum()), bad.size, i, got.ravel()[i],
+                                            want.ravel()[i]))
+
+
+# ------------------------------------------------------------- compaction --
+
+COMPACT_SHAPES = [
+    (1, 1, 1, 1), (2, 3, 5, 7), (3, 4, 12, 12), (2, 5, 27, 27), (1, 3, 13, 13),
+    (2, 2, 28, 28), (1, 2, 3, 100), (1, 2, 100, 3), (1, 1, 40, 70), (4, 1, 1, 65),
+]
+
+
+@pytest.mark.parametrize("shape", COMPACT_SHAPES)
+@pytest.mark.parametrize("sparsity", [0.0, 0.5, 0.9, 1.0])
+def test_compact_bitexact(torch, isc, shape, sparsity):
+    note("compact", shape, sparsity)
+    rng = np.random.default_rng(hash((shape, sparsity)) & 0xFFFF)
+    x = np.abs(rng.standard_normal(shape)).astype(np.float32) + np.float32(0.5)
+    x[rng.random(shape) < sparsity] = 0.0
+    _check_compact(torch, isc, x)
+
+
+def test_compact_special_values(torch, isc):
+    rng = np.random.default_rng(5)
+    x = np.abs(rng.standard_normal((2, 3, 9, 11))).astype(np.float32)
+    x[rng.random(x.shape) < 0.6] = 0.0
+    x[0, 0, 0, 0] = -0.0
+    x[0, 1, 2, 3] = np.float32(1e-45)
+    x[1, 0, 4, 4] = -np.float32(1e-40)
+    x[1, 1, 8, 10] = np.inf
+    x[1, 2, 5, 0] = np.nan
+    x[0, 2, 3, 3] = -2.5
+    note("compact special values")
+    _check_compact(torch, isc, x)
+
+
+def _check_compact(torch, isc, x):
+    N, C, H, W = x.shape
+    row_ptr, nz, total = isc.isc_compact(to_dev(torch, x))
+    torch.cuda.synchronize()
+    rp_o, v_o, ys_o, xs_o, tot_o = oracle.compact(x)
+    assert int(total.item()) == tot_o
+    assert np.array_equal(row_ptr.cpu().numpy(), rp_o)
+    ent = nz.cpu().numpy().reshape(N * C, H * W, 2)
+    for p in range(N * C):
+        cnt = rp_o[p, H]
+        assert np.array_equal(ent[p, :cnt, 0].view(np.uint32), v_o[p, :cnt].view(np.uint32))
+        yx = ent[p, :cnt, 1].view(np.uint32)
+        assert np.array_equal(yx >> 16, ys_o[p, :cnt].astype(np.uint32))
+        assert np.array_equal(yx & 0xFFFF, xs_o[p, :cnt].astype(np.uint32))
+
+
+# ----------------------------------------------------------------- im2col --
+
+@pytest.mark.parametrize("case", [
+    (2, 3, 8, 7, 3, 3, 1, 1), (1, 4, 12, 12, 5, 5, 1, 0), (2, 2, 11, 11, 5, 5, 2, 1),
+    (1, 3, 9, 10, 2, 3, 3, 2), (3, 2, 6, 6, 1, 1, 1, 0), (1, 1, 13, 13, 3, 3, 1, 1),
+])
+def test_im2col_bitexact(torch, isc, case):
+    N, C, H, W, R, S, T, P = case
+    note("im2col", case)
+    rng = np.random.default_rng(sum(case))
+    x = rng.standard_normal((N, C, H, W)).astype(np.float32)
+    x[rng.random(x.shape) < 0.3] = 0.0
+    x[0, 0, 0, 0] = -0.0
+    ho, wo = oracle.out_size(H, R, P, T), oracle.out_size(W, S, P, T)
+    ldc = N * ho * wo + 37
+    col = isc.isc_im2col(to_dev(torch, x), R, S, T, P, ldc=ldc).cpu().numpy()
+    want = oracle.im2col(x, R, S, T, P, ldc=ldc)
+    assert np.array_equal(col.view(np.uint32), want.view(np.uint32))
+
+
+# ------------------------------------------------------------------- GEMM --
+
+@pytest.mark.parametrize("mnk", [(1, 1, 1), (50, 512, 500), (32, 300, 17), (64, 257, 64),
+                                 (128, 1000, 33), (200, 130, 2400), (384, 256, 3)])
+def test_gemm_against_fp64(torch, isc, mnk):
+    M, N, Kd = mnk
+    note("gemm", mnk)
+    rng = np.random.default_rng(M * 7 + N * 3 + Kd)
+    a = rng.standard_normal((M, Kd)).astype(np.float32)
+    b = rng.standard_normal((Kd, N)).astype(np.float32)
+    c = isc.isc_gemm_f32(to_dev(torch, a), to_dev(torch, b)).cpu().numpy().astype(np.float64)
+    want = a.astype(np.float64) @ b.astype(np.float64)
+    # any order of fp32 sums of Kd products: |error| <= gamma_Kd * sum |a||b|,
+    # gamma_n = n u / (1 - n u), u = 2^-24 (+1 for the product rounding)
+    u = 2.0 ** -24
+    gamma = (Kd + 1) * u / (1 - (Kd + 1) * u)
+    bound = gamma * (np.abs(a.astype(np.float64)) @ np.abs(b.astype(np.float64)))
+    assert np.all(np.abs(c - want) <= bound), mnk
+
+
+# ------------------------------------------------------------ convolution --
+
+CONV_CASES = [
+    # N, C, H, W, K, R, S, T, P, sparsity
+    (2, 5, 12, 12, 50, 5, 5, 1, 0, 0.9),      # LeNet-like, K < 64
+    (2, 8, 27, 27, 70, 5, 5, 1, 2, 0.9),      # AlexNet conv2-like, ragged k-block
+    (2, 16, 13, 13, 130, 3, 3, 1, 1, 0.95),   # conv3-5-like
+    (2, 6, 28, 28, 64, 3, 3, 1, 1, 0.9),      # inception 3x3-like
+    (1, 4, 28, 28, 32, 5, 5, 1, 2, 0.9),      # inception 5x5-like
+    (2, 7, 14, 14, 40, 1, 1, 1, 0, 0.9),      # 1x1
+    (1, 3, 17, 15, 20, 7, 7, 1, 3, 0.8),      # 7x7
+    (2, 4, 11, 11, 64, 5, 5, 2, 1, 0.95),     # the paper's LeNet-Conv2 shape (T = 2)
+    (1, 3, 10, 9, 9, 2, 3, 1, 1, 0.5),        # generic R x S
+    (1, 2, 9, 9, 5, 3, 3, 3, 2, 0.7),         # stride 3
+    (1, 3, 20, 200, 66, 3, 3, 1, 1, 0.9),     # wide: several column tiles
+    (2, 3, 7, 7, 10, 5, 5, 1, 4, 0.6),        # pad larger than filter - 1
+    (1, 1, 1, 1, 1, 1, 1, 1, 0, 0.0),         # smallest
+    (3, 2, 6, 6, 3, 6, 6, 1, 0, 0.5),         # filter covers the map (Ho = 1), generic
+]
+
+
+@pytest.mark.parametrize("path", ["sparse", "dense", "auto"])
+@pytest.mark.parametrize("case", CONV_CASES)
+def test_conv_matches_oracle(torch, isc, case, path):
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("conv", path, case)
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=abs(hash(case)) % 10000)
+    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), T, P, path=path).cpu().numpy()
+    want = oracle.conv2d_f64(x, w, T, P)
+    assert y.shape == want.shape
+    assert_conv_close(y, want, "%s %s" % (path, case))
+
+
+@pytest.mark.parametrize("path", ["sparse", "dense"])
+@pytest.mark.parametrize("case", [(2, 6, 12, 12, 50, 5, 5, 1, 0), (2, 16, 13, 13, 130, 3, 3, 1, 1),
+                                  (1, 5, 11, 11, 20, 5, 5, 2, 1), (2, 3, 9, 9, 7, 2, 4, 1, 1)])
+def test_conv_integer_inputs_bitwise(torch, isc, case, path):
+    N, C, H, W, K, R, S, T, P = case
+    note("conv integer", path, case)
+    x, w = workloads.integer_case(N, C, H, W, K, R, S, seed=sum(case))
+    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), T, P, path=path).cpu().numpy()
+    want = oracle.conv2d_f64(x, w, T, P)
+    assert np.array_equal(y.astype(np.float64), want)
+
+
+@pytest.mark.parametrize("path", ["sparse", "dense", "auto"])
+def test_conv_zero_input_exact_zero(torch, isc, path):
+    note("conv zero input", path)
+    x = torch.zeros((2, 8, 13, 13), device="cuda")
+    w = torch.randn((40, 8, 3, 3), device="cuda")
+    y = isc.isc_conv2d(x, w, 1, 1, path=path)
+    assert bool((y == 0).all())
+
+
+def test_sparse_run_to_run_bitwise(torch, isc):
+    note("determinism")
+    x, w = workloads.make_case(2, 8, 27, 27, 70, 5, 5, 1, 2, 0.9, seed=11)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    a = isc.isc_conv2d(xd, wd, 1, 2, path="sparse").cpu().numpy()
+    b = isc.isc_conv2d(xd, wd, 1, 2, path="sparse").cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_output_redzone_untouched(torch, isc):
+    note("redzone")
+    x, w = workloads.make_case(2, 4, 12, 12, 50, 5, 5, 1, 0, 0.9, seed=12)
+    n_out = 2 * 50 * 8 * 8
+    for path in ("sparse", "dense", "auto"):
+        buf = torch.full((n_out + 2048,), 1234.5, device="cuda")
+        out = buf[1024:1024 + n_out].view(2, 50, 8, 8)
+        isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path=path, out=out)
+        b = buf.cpu().numpy()
+        assert np.all(b[:1024] == 1234.5) and np.all(b[1024 + n_out:] == 1234.5), path
+
+
+# ------------------------------------------------------------- dispatcher --
+
+def oracle_choice(x, threshold):
+    total = x.size
+    nnz = oracle.compact(x)[4]
+    return ("sparse" if 1.0 - nnz / total >= float(np.float32(threshold)) else "dense"), nnz
+
+
+@pytest.mark.parametrize("sparsity", [0.5, 0.85, 0.9, 0.95, 0.99])
+def test_auto_dispatch_choice(torch, isc, sparsity):
+    note("dispatch", sparsity)
+    x, w = workloads.make_case(4, 10, 12, 12, 50, 5, 5, 1, 0, sparsity, seed=int(sparsity * 100))
+    desc = isc.make_desc(4, 10, 12, 12, 50, 5, 5, 1, 0)
+    ws = isc.workspace(desc, "auto")
+    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path="auto", ws=ws)
+    nnz, taken = isc.isc_decision(desc, ws)
+    want_path, want_nnz = oracle_choice(x, 0.9)
+    assert nnz == want_nnz
+    assert taken == want_path
+    assert_conv_close(y.cpu().numpy(), oracle.conv2d_f64(x, w, 1, 0), "auto %g" % sparsity)
+
+
+def test_dispatch_threshold_boundary(torch, isc):
+    # exactly at the threshold the sparse path is taken; one more nonzero
+    # flips it to dense
+    note("dispatch boundary")
+    N, C, H, W = 1, 4, 10, 10   # 400 inputs: sparsity 0.9 <=> 40 nonzeros
+    rng = np.random.default_rng(3)
+    w = rng.standard_normal((8, C, 3, 3)).astype(np.float32)
+    desc = isc.make_desc(N, C, H, W, 8, 3, 3, 1, 1)
+    for nnz, want in ((40, "sparse"), (41, "dense")):
+        x = np.zeros((N, C, H, W), np.float32)
+        idx = rng.choice(x.size, nnz, replace=False)
+        x.ravel()[idx] = 1.0 + rng.random(nnz).astype(np.float32)
+        assert oracle_choice(x, 0.9)[0] == want
+        ws = isc.workspace(desc, "auto")
+        y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 1, path="auto", threshold=0.9, ws=ws)
+        got_nnz, taken = isc.isc_decision(desc, ws)
+        assert (got_nnz, taken) == (nnz, want)
+        assert_conv_close(y.cpu().numpy(), oracle.conv2d_f64(x, w, 1, 1), "boundary %d" % nnz)
+
+
+def test_forced_paths_record_decision(torch, isc):
+    note("forced path record")
+    x, w = workloads.make_case(2, 4, 12, 12, 50, 5, 5, 1, 0, 0.5, seed=4)
+    desc = isc.make_desc(2, 4, 12, 12, 50, 5, 5, 1, 0)
+    ws = isc.workspace(desc, "sparse")
+    isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path="sparse", ws=ws)
+    nnz, taken = isc.isc_decision(desc, ws)
+    assert taken == "sparse" and nnz == oracle.compact(x)[4]
+    ws = isc.workspace(desc, "dense")
+    isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path="dense", ws=ws)
+    nnz, taken = isc.isc_decision(desc, ws)
+    assert taken == "dense" and nnz == 2 ** 64 - 1
+
+
+def test_gpu_error_codes(torch, isc):
+    note("error codes")
+    x = torch.zeros((1, 3, 8, 8), device="cuda")
+    w = torch.zeros((3, 3, 3, 3), device="cuda")
+    with pytest.raises(isc.IscError) as e:
+        isc.isc_conv2d(x, w, 1, 1, ws=torch.empty(16, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == 4
+    with pytest.raises(isc.IscError) as e:
+        isc.isc_conv2d(x, w, 1, 1, out=x)          # output overlaps the input
+    assert e.value.status == 5
+    with pytest.raises(KeyError):
+        isc.isc_conv2d(x, w, 1, 1, path="sideways")
+
+
+@pytest.mark.parametrize("path", ["auto", "sparse", "dense"])
+def test_graph_replay_matches_eager(torch, isc, path):
+    """isc_conv2d captured into a HIP graph: every replay, with eager work
+    in between, equals the eager result bitwise."""
+    note("graph replay", path)
+    x, w = workloads.make_case(3, 6, 13, 13, 70, 3, 3, 1, 1, 0.9, seed=21)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    desc = isc.make_desc(3, 6, 13, 13, 70, 3, 3, 1, 1)
+    eager = isc.isc_conv2d(xd, wd, 1, 1, path=path).clone()
+    y = torch.empty_like(eager)
+    ws = isc.workspace(desc, path)
+    fn = lambda: isc.isc_conv2d(xd, wd, 1, 1, path=path, out=y, ws=ws)  # noqa: E731
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fn()
+    other_x, other_w = workloads.make_case(2, 6, 13, 13, 70, 3, 3, 1, 1, 0.5, seed=22)
+    for _ in range(3):
+        y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager)
+        isc.isc_conv2d(to_dev(torch, other_x), to_dev(torch, other_w), 1, 1, path=path)
+        torch.cuda.synchronize()
+    assert_conv_close(eager.cpu().numpy(), oracle.conv2d_f64(x, w, 1, 1), "graph %s" % path)
+
+
+def test_sparse_conv_entry_from_lists(torch, isc):
+    """isc_compact + isc_repack_filter + isc_sparse_conv, one compaction
+    shared by two convolutions of the same input (inception-style)."""
+    note("sparse conv from shared lists")
+    x, _ = workloads.make_case(2, 8, 28, 28, 1, 1, 1, 1, 0, 0.9, seed=31)
+    rng = np.random.default_rng(32)
+    w3 = (rng.standard_normal((40, 8, 3, 3)) * 0.1).astype(np.float32)
+    w5 = (rng.standard_normal((20, 8, 5, 5)) * 0.1).astype(np.float32)
+    xd = to_dev(torch, x)
+    lists = isc.isc_compact(xd)
+    for w, P in ((w3, 1), (w5, 2)):
+        wt = isc.isc_repack_filter(to_dev(torch, w))
+        want_wt = np.ascontiguousarray(w.transpose(1, 2, 3, 0))
+        assert np.array_equal(wt.cpu().numpy(), want_wt)
+        y = isc.isc_sparse_conv(xd.shape, lists, wt, 1, P).cpu().numpy()
+        assert_conv_close(y, oracle.conv2d_f64(x, w, 1, P), "lists P=%d" % P)
+
+
+# ----------------------------------------------- full-size configurations --
+
+def full_layers():
+    for wl in workloads.WORKLOADS.values():
+        for layer in wl.layers:
+            if wl.name == "lenet_conv2_batch" and layer.sparsity not in (0.5, 0.9, 0.99):
+                continue
+            yield pytest.param(layer, id=layer.name)
+
+
+@pytest.mark.parametrize("layer", list(full_layers()))
+def test_full_size_sampled(torch, isc, layer):
+    """Workload shapes at full size, in the launch configuration the benchmark
+    times: compaction bit-exact in full, convolution outputs checked at
+    sampled positions against the oracle evaluated point by point."""
+    note("full", layer.name, layer.x_shape, layer.w_shape)
+    x, w = workloads.make_inputs(layer)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    T, P = layer.T, layer.P
+    # compaction: totals and a bit-exact comparison on a sample of planes
+    row_ptr, nz, total = isc.isc_compact(xd)
+    rp_o, v_o, ys_o, xs_o, tot_o = oracle.compact(x)
+    assert int(total.item()) == tot_o
+    assert np.array_equal(row_ptr.cpu().numpy(), rp_o)
+    ent = nz.cpu().numpy()
+    rng = np.random.default_rng(layer.seed)
+    H = layer.H
+    for p in rng.choice(ent.shape[0], size=min(256, ent.shape[0]), replace=False):
+        cnt = rp_o[p, H]
+        assert np.array_equal(ent[p, :cnt, 0].view(np.uint32), v_o[p, :cnt].view(np.uint32))
+        yx = ent[p, :cnt, 1].view(np.uint32)
+        assert np.array_equal(yx >> 16, ys_o[p, :cnt].astype(np.uint32))
+        assert np.array_equal(yx & 0xFFFF, xs_o[p, :cnt].astype(np.uint32))
+    del row_ptr, nz, ent
+    for path in ("sparse", "dense", "auto"):
+        y = isc.isc_conv2d(xd, wd, T, P, path=path)
+        flat = y.view(-1)
+        idx = rng.choice(flat.numel(), size=1500, replace=False)
+        got = flat[torch.from_numpy(idx).cuda()].cpu().numpy()
+        want = oracle.conv2d_f64_at(x, w, T, P, idx)
+        assert_conv_close(got, want, "%s %s" % (layer.name, path))
+        del y
+    torch.cuda.empty_cache()
