@@ -138,11 +138,18 @@ int isc_decision(const isc_conv_desc *d, const void *ws, size_t ws_bytes,
 int isc_compact(const isc_conv_desc *d, const float *x, int32_t *row_ptr,
                 isc_nz *nz, uint64_t *nnz_total, void *stream);
 
+/* Bytes isc_repack_filter writes for this descriptor (K, C, R, S used).
+ * Host-only.  Errors: NULL, SHAPE, LIMIT. */
+int isc_repacked_filter_size(const isc_conv_desc *d, size_t *bytes);
+
 /* ISC step 2's filter layout (Sec. "Sparse Convolution": the kernel matrix
- * stored so that, for one input channel and tap, the weights of consecutive
- * output maps are contiguous):
- *   wt[((c*R + r)*S + s)*K + k] = w[k, c, r, s]
- *   w: device K x C x R x S; wt: device float[K*C*R*S], must not overlap w.
+ * stored column-major, so that for one input channel and tap the weights of
+ * consecutive output maps are contiguous and can be fetched together), with
+ * the output-map dimension zero padded to a multiple of 64:
+ *   wt[((c*R + r)*S + s)*Kp + k] = w[k, c, r, s],  Kp = ceil(K/64)*64,
+ *   0 for K <= k < Kp.
+ *   w: device K x C x R x S; wt: device buffer of isc_repacked_filter_size
+ *   bytes, 16-byte aligned, must not overlap w.
  * Only K, C, R, S of d are used (all must be valid).  Errors: NULL, SHAPE,
  * LIMIT, ALIAS, ALIGN, DEVICE, HIP. */
 int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *stream);
@@ -154,7 +161,7 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
  *   row_ptr, nz: as written by isc_compact for N, C, H, W of d (read only;
  *     nz must have 64 readable entries past N*C*H*W -- isc_conv2d's
  *     workspace does; a caller's own buffer of N*C*H*W + 64 entries does).
- *   wt: the repacked filter of isc_repack_filter.
+ *   wt: the repacked filter of isc_repack_filter (16-byte aligned).
  *   y: device output N x K x Ho x Wo, fully written, must not overlap the
  *     inputs.
  * One launch, no workspace, deterministic (each output is summed by one

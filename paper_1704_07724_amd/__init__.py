@@ -27,8 +27,8 @@ STATUS = {
     8: "ISC_ERR_HIP", 9: "ISC_ERR_ALIGN", 10: "ISC_ERR_ARG",
 }
 EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
-           "isc_compact", "isc_repack_filter", "isc_sparse_conv", "isc_im2col", "isc_gemm_f32",
-           "isc_status_str", "isc_version")
+           "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
+           "isc_im2col", "isc_gemm_f32", "isc_status_str", "isc_version")
 
 
 class IscError(RuntimeError):
@@ -65,11 +65,12 @@ def lib():
     L.isc_conv2d.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, vp]
     L.isc_decision.argtypes = [dp, vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(i32), vp]
     L.isc_compact.argtypes = [dp, vp, vp, vp, vp, vp]
+    L.isc_repacked_filter_size.argtypes = [dp, ctypes.POINTER(sz)]
     L.isc_repack_filter.argtypes = [dp, vp, vp, vp]
     L.isc_sparse_conv.argtypes = [dp, vp, vp, vp, vp, vp]
     L.isc_im2col.argtypes = [dp, vp, vp, i64, vp]
     L.isc_gemm_f32.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
-    for name in EXPORTS[:9]:
+    for name in EXPORTS[:10]:
         getattr(L, name).restype = ctypes.c_int
     L.isc_status_str.argtypes = [ctypes.c_int]
     L.isc_status_str.restype = ctypes.c_char_p
@@ -219,34 +220,53 @@ def isc_compact(x, stream=None, out=None):
     return row_ptr, nz, total
 
 
+def isc_repacked_filter_size(desc: ConvDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().isc_repacked_filter_size(ctypes.byref(desc), ctypes.byref(n)),
+           "isc_repacked_filter_size")
+    return n.value
+
+
+class RepackedFilter:
+    """ISC step 2's blocked K-contiguous filter (see isc_repack_filter)."""
+
+    def __init__(self, data, K, C, R, S):
+        self.data, self.K, self.C, self.R, self.S = data, K, C, R, S
+
+    def dense(self):
+        """[C, R, S, Kp] view of the buffer (Kp = K rounded up to 64)."""
+        kp = (self.K + 63) // 64 * 64
+        return self.data.view(self.C, self.R, self.S, kp)
+
+
 def isc_repack_filter(w, out=None, stream=None):
-    """ISC step 2's filter layout: wt [C, R, S, K] with K contiguous."""
+    """ISC step 2's filter layout for w [K, C, R, S] (a RepackedFilter)."""
     torch = _torch()
     w = _dev_f32(w, "w")
     K, C, R, S = (int(v) for v in w.shape)
-    desc = make_desc(1, C, max(R, 1), max(S, 1), K, R, S, 1, 0)
-    if out is None:
-        out = torch.empty((C, R, S, K), dtype=torch.float32, device=w.device)
-    _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), out.data_ptr(),
+    desc = make_desc(1, C, R, S, K, R, S, 1, 0)
+    n = isc_repacked_filter_size(desc) // 4
+    data = out if out is not None else torch.empty(n, dtype=torch.float32, device=w.device)
+    _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), data.data_ptr(),
                                    _stream(stream)), "isc_repack_filter")
-    return out
+    return RepackedFilter(data, K, C, R, S)
 
 
 def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):
     """ISC steps 2-3 from compacted lists (isc_compact's (row_ptr, entries,
-    ...)) and a repacked filter wt [C, R, S, K]; returns y [N, K, Ho, Wo]."""
+    ...)) and a RepackedFilter; returns y [N, K, Ho, Wo]."""
     torch = _torch()
     N, C, H, W = (int(v) for v in x_shape)
-    C2, R, S, K = (int(v) for v in wt.shape)
-    if C != C2:
+    K, R, S = wt.K, wt.R, wt.S
+    if C != wt.C:
         raise ValueError("channel mismatch")
     row_ptr, nz = lists[0], lists[1]
     desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
     ho, wo = isc_out_shape(desc)
     if out is None:
-        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=wt.device)
+        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=wt.data.device)
     _check(lib().isc_sparse_conv(ctypes.byref(desc), row_ptr.data_ptr(), nz.data_ptr(),
-                                 wt.data_ptr(), out.data_ptr(), _stream(stream)),
+                                 wt.data.data_ptr(), out.data_ptr(), _stream(stream)),
            "isc_sparse_conv")
     return out
 

@@ -37,9 +37,23 @@ DEVICE_FLAGS = [
 ]
 
 
+# Per-file extra flags.  sparse_reg.hip keeps accumulator tiles in registers
+# through a compile-time dispatch tree on a wave-uniform value:
+#  - SimplifyCFG's sinking of the common tails of the tree's leaves turns
+#    constant register indices into selected pointers and forces the tile to
+#    scratch memory, so sinking is disabled;
+#  - every branch of the tree is uniform, so the CFG structurizer is told to
+#    leave uniform regions alone (otherwise its flow blocks add scalar work
+#    per level and break the in-place accumulate into copy chains).
+FILE_FLAGS = {
+    "sparse_reg.hip": ["-mllvm", "-simplifycfg-sink-common=false",
+                       "-mllvm", "-structurizecfg-skip-uniform-regions"],
+}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + DEVICE_FLAGS + ["-c", src, "-o", obj]
+    cmd = [HIPCC] + DEVICE_FLAGS + FILE_FLAGS.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr))

@@ -9,7 +9,8 @@
 // the first element of a row writes that row's offset.  The per-plane lists
 // are dense in fixed H*W slots, so the output is unique and needs no second
 // pass.  Traffic: 4 bytes read per input element, 8 bytes written per
-// nonzero, 4 bytes per row offset.
+// nonzero, 4 bytes per row offset.  A second, one-workgroup kernel adds the
+// per-plane counts into the total the dispatcher reads.
 #include "isc_internal.hpp"
 
 namespace isc {
@@ -23,16 +24,9 @@ __device__ __forceinline__ uint32_t lanes_below(unsigned long long mask) {
                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-__global__ __launch_bounds__(64)
-void zero_counter_kernel(unsigned long long *counter) {
-    if (threadIdx.x == 0) *counter = 0ull;
-}
-
 __global__ __launch_bounds__(kWaves * 64)
 void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
-                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz,
-                    unsigned long long *__restrict__ counter) {
-    __shared__ uint32_t wave_sum[kWaves];
+                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz) {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int HW = H * W;
@@ -43,7 +37,6 @@ void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
     const int dy = 64 / W;
     const int dx = 64 - dy * W;
 
-    uint32_t counted = 0;  // nonzeros in the planes this wave handled
     for (int p = blockIdx.x * kWaves + wave; p < planes; p += gridDim.x * kWaves) {
         const float *xp = x + static_cast<size_t>(p) * HW;
         NzEntry *np = nz + static_cast<size_t>(p) * HW;
@@ -82,31 +75,41 @@ void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
             }
         }
         if (lane == 0) rp[H] = static_cast<int32_t>(base);
-        counted += base;
     }
-    if (lane == 0) wave_sum[wave] = counted;
+}
+
+// Total of the per-plane counts (row_ptr[p][H]) by one workgroup, written
+// to *total with a plain store: no counter to clear, no same-address atomics.
+constexpr int kCountThreads = 1024;
+
+__global__ __launch_bounds__(kCountThreads)
+void count_kernel(const int32_t *__restrict__ row_ptr, int planes, int H,
+                  unsigned long long *__restrict__ total) {
+    __shared__ unsigned long long part[kCountThreads / 64];
+    unsigned long long s = 0;
+    for (int p = threadIdx.x; p < planes; p += kCountThreads)
+        s += static_cast<uint32_t>(row_ptr[static_cast<size_t>(p) * (H + 1) + H]);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned long long s = 0;
+        unsigned long long t = 0;
 #pragma unroll
-        for (int i = 0; i < kWaves; ++i) s += wave_sum[i];
-        if (s) atomicAdd(counter, s);
+        for (int i = 0; i < kCountThreads / 64; ++i) t += part[i];
+        *total = t;
     }
 }
 
 }  // namespace
 
-hipError_t launch_zero_counter(unsigned long long *counter, hipStream_t s) {
-    zero_counter_kernel<<<1, 64, 0, s>>>(counter);
-    return hipGetLastError();
-}
-
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s) {
-    // enough workgroups to fill 256 CUs several times over, one atomic each
+    // one wavefront per plane; enough workgroups to cover 256 CUs many times
     int groups = (planes + kWaves - 1) / kWaves;
-    if (groups > 2048) groups = 2048;
-    compact_kernel<<<groups, kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz, counter);
+    if (groups > 8192) groups = 8192;
+    compact_kernel<<<groups, kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz);
+    count_kernel<<<1, kCountThreads, 0, s>>>(row_ptr, planes, H, counter);
     return hipGetLastError();
 }
 

@@ -10,7 +10,7 @@
 #include <limits>
 
 namespace isc {
-bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *ctiles, int *WA, int *hx);
+bool sparse_conv_feasible(const SparseShape &sh);
 }
 
 namespace {
@@ -77,7 +77,9 @@ Layout layout_for(const Shape &s, int32_t path) {
         L.nz = off;
         off = align_up(off + sizeof(NzEntry) * static_cast<size_t>(s.in_elems() + kNzTail), kAlign);
         L.wt = off;
-        off = align_up(off + sizeof(float) * static_cast<size_t>(s.filt_elems()), kAlign);
+        off = align_up(off + sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
+                                                                         static_cast<int>(s.R), static_cast<int>(s.S)),
+                       kAlign);
     }
     if (L.dense) {
         L.col = off;
@@ -194,8 +196,7 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
                         static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
                         static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
                         static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
-    int th, bands, tw, ct, wa, hx;
-    const bool sparse_fits = isc::sparse_tiling(sh, &th, &bands, &tw, &ct, &wa, &hx);
+    const bool sparse_fits = isc::sparse_conv_feasible(sh);
     if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
     if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
 
@@ -211,9 +212,8 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
         int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
         NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
         float *wt = reinterpret_cast<float *>(base + L.wt);
-        // prologue: clear the counter, repack the filter to K-contiguous
-        if ((e = isc::launch_zero_counter(&ctrl->nnz_total, hs)) != hipSuccess) return hip_status(e);
-        if ((e = isc::launch_repack_filter(w, sh.K, static_cast<int>(s.crs()), wt, hs)) != hipSuccess)
+        // prologue: repack the filter to K-contiguous
+        if ((e = isc::launch_repack_filter(w, sh.K, sh.C, sh.R, sh.S, wt, hs)) != hipSuccess)
             return hip_status(e);
         // step 1
         if ((e = isc::launch_compact(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz,
@@ -281,11 +281,19 @@ int isc_compact(const isc_conv_desc *d, const float *x, int32_t *row_ptr, isc_nz
     static_assert(sizeof(unsigned long long) == sizeof(uint64_t), "counter layout");
     hipStream_t hs = static_cast<hipStream_t>(stream);
     unsigned long long *counter = reinterpret_cast<unsigned long long *>(nnz_total);
-    hipError_t e = isc::launch_zero_counter(counter, hs);
-    if (e == hipSuccess)
-        e = isc::launch_compact(x, static_cast<int>(s.N * s.C), static_cast<int>(s.H), static_cast<int>(s.W),
+    hipError_t e = isc::launch_compact(x, static_cast<int>(s.N * s.C), static_cast<int>(s.H), static_cast<int>(s.W),
                                 row_ptr, reinterpret_cast<NzEntry *>(nz), counter, hs);
     return hip_status(e);
+}
+
+int isc_repacked_filter_size(const isc_conv_desc *d, size_t *bytes) {
+    if (!bytes) return ISC_ERR_NULL;
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    *bytes = sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
+                                                         static_cast<int>(s.R), static_cast<int>(s.S));
+    return ISC_OK;
 }
 
 int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *stream) {
@@ -293,12 +301,16 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
     int st = check_desc(d, &s);
     if (st) return st;
     if (!w || !wt) return ISC_ERR_NULL;
-    if (!aligned(w, 4) || !aligned(wt, 4)) return ISC_ERR_ALIGN;
+    if (!aligned(w, 4) || !aligned(wt, 16)) return ISC_ERR_ALIGN;
     const size_t wb = sizeof(float) * static_cast<size_t>(s.filt_elems());
-    if (overlap(w, wb, wt, wb)) return ISC_ERR_ALIAS;
+    const size_t tb = sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
+                                                                  static_cast<int>(s.R), static_cast<int>(s.S));
+    if (tb > static_cast<size_t>(kI32Max) * sizeof(float)) return ISC_ERR_LIMIT;
+    if (overlap(w, wb, wt, tb)) return ISC_ERR_ALIAS;
     st = check_device();
     if (st) return st;
-    return hip_status(isc::launch_repack_filter(w, static_cast<int>(s.K), static_cast<int>(s.crs()), wt,
+    return hip_status(isc::launch_repack_filter(w, static_cast<int>(s.K), static_cast<int>(s.C),
+                                                static_cast<int>(s.R), static_cast<int>(s.S), wt,
                                                 static_cast<hipStream_t>(stream)));
 }
 
@@ -308,18 +320,19 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
     int st = check_desc(d, &s);
     if (st) return st;
     if (!row_ptr || !nz || !wt || !y) return ISC_ERR_NULL;
-    if (!aligned(row_ptr, 4) || !aligned(nz, 8) || !aligned(wt, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
+    if (!aligned(row_ptr, 4) || !aligned(nz, 8) || !aligned(wt, 16) || !aligned(y, 4)) return ISC_ERR_ALIGN;
     const size_t yb = sizeof(float) * static_cast<size_t>(s.out_elems());
+    const size_t tb = sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
+                                                                  static_cast<int>(s.R), static_cast<int>(s.S));
     if (overlap(y, yb, row_ptr, sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1))) ||
         overlap(y, yb, nz, sizeof(isc_nz) * static_cast<size_t>(s.in_elems() + kNzTail)) ||
-        overlap(y, yb, wt, sizeof(float) * static_cast<size_t>(s.filt_elems())))
+        overlap(y, yb, wt, tb))
         return ISC_ERR_ALIAS;
     isc::SparseShape sh{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
                         static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
                         static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
                         static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
-    int th, bands, tw, ct, wa, hx;
-    if (!isc::sparse_tiling(sh, &th, &bands, &tw, &ct, &wa, &hx)) return ISC_ERR_LIMIT;
+    if (!isc::sparse_conv_feasible(sh)) return ISC_ERR_LIMIT;
     st = check_device();
     if (st) return st;
     isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};

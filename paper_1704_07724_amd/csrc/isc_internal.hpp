@@ -41,15 +41,15 @@ __device__ __forceinline__ bool decision_says_run(const Decision &d) {
 
 // --- launchers (each returns hipGetLastError() of its launches) ------------
 
-// Clears a nonzero counter before the compaction adds to it.
-hipError_t launch_zero_counter(unsigned long long *counter, hipStream_t s);
-
-// ISC step 1: per-plane row-major nonzero lists; adds the count to *counter.
+// ISC step 1: per-plane row-major nonzero lists, then their total in *counter.
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s);
 
-// Filter repack KCRS -> [C][R][S][K] (K contiguous), ISC step 2's layout.
-hipError_t launch_repack_filter(const float *w, int K, int CRS, float *wt, hipStream_t s);
+// Filter repack KCRS -> ISC step 2's K-contiguous kernel matrix, blocked by
+// 64 output maps: wt[((c*ceil(K/64) + kb)*64 + l)*RSP + t], RSP = R*S
+// rounded up to 4, zero padded.
+size_t repacked_filter_floats(int K, int C, int R, int S);
+hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, float *wt, hipStream_t s);
 
 struct SparseShape {
     int N, C, H, W, K, R, S, T, P, Ho, Wo;

@@ -1,27 +1,25 @@
-// ISC steps 2 and 3 (Sec. "Sparse Convolution"): zero-skipping convolution
-// over the compacted nonzero lists, output-stationary per workgroup.
+// ISC steps 2 and 3 (Sec. "Sparse Convolution"), general kernel: zero-skipping
+// convolution over the compacted nonzero lists with the output tile kept in
+// LDS.  It handles every shape (any R x S, any stride); the register-tile
+// kernel (sparse_reg.hip) is used instead where it applies.
 //
 // Layout of the work.  A workgroup owns one image n, one block of 64 output
 // maps k, a band of output rows and a tile of output columns; each of its
-// wavefronts owns TH consecutive rows of the band.  Lanes run over k, as the
-// paper's SIMD lanes do (step 2 multiplies one nonzero input by K-contiguous
-// weights), so every nonzero input is a wave-uniform scalar and the only
-// per-lane data are the weights and the accumulators.  The wavefront walks
-// the nonzeros of the input rows that reach its output rows -- one
-// contiguous slice of the plane's row-major list, found from the row
-// offsets -- and for every nonzero and every filter tap adds v * W[k,c,r,s]
-// into an accumulator tile kept in LDS as [row][column][k], the "temporary
+// four wavefronts owns TH consecutive rows of the band.  Lanes run over k, as
+// the paper's SIMD lanes do (step 2 multiplies one nonzero input by
+// K-contiguous weights), so every nonzero input is a wave-uniform scalar and
+// the only per-lane data are the weights and the accumulators.  A wavefront
+// walks the nonzeros of the input rows that reach its output rows -- one
+// contiguous slice of each plane's row-major list, found from the row
+// offsets -- and for every nonzero and filter tap adds v * W[k, c, r, s] into
+// an accumulator tile kept in LDS as [row][column][k], the "temporary
 // results" of step 2.  The tile has halo columns, so taps that fall left or
-// right of the output need no test at stride 1; rows outside the wavefront's
-// band are skipped per filter row.  At the end the tile is read back
-// transposed and stored to NCHW (step 3).
+// right of the output need no test at stride 1; rows outside the
+// wavefront's band are skipped per filter row.  At the end the tile is read
+// back transposed and stored to NCHW (step 3).
 //
-// Filter weights come from the repacked [C][R][S][K] copy (the paper's
-// column-major kernel matrix): for a channel c the R*S weights of the lane's
-// k sit in registers, loaded one channel ahead.
-//
-// Every accumulator element is updated only by its own lane, in the order of
-// the nonzero list, so results are deterministic run to run.
+// Every accumulator element is updated only by its own lane, in list order,
+// so results are deterministic run to run.
 #include "isc_internal.hpp"
 
 #include <algorithm>
@@ -33,13 +31,16 @@ namespace {
 
 constexpr int kLanes = 64;
 constexpr int kAccStride = kLanes + 1;  // padded: transposed reads avoid bank conflicts
+constexpr int kWaves = 4;               // wavefronts per workgroup
 
+// wt: the repacked filter, wt[((c * R + r) * S + s) * Kp + k] (see
+// launch_repack_filter).
 struct SparseArgs {
     const int32_t *row_ptr;
     const NzEntry *nz;
-    const float *wt;  // [C][R][S][K]
+    const float *wt;
     float *y;
-    int N, C, H, W, K, R, S, T, P, Ho, Wo;
+    int N, C, H, W, K, Kp, R, S, T, P, Ho, Wo;
     int TH;       // output rows per wavefront
     int bands;    // row bands per image
     int TW;       // output columns per tile
@@ -50,174 +51,176 @@ struct SparseArgs {
     Decision dec;
 };
 
-// acc += v * w on the lane's own accumulator; kAtomic selects an LDS atomic
-// add (no read-back, fire and forget) instead of load / fma / store.
-template <bool kAtomic>
-__device__ __forceinline__ void acc_add(float *p, float v, float w) {
-    if constexpr (kAtomic) {
-        __hip_atomic_fetch_add(p, v * w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-    } else {
-        *p = __builtin_fmaf(v, w, *p);
-    }
-}
+// Where a workgroup / wavefront sits in the output.
+struct Tile {
+    int n, kb, oy0, ox0, rows, cols;
+    int ylo, yhi, xlo, xhi;  // input rows / columns whose taps reach the tile
+    bool any;                // the wavefront owns at least one output
+    bool whole_rows;         // the tile's input columns are the full rows
+};
 
-template <int RT, int ST, bool kAtomic>
-__global__ __launch_bounds__(256)
-void sparse_conv_kernel(SparseArgs a) {
-    const bool run = decision_says_run(a.dec);
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.dec.record) a.dec.record->path_taken = run ? 1u : 2u;
-    if (!run) return;
-
-    extern __shared__ float lds[];
-    const int lane = threadIdx.x & (kLanes - 1);
-    const int wave = threadIdx.x / kLanes;
-    const int waves = blockDim.x / kLanes;
-
-    constexpr int kRegRS = RT * ST;  // weights held in registers (0: read per tap)
-    const int R = RT > 0 ? RT : a.R;
-    const int S = ST > 0 ? ST : a.S;
-    const int RS = R * S;
-    const int T = a.T, P = a.P, H = a.H, W = a.W, K = a.K;
-    const int Ho = a.Ho, Wo = a.Wo, TH = a.TH, WA = a.WA, hx = a.hx;
-
+__device__ __forceinline__ Tile tile_of(const SparseArgs &a, int wave) {
+    Tile t;
     int b = blockIdx.x;
-    const int kb = b % a.kblocks;
+    t.kb = b % a.kblocks;
     b /= a.kblocks;
     const int ct = b % a.ctiles;
     b /= a.ctiles;
     const int band = b % a.bands;
-    const int n = b / a.bands;
+    t.n = b / a.bands;
+    t.oy0 = (band * kWaves + wave) * a.TH;
+    t.ox0 = ct * a.TW;
+    t.rows = min(a.TH, a.Ho - t.oy0);
+    t.cols = min(a.TW, a.Wo - t.ox0);
+    t.ylo = max(0, t.oy0 * a.T - a.P);
+    t.yhi = min(a.H - 1, (t.oy0 + t.rows - 1) * a.T - a.P + a.R - 1);
+    t.xlo = max(0, t.ox0 * a.T - a.P);
+    t.xhi = min(a.W - 1, (t.ox0 + t.cols - 1) * a.T - a.P + a.S - 1);
+    t.any = t.rows > 0 && t.cols > 0 && t.ylo <= t.yhi;
+    t.whole_rows = t.xlo == 0 && t.xhi == a.W - 1;
+    return t;
+}
 
-    const int oy0 = (band * waves + wave) * TH;  // first output row of this wavefront
-    const int ox0 = ct * a.TW;                   // first output column of the tile
-    const int k = kb * kLanes + lane;
-    const bool k_ok = k < K;
-
-    float *acc = lds + static_cast<size_t>(wave) * TH * WA * kAccStride;
-    for (int pos = 0; pos < TH * WA; ++pos) acc[pos * kAccStride + lane] = 0.0f;
-
-    const int rows = min(TH, Ho - oy0);      // rows this wavefront owns
-    const int cols = min(a.TW, Wo - ox0);    // columns of this tile
-    if (rows > 0) {
-        // input rows / columns whose taps reach the owned outputs
-        const int ylo = max(0, oy0 * T - P);
-        const int yhi = min(H - 1, (oy0 + rows - 1) * T - P + R - 1);
-        const int xlo = max(0, ox0 * T - P);
-        const int xhi = min(W - 1, (ox0 + cols - 1) * T - P + S - 1);
-        const bool whole_rows = xlo == 0 && xhi == W - 1;
-        const size_t HW = static_cast<size_t>(H) * W;
-
-        float wcur[kRegRS > 0 ? kRegRS : 1];
-        float wnext[kRegRS > 0 ? kRegRS : 1];
-        if constexpr (kRegRS > 0) {
+// One nonzero input (value v at row yy, column xx of a channel's plane): add
+// its products with that channel's filter taps w(r*S + s) (this lane's k)
+// into the wavefront's accumulator tile.
+template <int RT, int ST, typename WFn>
+__device__ __forceinline__ void scatter_nonzero(const SparseArgs &a, const Tile &t, float *acc, int lane,
+                                                WFn w, float v, int yy, int xx) {
+    const int T = a.T, P = a.P, WA = a.WA, hx = a.hx;
+    const int R = RT > 0 ? RT : a.R;
+    const int S = ST > 0 ? ST : a.S;
+    if (T == 1) {
+        // accumulator column of tap s is col_last + (S - 1 - s): tap S-1 is
+        // the leftmost, so every tap is a positive constant offset from one
+        // address (the halo absorbs taps left or right of the tile)
+        const int col_last = xx + P - t.ox0 + hx - (S - 1);
+        if constexpr (RT > 0) {
 #pragma unroll
-            for (int t = 0; t < kRegRS; ++t)
-                wcur[t] = k_ok ? a.wt[static_cast<size_t>(t) * K + k] : 0.0f;
+            for (int r = 0; r < RT; ++r) {
+                const int oy = yy + P - r - t.oy0;
+                if (static_cast<unsigned>(oy) < static_cast<unsigned>(t.rows)) {
+                    float *arow = acc + (oy * WA + col_last) * kAccStride + lane;
+#pragma unroll
+                    for (int s = 0; s < ST; ++s) {
+                        float *p = arow + (ST - 1 - s) * kAccStride;
+                        *p = __builtin_fmaf(v, w(r * ST + s), *p);
+                    }
+                }
+            }
+        } else {
+            for (int r = 0; r < R; ++r) {
+                const int oy = yy + P - r - t.oy0;
+                if (static_cast<unsigned>(oy) >= static_cast<unsigned>(t.rows)) continue;
+                float *arow = acc + (oy * WA + col_last) * kAccStride + lane;
+                for (int s = 0; s < S; ++s) {
+                    float *p = arow + (S - 1 - s) * kAccStride;
+                    *p = __builtin_fmaf(v, w(r * S + s), *p);
+                }
+            }
         }
-
-        for (int c = 0; c < a.C; ++c) {
-            if constexpr (kRegRS > 0) {
-                if (c + 1 < a.C) {
-                    const float *wn = a.wt + static_cast<size_t>(c + 1) * kRegRS * K;
+    } else {
+        // general stride: a tap reaches output (oy, ox) only when its offset
+        // divides by T (loops unrolled when R, S are compile-time, so the
+        // weights stay in fixed registers)
 #pragma unroll
-                    for (int t = 0; t < kRegRS; ++t)
-                        wnext[t] = k_ok ? wn[static_cast<size_t>(t) * K + k] : 0.0f;
-                }
-            }
-            const size_t plane = static_cast<size_t>(n) * a.C + c;
-            const int32_t *rp = a.row_ptr + plane * (H + 1);
-            const int e_begin = ylo <= yhi ? rp[ylo] : 0;
-            const int e_end = ylo <= yhi ? rp[yhi + 1] : 0;
-            const NzEntry *ent = a.nz + plane * HW;
-            const float *wc = a.wt + static_cast<size_t>(c) * RS * K;
-
-            for (int e = e_begin; e < e_end; ++e) {
-                const NzEntry q = ent[e];
-                const float v = q.v;
-                const int yy = static_cast<int>(q.yx >> 16);
-                const int xx = static_cast<int>(q.yx & 0xffffu);
-                if (!whole_rows && (xx < xlo || xx > xhi)) continue;
-                if (T == 1) {
-                    // accumulator column of tap s is col_s0 - s (halo absorbs
-                    // taps left or right of the tile)
-                    const int col_s0 = xx + P - ox0 + hx;
-                    if constexpr (kRegRS > 0) {
+        for (int r = 0; r < (RT > 0 ? RT : R); ++r) {
+            const int ty = yy + P - r;
+            if (ty < 0 || ty % T) continue;
+            const int oy = ty / T - t.oy0;
+            if (static_cast<unsigned>(oy) >= static_cast<unsigned>(t.rows)) continue;
 #pragma unroll
-                        for (int r = 0; r < RT; ++r) {
-                            const int oy = yy + P - r - oy0;
-                            if (static_cast<unsigned>(oy) < static_cast<unsigned>(rows)) {
-                                float *arow = acc + (oy * WA + col_s0) * kAccStride + lane;
-#pragma unroll
-                                for (int s = 0; s < ST; ++s)
-                                    acc_add<kAtomic>(arow - s * kAccStride, v, wcur[r * ST + s]);
-                            }
-                        }
-                    } else {
-                        for (int r = 0; r < R; ++r) {
-                            const int oy = yy + P - r - oy0;
-                            if (static_cast<unsigned>(oy) >= static_cast<unsigned>(rows)) continue;
-                            float *arow = acc + (oy * WA + col_s0) * kAccStride + lane;
-                            for (int s = 0; s < S; ++s) {
-                                const float wv = k_ok ? wc[static_cast<size_t>(r * S + s) * K + k] : 0.0f;
-                                acc_add<kAtomic>(arow - s * kAccStride, v, wv);
-                            }
-                        }
-                    }
-                } else {
-                    // general stride: a tap reaches output (oy, ox) only when
-                    // its offset divides by T
-                    for (int r = 0; r < R; ++r) {
-                        const int ty = yy + P - r;
-                        if (ty < 0 || ty % T) continue;
-                        const int oy = ty / T - oy0;
-                        if (static_cast<unsigned>(oy) >= static_cast<unsigned>(rows)) continue;
-                        for (int s = 0; s < S; ++s) {
-                            const int tx = xx + P - s;
-                            if (tx < 0 || tx % T) continue;
-                            const int ox = tx / T - ox0;
-                            if (static_cast<unsigned>(ox) >= static_cast<unsigned>(cols)) continue;
-                            float wv;
-                            if constexpr (kRegRS > 0) {
-                                wv = wcur[r * ST + s];
-                            } else {
-                                wv = k_ok ? wc[static_cast<size_t>(r * S + s) * K + k] : 0.0f;
-                            }
-                            acc_add<kAtomic>(acc + (oy * WA + ox + hx) * kAccStride + lane, v, wv);
-                        }
-                    }
-                }
-            }
-            if constexpr (kRegRS > 0) {
-#pragma unroll
-                for (int t = 0; t < kRegRS; ++t) wcur[t] = wnext[t];
+            for (int s = 0; s < (ST > 0 ? ST : S); ++s) {
+                const int tx = xx + P - s;
+                if (tx < 0 || tx % T) continue;
+                const int ox = tx / T - t.ox0;
+                if (static_cast<unsigned>(ox) >= static_cast<unsigned>(t.cols)) continue;
+                float *p = acc + (oy * WA + ox + hx) * kAccStride + lane;
+                *p = __builtin_fmaf(v, w(r * S + s), *p);
             }
         }
     }
+}
 
+// Walk cnt entries of a wavefront-resident slice (lane j holds entry j).
+template <int RT, int ST, typename WFn>
+__device__ __forceinline__ void run_slice(const SparseArgs &a, const Tile &t, float *acc, int lane, WFn w,
+                                          const NzEntry &mine, int cnt) {
+    for (int j = 0; j < cnt; ++j) {
+        const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine.v), j));
+        const uint32_t yx = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(mine.yx), j));
+        const int yy = static_cast<int>(yx >> 16);
+        const int xx = static_cast<int>(yx & 0xffffu);
+        if (!t.whole_rows && (xx < t.xlo || xx > t.xhi)) continue;
+        scatter_nonzero<RT, ST>(a, t, acc, lane, w, v, yy, xx);
+    }
+}
+
+__device__ __forceinline__ void zero_acc(float *acc, int positions, int lane) {
+    for (int pos = 0; pos < positions; ++pos) acc[pos * kAccStride + lane] = 0.0f;
+}
+
+// Step 3: transpose the wavefront's [row][column][k] tile to NCHW; for a
+// fixed k the rows x cols block is stored with consecutive lanes on
+// consecutive columns (contiguous when the tile spans the output width).
+__device__ __forceinline__ void write_tile(const SparseArgs &a, const Tile &t, const float *acc, int lane) {
     // other lanes' accumulators are read below: finish this wave's LDS writes
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    if (rows > 0 && cols > 0) {
-        // step 3: transpose [row][column][k] -> NCHW; for a fixed k the
-        // wavefront stores its rows x cols block, contiguous when the tile
-        // spans the full output width
-        const int count = rows * cols;
-        const size_t plane_out = static_cast<size_t>(Ho) * Wo;
-        const int kmax = min(kLanes, K - kb * kLanes);
-        float *ybase = a.y + (static_cast<size_t>(n) * K + kb * kLanes) * plane_out;
-        for (int i0 = 0; i0 < count; i0 += kLanes) {
-            const int idx = i0 + lane;
-            if (idx < count) {
-                const int oy = idx / cols;
-                const int ox = idx - oy * cols;
-                const float *src = acc + (oy * WA + ox + hx) * kAccStride;
-                float *dst = ybase + static_cast<size_t>(oy0 + oy) * Wo + ox0 + ox;
-                for (int kk = 0; kk < kmax; ++kk) dst[static_cast<size_t>(kk) * plane_out] = src[kk];
-            }
+    if (t.rows <= 0 || t.cols <= 0) return;
+    const int count = t.rows * t.cols;
+    const size_t plane_out = static_cast<size_t>(a.Ho) * a.Wo;
+    const int kmax = min(kLanes, a.K - t.kb * kLanes);
+    float *ybase = a.y + (static_cast<size_t>(t.n) * a.K + t.kb * kLanes) * plane_out;
+    for (int i0 = 0; i0 < count; i0 += kLanes) {
+        const int idx = i0 + lane;
+        if (idx < count) {
+            const int oy = idx / t.cols;
+            const int ox = idx - oy * t.cols;
+            const float *src = acc + (oy * a.WA + ox + a.hx) * kAccStride;
+            float *dst = ybase + static_cast<size_t>(t.oy0 + oy) * a.Wo + t.ox0 + ox;
+            for (int kk = 0; kk < kmax; ++kk) dst[static_cast<size_t>(kk) * plane_out] = src[kk];
         }
     }
+}
+
+__device__ __forceinline__ bool gate_and_record(const SparseArgs &a) {
+    const bool run = decision_says_run(a.dec);
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.dec.record) a.dec.record->path_taken = run ? 1u : 2u;
+    return run;
+}
+
+// ---------------------------------------------------------------------------
+// Generic kernel: any R x S (runtime), one channel at a time, weights read
+// per tap from the repacked filter.
+
+__global__ __launch_bounds__(kWaves * kLanes)
+void sparse_conv_generic_kernel(SparseArgs a) {
+    if (!gate_and_record(a)) return;
+    extern __shared__ float4 lds4[];
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+    const Tile t = tile_of(a, wave);
+    float *acc = reinterpret_cast<float *>(lds4) + static_cast<size_t>(wave) * a.TH * a.WA * kAccStride;
+    zero_acc(acc, a.TH * a.WA, lane);
+    if (t.any) {
+        const int RS = a.R * a.S;
+        const size_t HW = static_cast<size_t>(a.H) * a.W;
+        const float *wk = a.wt + t.kb * kLanes + lane;  // this lane's k (zero padded to Kp)
+        for (int c = 0; c < a.C; ++c) {
+            const size_t plane = static_cast<size_t>(t.n) * a.C + c;
+            const int32_t *rp = a.row_ptr + plane * (a.H + 1);
+            const int eb = rp[t.ylo];
+            const int ee = rp[t.yhi + 1];
+            const float *wc = wk + static_cast<size_t>(c) * RS * a.Kp;
+            auto wfn = [&](int tap) { return wc[static_cast<size_t>(tap) * a.Kp]; };
+            const NzEntry *ent = a.nz + plane * HW;
+            for (int e = eb; e < ee; e += kLanes)
+                run_slice<0, 0>(a, t, acc, lane, wfn, ent[e + lane], min(kLanes, ee - e));
+        }
+    }
+    write_tile(a, t, acc, lane);
 }
 
 // Raise a kernel's dynamic-LDS limit once (per process) to the largest size
@@ -235,54 +238,55 @@ hipError_t ensure_lds(Kern kern, std::atomic<int> &granted, int bytes) {
     return e;
 }
 
-template <int RT, int ST>
-hipError_t launch_sparse_t(const SparseArgs &a, int waves, bool atomic, hipStream_t s) {
-    static std::atomic<int> granted_plain{0}, granted_atomic{0};
-    const size_t lds = static_cast<size_t>(waves) * a.TH * a.WA * kAccStride * sizeof(float);
-    const int grid = a.N * a.bands * a.ctiles * a.kblocks;
-    auto kern = atomic ? sparse_conv_kernel<RT, ST, true> : sparse_conv_kernel<RT, ST, false>;
-    hipError_t e = ensure_lds(kern, atomic ? granted_atomic : granted_plain, static_cast<int>(lds));
-    if (e != hipSuccess) return e;
-    kern<<<grid, waves * kLanes, lds, s>>>(a);
-    return hipGetLastError();
+constexpr size_t kLdsBudget = 80 * 1024;   // per workgroup: two workgroups per CU
+constexpr size_t kLdsMax = 160 * 1024;
+constexpr int64_t kTargetWaves = 256 * 16;  // ~16 wavefronts per CU
+
+size_t acc_bytes(int th, int wa) {
+    return ((static_cast<size_t>(kWaves) * th * wa * kAccStride + 3) / 4) * sizeof(float4);
 }
 
-constexpr size_t kLdsBudget = 80 * 1024;  // per workgroup: two workgroups per CU
-constexpr int kWaves = 4;
-
-}  // namespace
-
-// Tiling of the sparse kernel for a shape; false if no tile fits in LDS.
-bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *ctiles, int *WA, int *hx) {
-    const size_t per_col = static_cast<size_t>(kAccStride) * sizeof(float);
-    int tw = sh.Wo, wa, h;
-    auto halo = [&](int t, int *wa_out, int *hx_out) {
+// Tiling for a shape, given the LDS the kernel needs besides the
+// accumulators; false if no tile fits.
+bool tiling_for(const SparseShape &sh, size_t extra, int *TH, int *bands, int *TW, int *ctiles, int *WA,
+                int *hx) {
+    if (extra >= kLdsBudget) return false;
+    const size_t budget = kLdsBudget - extra;
+    int tw = sh.Wo, wa = 0, h = 0;
+    auto halo = [&](int w, int *wa_out, int *hx_out) {
         if (sh.T != 1) {
             *hx_out = 0;
-            *wa_out = t;
-        } else if (t == sh.Wo) {
+            *wa_out = w;
+        } else if (w == sh.Wo) {
             // taps reach output columns x + P - s in [P - S + 1, W - 1 + P]
             *hx_out = std::max(0, sh.S - 1 - sh.P);
             *wa_out = *hx_out + std::max(sh.Wo, sh.W + sh.P);
         } else {
             *hx_out = sh.S - 1;
-            *wa_out = t + 2 * (sh.S - 1);
+            *wa_out = w + 2 * (sh.S - 1);
         }
     };
     halo(tw, &wa, &h);
-    if (kWaves * wa * per_col > kLdsBudget) {
-        const int fit = static_cast<int>(kLdsBudget / (kWaves * per_col));
+    if (acc_bytes(1, wa) > budget) {
+        const int fit = static_cast<int>(budget / (kWaves * kAccStride * sizeof(float))) - 1;
         tw = sh.T == 1 ? fit - 2 * (sh.S - 1) : fit;
         if (tw < 1) return false;
         halo(tw, &wa, &h);
     }
-    const size_t per_row = static_cast<size_t>(wa) * per_col;
-    int th = static_cast<int>(kLdsBudget / (kWaves * per_row));
-    th = std::max(1, std::min(th, (sh.Ho + kWaves - 1) / kWaves));
+    // rows per wavefront: as many as LDS allows while the grid keeps about
+    // 16 wavefronts per CU (other wavefronts hide each one's latencies)
+    const int64_t kblocks = (sh.K + kLanes - 1) / kLanes;
+    const int64_t ctl = (sh.Wo + tw - 1) / tw;
+    int th = 1;
+    for (int t = 2; t <= sh.Ho && acc_bytes(t, wa) <= budget; ++t) {
+        const int64_t wavefronts = static_cast<int64_t>(sh.N) * ((sh.Ho + t - 1) / t) * ctl * kblocks;
+        if (wavefronts < kTargetWaves) break;
+        th = t;
+    }
     const int bands0 = (sh.Ho + kWaves * th - 1) / (kWaves * th);
     th = (sh.Ho + bands0 * kWaves - 1) / (bands0 * kWaves);  // balance rows over wavefronts
     if (const char *env = std::getenv("ISC_SPARSE_TH")) th = std::max(1, std::atoi(env));
-    if (kWaves * th * per_row > 160 * 1024) return false;
+    if (acc_bytes(th, wa) + extra > kLdsMax) return false;
     *TH = th;
     *bands = (sh.Ho + kWaves * th - 1) / (kWaves * th);
     *TW = tw;
@@ -292,52 +296,87 @@ bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *cti
     return true;
 }
 
+template <typename Kern>
+hipError_t launch_with(Kern kern, std::atomic<int> &granted, const SparseArgs &a, size_t extra, hipStream_t s) {
+    const size_t lds = acc_bytes(a.TH, a.WA) + extra;
+    const int grid = a.N * a.bands * a.ctiles * a.kblocks;
+    hipError_t e = ensure_lds(kern, granted, static_cast<int>(lds));
+    if (e != hipSuccess) return e;
+    kern<<<grid, kWaves * kLanes, lds, s>>>(a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool sparse_reg_applies(const SparseShape &sh);
+hipError_t launch_sparse_reg(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz, const float *wt,
+                             float *y, const Decision &dec, hipStream_t s);
+
+bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *ctiles, int *WA, int *hx) {
+    return tiling_for(sh, 0, TH, bands, TW, ctiles, WA, hx);
+}
+
+bool sparse_conv_feasible(const SparseShape &sh) {
+    int th, bands, tw, ct, wa, hx;
+    return sparse_reg_applies(sh) || tiling_for(sh, 0, &th, &bands, &tw, &ct, &wa, &hx);
+}
+
 hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz,
                               const float *wt, float *y, const Decision &dec, hipStream_t s) {
+    const char *force = std::getenv("ISC_SPARSE_KERNEL");  // "lds" forces the general kernel
+    const bool use_reg = sparse_reg_applies(sh) && !(force && force[0] == 'l');
+    if (use_reg) return launch_sparse_reg(sh, row_ptr, nz, wt, y, dec, s);
     SparseArgs a{};
     a.row_ptr = row_ptr;
     a.nz = nz;
     a.wt = wt;
     a.y = y;
-    a.N = sh.N; a.C = sh.C; a.H = sh.H; a.W = sh.W; a.K = sh.K;
+    a.N = sh.N; a.C = sh.C; a.H = sh.H; a.W = sh.W; a.K = sh.K; a.Kp = (sh.K + kLanes - 1) / kLanes * kLanes;
     a.R = sh.R; a.S = sh.S; a.T = sh.T; a.P = sh.P; a.Ho = sh.Ho; a.Wo = sh.Wo;
     a.dec = dec;
-    if (!sparse_tiling(sh, &a.TH, &a.bands, &a.TW, &a.ctiles, &a.WA, &a.hx)) return hipErrorInvalidValue;
+    if (!tiling_for(sh, 0, &a.TH, &a.bands, &a.TW, &a.ctiles, &a.WA, &a.hx)) return hipErrorInvalidValue;
     a.kblocks = (sh.K + kLanes - 1) / kLanes;
-    const char *env = std::getenv("ISC_SPARSE_ATOMIC");
-    const bool atomic = env ? std::atoi(env) != 0 : false;
-
-    if (sh.R == 1 && sh.S == 1) return launch_sparse_t<1, 1>(a, kWaves, atomic, s);
-    if (sh.R == 3 && sh.S == 3) return launch_sparse_t<3, 3>(a, kWaves, atomic, s);
-    if (sh.R == 5 && sh.S == 5) return launch_sparse_t<5, 5>(a, kWaves, atomic, s);
-    if (sh.R == 7 && sh.S == 7) return launch_sparse_t<7, 7>(a, kWaves, atomic, s);
-    return launch_sparse_t<0, 0>(a, kWaves, atomic, s);
+    static std::atomic<int> granted{0};
+    return launch_with(sparse_conv_generic_kernel, granted, a, 0, s);
 }
 
 // --- filter repack ----------------------------------------------------------
+//
+// ISC step 2's kernel matrix in the paper's K-contiguous ("column-major")
+// order: for one input channel and tap the weights of consecutive output maps
+// are adjacent, padded to Kp = K rounded up to 64 so that every block of 64
+// output maps is a 256-byte run:
+//   wt[((c * R + r) * S + s) * Kp + k] = w[k][c][r][s]   (0 for k >= K)
 
 namespace {
 __global__ __launch_bounds__(256)
-void repack_filter_kernel(const float *__restrict__ w, int K, int CRS, float *__restrict__ wt) {
-    // wt[q][k] = w[k][q] through a 64 x 64 LDS tile, both sides coalesced
+void repack_filter_kernel(const float *__restrict__ w, int K, int Kp, int CRS, float *__restrict__ wt) {
+    // 64 x 64 tile through LDS: reads along q = (c, r, s), writes along k
     __shared__ float tile[64][65];
     const int q0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
     for (int i = ty; i < 64; i += 4) {
-        const int kk = k0 + i, q = q0 + tx;
-        tile[i][tx] = (kk < K && q < CRS) ? w[static_cast<size_t>(kk) * CRS + q] : 0.0f;
+        const int k = k0 + i, q = q0 + tx;
+        tile[i][tx] = (k < K && q < CRS) ? w[static_cast<size_t>(k) * CRS + q] : 0.0f;
     }
     __syncthreads();
     for (int i = ty; i < 64; i += 4) {
-        const int q = q0 + i, kk = k0 + tx;
-        if (q < CRS && kk < K) wt[static_cast<size_t>(q) * K + kk] = tile[tx][i];
+        const int q = q0 + i, k = k0 + tx;
+        if (q < CRS && k < Kp) wt[static_cast<size_t>(q) * Kp + k] = tile[tx][i];
     }
 }
 }  // namespace
 
-hipError_t launch_repack_filter(const float *w, int K, int CRS, float *wt, hipStream_t s) {
-    dim3 grid((CRS + 63) / 64, (K + 63) / 64);
-    repack_filter_kernel<<<grid, 256, 0, s>>>(w, K, CRS, wt);
+size_t repacked_filter_floats(int K, int C, int R, int S) {
+    const size_t Kp = (static_cast<size_t>(K) + 63) / 64 * 64;
+    return static_cast<size_t>(C) * R * S * Kp;
+}
+
+hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, float *wt, hipStream_t s) {
+    const int CRS = C * R * S;
+    const int Kp = (K + 63) / 64 * 64;
+    dim3 grid((CRS + 63) / 64, Kp / 64);
+    repack_filter_kernel<<<grid, 256, 0, s>>>(w, K, Kp, CRS, wt);
     return hipGetLastError();
 }
 

@@ -330,8 +330,11 @@ def test_sparse_conv_entry_from_lists(torch, isc):
     lists = isc.isc_compact(xd)
     for w, P in ((w3, 1), (w5, 2)):
         wt = isc.isc_repack_filter(to_dev(torch, w))
-        want_wt = np.ascontiguousarray(w.transpose(1, 2, 3, 0))
-        assert np.array_equal(wt.cpu().numpy(), want_wt)
+        K, C, R, S = w.shape
+        # [c][r][s][k], K contiguous and zero padded to a multiple of 64
+        want_wt = np.zeros((C, R, S, (K + 63) // 64 * 64), np.float32)
+        want_wt[..., :K] = w.transpose(1, 2, 3, 0)
+        assert np.array_equal(wt.dense().cpu().numpy(), want_wt)
         y = isc.isc_sparse_conv(xd.shape, lists, wt, 1, P).cpu().numpy()
         assert_conv_close(y, oracle.conv2d_f64(x, w, 1, P), "lists P=%d" % P)
 
