@@ -159,8 +159,8 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
  * filter tap (r, s) that reaches a valid output, add x * wt[c,r,s,k] to
  * y[n, k, (y+P-r)/T, (x+P-s)/T]; then y holds the convolution of Eq. 1.
  *   row_ptr, nz: as written by isc_compact for N, C, H, W of d (read only;
- *     nz must have 64 readable entries past N*C*H*W -- isc_conv2d's
- *     workspace does; a caller's own buffer of N*C*H*W + 64 entries does).
+ *     nz must have 256 readable entries past N*C*H*W -- isc_conv2d's
+ *     workspace does; a caller's own buffer of N*C*H*W + 256 entries does).
  *   wt: the repacked filter of isc_repack_filter (16-byte aligned).
  *   y: device output N x K x Ho x Wo, fully written, must not overlap the
  *     inputs.

@@ -192,7 +192,7 @@ def isc_decision(desc: ConvDesc, ws, stream=None):
     return nnz.value, PATH_NAMES.get(path.value, path.value)
 
 
-NZ_TAIL = 64  # spare entries isc_sparse_conv may read past the last plane
+NZ_TAIL = 256  # spare entries isc_sparse_conv may read past the last plane
 
 
 def isc_compact(x, stream=None, out=None):

@@ -21,7 +21,7 @@ using isc::NzEntry;
 constexpr int64_t kI32Max = std::numeric_limits<int32_t>::max();
 constexpr size_t kAlign = 256;
 constexpr int64_t kColPad = 256;   // im2col rows padded to this many columns
-constexpr int64_t kNzTail = 64;    // spare list entries after the last plane
+constexpr int64_t kNzTail = 256;   // spare list entries after the last plane (read, never used)
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 

@@ -15,16 +15,19 @@
 // multiply-adds per nonzero plus a few scalar compares.
 //
 // The workgroup's four wavefronts own four consecutive output rows of one
-// image and share the filter: channel by channel the workgroup copies the
-// channel's R*S*64*KPL weights into LDS, and each wavefront its nonzero run
-// for that channel (both loaded into registers while the previous channel is
-// computed), so the compute phase reads only LDS and registers.  At the end each lane stores its
+// image and share the filter.  Channels flow through a ring of NBUF stages:
+// each stage's R*S*64*KPL weights go global -> LDS by direct loads (no
+// staging registers), each wavefront's nonzero run for that channel goes into
+// a matching ring of registers, and stages are issued NBUF-1 channels ahead;
+// one barrier per channel, after a wait for exactly the stage consumed.  The
+// compute phase reads only LDS and registers whose loads have completed.  At the end each lane stores its
 // accumulators to NCHW (step 3).  Summation order per output is fixed (list
 // order within a channel, channels in order), so results are deterministic.
 #include "isc_internal.hpp"
 
 #include <algorithm>
 #include <cstdlib>
+#include <type_traits>
 
 namespace isc {
 namespace {
@@ -73,31 +76,67 @@ __device__ __forceinline__ void dispatch(int xp, float (&acc)[TWM][KPL], const f
     }
 }
 
+// 16 bytes per lane from global memory straight into LDS at dst + 16 * lane
+// (dst wave-uniform).  Kept in a device function: the builtin has no host
+// form, and host-side instantiation of a lambda calling it would drop the
+// kernel.
+__device__ __forceinline__ void load_lds16(const float *src, float4 *dst) {
+    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// s_waitcnt vmcnt(VM) lgkmcnt(0) (expcnt untouched), then a workgroup
+// barrier that the compiler may not move memory operations across.
+template <int VM>
+__device__ __forceinline__ void wait_vm_and_barrier() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt field");
+    constexpr int imm = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4);  // lgkmcnt = 0
+    __builtin_amdgcn_s_waitcnt(imm);
+    asm volatile("s_barrier" ::: "memory");
+}
+
+template <int RS_, int KPL>
+struct RegShape {
+    static constexpr int KW = kLanes * KPL;                 // output maps per wavefront
+    static constexpr int WFLOATS = RS_ * RS_ * KW;          // one channel's weights
+    static constexpr int NDW = (WFLOATS + 255) / 256;       // 1 KB direct-to-LDS blocks
+    static constexpr int SLOT4 = NDW * kLanes;              // float4 per ring slot
+    // ring depth: deeper when a channel's weights are small
+    static constexpr int NBUF = SLOT4 * 16 <= 8192 ? 4 : (SLOT4 * 16 <= 16384 ? 3 : 2);
+    static constexpr int DPW = (NDW + kWaves - 1) / kWaves;  // weight blocks per wavefront
+    static constexpr int EPL = kRunMax / kLanes;             // run entries per lane
+    static constexpr int VPS = DPW + EPL;                    // vector-memory ops per stage
+    static constexpr size_t lds_static = sizeof(float4) * NBUF * SLOT4;
+};
+
 template <int RS_, int KPL, int TWM>
 __global__ __launch_bounds__(kWaves * kLanes)
 void sparse_conv_reg_kernel(RegArgs a) {
+    using SH = RegShape<RS_, KPL>;
     constexpr int R = RS_, S = RS_;
-    constexpr int XMAX = TWM + S - 1;             // shifted columns a tile can see
-    constexpr int KW = kLanes * KPL;              // output maps per wavefront
-    constexpr int WF4 = R * S * KW / 4;           // float4 of one channel's weights
-    constexpr int WPT = (WF4 + kWaves * kLanes - 1) / (kWaves * kLanes);
-    constexpr int NOFF = R + 1;                   // row offsets kept per channel
-    constexpr int EPL = kRunMax / kLanes;         // staged run entries per lane
+    constexpr int XMAX = TWM + S - 1;  // shifted columns a tile can see
+    constexpr int KW = SH::KW, NDW = SH::NDW, NBUF = SH::NBUF, DPW = SH::DPW, EPL = SH::EPL;
+    constexpr int NOFF = R + 1;        // row offsets kept per channel
 
-    const bool run = decision_says_run(a.dec);
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.dec.record) a.dec.record->path_taken = run ? 1u : 2u;
-    if (!run) return;
+    // ring of NBUF slots, each one channel's weights [R*S][KW] (k = kbase +
+    // lane*KPL + j) padded to whole 1 KB blocks; static, so that the compiler
+    // can tell the slot being read from the slots being filled
+    __shared__ float4 wring[NBUF][SH::SLOT4];
+    extern __shared__ int32_t offs_all[];  // [waves][C][R+1] row offsets
 
-    // LDS: one channel's weights [R*S][KW] | each wavefront's staged nonzero
-    // run [kRunMax] | each wavefront's row offsets [C][R+1]
-    extern __shared__ float4 lds4[];
-    float *wlds = reinterpret_cast<float *>(lds4);
+    const bool run_ok = decision_says_run(a.dec);
+    if (blockIdx.x == 0 && threadIdx.x == 0 && a.dec.record) a.dec.record->path_taken = run_ok ? 1u : 2u;
+    if (!run_ok) return;
+
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
-    NzEntry *ebuf = reinterpret_cast<NzEntry *>(lds4 + WF4) + wave * kRunMax;
-    int32_t *offs = reinterpret_cast<int32_t *>(reinterpret_cast<NzEntry *>(lds4 + WF4) + kWaves * kRunMax) +
-                    wave * a.C * NOFF;
-
     int b = blockIdx.x;
     const int kg = b % a.kgroups;
     b /= a.kgroups;
@@ -108,7 +147,7 @@ void sparse_conv_reg_kernel(RegArgs a) {
     const int oy = band * kWaves + wave;
     const int ox0 = ct * a.TW;
     const int kbase = kg * KW;
-    const int C = a.C, H = a.H, P = a.P;
+    const int C = a.C, H = a.H, P = a.P, Kp = a.Kp;
     const bool row_ok = oy < a.Ho;
     // input rows oy + r - P for r in [0, R), clipped to the map
     const int ylo = max(0, oy - P);
@@ -117,11 +156,11 @@ void sparse_conv_reg_kernel(RegArgs a) {
     const int tw = min(a.TW, a.Wo - ox0);
     const int xlo = max(0, ox0 - P);
     const int xhi = min(a.W - 1, ox0 + tw - 1 - P + S - 1);
-    const bool whole_rows = xlo == 0 && xhi == a.W - 1;
     const size_t HW = static_cast<size_t>(H) * a.W;
     const NzEntry *nz_n = a.nz + static_cast<size_t>(n) * C * HW;
+    int32_t *offs = offs_all + wave * C * NOFF;
 
-    // row offsets of this wavefront's input rows, every channel, into LDS
+    // row offsets of this wavefront's input rows, every channel
     {
         const int32_t *rp_n = a.row_ptr + static_cast<size_t>(n) * C * (H + 1);
         for (int idx = lane; idx < C * NOFF; idx += kLanes) {
@@ -140,101 +179,92 @@ void sparse_conv_reg_kernel(RegArgs a) {
 #pragma unroll
         for (int j = 0; j < KPL; ++j) acc[x][j] = 0.0f;
 
-    // one channel's weights, [R*S][KW] with k = kbase + lane*KPL + j, as
-    // float4 runs of the K-contiguous filter (zero past Kp)
-    float4 wst[WPT];
-    auto load_weights = [&](int c) {
+    // this wavefront's nonzero run of a channel (its R input rows, at most
+    // kRunMax entries: the kernel is used only when R * W <= kRunMax), one
+    // register ring slot per weight slot; lanes past the run read later
+    // slots or the list's 256-entry tail and are ignored
+    NzEntry run[NBUF][EPL];
+
+    // stage c -> slot SLOT: weights by direct global->LDS loads (every
+    // wavefront issues exactly DPW blocks and EPL run loads, so the number of
+    // vector-memory operations per stage is the same everywhere)
+    auto issue = [&](auto slot_c, int c) {
+        constexpr int SLOT = decltype(slot_c)::value;
 #pragma unroll
-        for (int q = 0; q < WPT; ++q) {
-            const int f = threadIdx.x + q * kWaves * kLanes;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (f < WF4) {
-                const int tap = f / (KW / 4);
-                const int k4 = kbase + 4 * (f - tap * (KW / 4));
-                if (k4 < a.Kp)
-                    v = *reinterpret_cast<const float4 *>(a.wt + (static_cast<size_t>(c) * R * S + tap) * a.Kp + k4);
-            }
-            wst[q] = v;
+        for (int i = 0; i < DPW; ++i) {
+            const int d = min(wave + i * kWaves, NDW - 1);
+            const int f = d * 256 + lane * 4;  // float offset in the slot
+            int tap = f / KW;
+            const int koff = f - tap * KW;
+            tap = min(tap, R * S - 1);         // padding of the last block
+            const int k = min(kbase + koff, Kp - 4);
+            const float *src = a.wt + (static_cast<size_t>(c) * R * S + tap) * Kp + k;
+            load_lds16(src, &wring[SLOT][d * kLanes]);
         }
-    };
-    auto store_weights = [&]() {
-#pragma unroll
-        for (int q = 0; q < WPT; ++q) {
-            const int f = threadIdx.x + q * kWaves * kLanes;
-            if (f < WF4) lds4[f] = wst[q];
-        }
-    };
-    // this wavefront's nonzero run of channel c (at most kRunMax entries:
-    // the kernel is used only when R * W <= kRunMax), lane-strided
-    NzEntry est[EPL];
-    auto load_run = [&](int c) {
         const int e0 = __builtin_amdgcn_readfirstlane(offs[c * NOFF]);
-        const int cnt = __builtin_amdgcn_readfirstlane(offs[c * NOFF + nrows]) - e0;
-        const NzEntry *src = nz_n + static_cast<size_t>(c) * HW + e0;
+        const NzEntry *rsrc = nz_n + static_cast<size_t>(c) * HW + e0 + lane;
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-            NzEntry m{0.0f, 0u};
-            if (q * kLanes + lane < cnt) m = src[q * kLanes + lane];
-            est[q] = m;
-        }
-    };
-    auto store_run = [&]() {
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) ebuf[q * kLanes + lane] = est[q];
+        for (int q = 0; q < EPL; ++q) run[SLOT][q] = rsrc[q * kLanes];
     };
 
-    load_weights(0);
-    load_run(0);
-    store_weights();
-    store_run();
-    __syncthreads();
-
-    for (int c = 0; c < C; ++c) {
-        // prefetch channel c + 1 into registers; the compute below reads
-        // only LDS and registers that no load in flight writes
-        if (c + 1 < C) {
-            load_weights(c + 1);
-            load_run(c + 1);
-        }
+    // channel c from slot SLOT: LDS weights and register runs only
+    auto compute = [&](auto slot_c, int c) {
+        constexpr int SLOT = decltype(slot_c)::value;
+        const float *wl = reinterpret_cast<const float *>(&wring[SLOT][0]);
         const int *oc = offs + c * NOFF;
         const int e0 = __builtin_amdgcn_readfirstlane(oc[0]);
         const int e_all = __builtin_amdgcn_readfirstlane(oc[nrows]) - e0;
-        if (e_all > 0) {
-            // one copy of the dispatch code: filter rows run as a loop, the
-            // row's weights reloaded into the same registers
+        if (e_all <= 0) return;
+        // one copy of the dispatch code: filter rows run as a loop, the row's
+        // weights reloaded into the same registers
 #pragma unroll 1
-            for (int r = 0; r < R; ++r) {
-                const int y = oy + r - P;
-                if (y < ylo || y > yhi) continue;
-                const int lo = __builtin_amdgcn_readfirstlane(oc[y - ylo]) - e0;
-                const int hi = __builtin_amdgcn_readfirstlane(oc[y - ylo + 1]) - e0;
-                if (hi <= lo) continue;
-                float w[S][KPL];
+        for (int r = 0; r < R; ++r) {
+            const int y = oy + r - P;
+            if (y < ylo || y > yhi) continue;
+            const int lo = __builtin_amdgcn_readfirstlane(oc[y - ylo]) - e0;
+            const int hi = __builtin_amdgcn_readfirstlane(oc[y - ylo + 1]) - e0;
+            if (hi <= lo) continue;
+            float w[S][KPL];
 #pragma unroll
-                for (int s = 0; s < S; ++s)
+            for (int s = 0; s < S; ++s)
 #pragma unroll
-                    for (int j = 0; j < KPL; ++j) w[s][j] = wlds[(r * S + s) * KW + lane * KPL + j];
+                for (int j = 0; j < KPL; ++j) w[s][j] = wl[(r * S + s) * KW + lane * KPL + j];
 #pragma unroll 1
-                for (int q0 = lo & ~(kLanes - 1); q0 < hi; q0 += kLanes) {
-                    const NzEntry mine = ebuf[q0 + lane];
-                    const int jlo = max(lo, q0) - q0, jhi = min(hi, q0 + kLanes) - q0;
+            for (int q0 = lo & ~(kLanes - 1); q0 < hi; q0 += kLanes) {
+                const int qi = q0 / kLanes;
+                NzEntry mine = run[SLOT][0];
+#pragma unroll
+                for (int q = 1; q < EPL; ++q)
+                    if (qi == q) mine = run[SLOT][q];
+                const int jlo = max(lo, q0) - q0, jhi = min(hi, q0 + kLanes) - q0;
 #pragma unroll 1
-                    for (int jj = jlo; jj < jhi; ++jj) {
-                        const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine.v), jj));
-                        const int x = __builtin_amdgcn_readlane(static_cast<int>(mine.yx), jj) & 0xffff;
-                        if (static_cast<unsigned>(x - xlo) > static_cast<unsigned>(xhi - xlo)) continue;
-                        dispatch<S, KPL, TWM, 0, XMAX>(x + P - ox0, acc, w, v);
-                    }
+                for (int jj = jlo; jj < jhi; ++jj) {
+                    const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine.v), jj));
+                    const int x = __builtin_amdgcn_readlane(static_cast<int>(mine.yx), jj) & 0xffff;
+                    if (static_cast<unsigned>(x - xlo) > static_cast<unsigned>(xhi - xlo)) continue;
+                    dispatch<S, KPL, TWM, 0, XMAX>(x + P - ox0, acc, w, v);
                 }
             }
         }
-        __syncthreads();
-        if (c + 1 < C) {
-            store_weights();
-            store_run();
-        }
-        __syncthreads();
+    };
+
+    // prologue: stages 0 .. NBUF-2 in flight (past the last channel the last
+    // channel is loaded again, keeping the per-stage operation count fixed)
+    static_for<0, NBUF - 1>([&](auto sl) { issue(sl, min(decltype(sl)::value, C - 1)); });
+    for (int c0 = 0; c0 < C; c0 += NBUF) {
+        static_for<0, NBUF>([&](auto sl) {
+            constexpr int B = decltype(sl)::value;
+            const int c = c0 + B;
+            if (c < C) {
+                // stage c complete for every wavefront; everyone is done with
+                // stage c - 1, whose slot is refilled next
+                wait_vm_and_barrier<(NBUF - 2) * SH::VPS>();
+                issue(std::integral_constant<int, (B + NBUF - 1) % NBUF>{}, min(c + NBUF - 1, C - 1));
+                compute(sl, c);
+            }
+        });
     }
+    __builtin_amdgcn_s_waitcnt(0);  // no load into LDS may outlive the workgroup
 
     // step 3: each lane stores its accumulators to NCHW
     if (row_ok) {
@@ -265,15 +295,15 @@ int twm_for(int Wo) { return Wo <= 8 ? 8 : (Wo <= 16 ? 16 : 28); }
 
 template <int RS_, int KPL, int TWM>
 hipError_t launch_reg_t(const RegArgs &a, hipStream_t s) {
-    constexpr size_t wbytes = sizeof(float) * RS_ * RS_ * kLanes * KPL;
-    const size_t lds = wbytes + sizeof(NzEntry) * kWaves * kRunMax + sizeof(int32_t) * kWaves * a.C * (RS_ + 1);
-    if (lds > 160 * 1024) return hipErrorInvalidValue;
+    const size_t dyn = sizeof(int32_t) * kWaves * a.C * (RS_ + 1);
+    if (RegShape<RS_, KPL>::lds_static + dyn > 160 * 1024) return hipErrorInvalidValue;
     auto kern = sparse_conv_reg_kernel<RS_, KPL, TWM>;
-    if (lds > 64 * 1024) {
+    if (RegShape<RS_, KPL>::lds_static + dyn > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(dyn));
         if (e != hipSuccess) return e;
     }
+    const size_t lds = dyn;
     const int grid = a.N * a.bands * a.ctiles * a.kgroups;
     kern<<<grid, kWaves * kLanes, lds, s>>>(a);
     return hipGetLastError();
@@ -306,10 +336,9 @@ bool sparse_reg_applies(const SparseShape &sh) {
     if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     // a wavefront's run (R whole input rows) must fit the staging buffer
     if (static_cast<int64_t>(sh.R) * sh.W > kRunMax) return false;
-    // LDS: one channel's weights, the staged runs, the row offsets
-    const size_t kw = static_cast<size_t>(kLanes) * kpl_for(sh.K, sh.S);
-    const size_t lds = sizeof(float) * sh.R * sh.S * kw + sizeof(NzEntry) * kWaves * kRunMax +
-                       sizeof(int32_t) * kWaves * sh.C * (sh.R + 1);
+    // LDS: the weight ring (at most 2 x 25 KB for the shapes instantiated)
+    // and the row offsets of every channel
+    const size_t lds = 64 * 1024 + sizeof(int32_t) * kWaves * sh.C * (sh.R + 1);
     return lds <= 160 * 1024;
 }
 
