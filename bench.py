@@ -84,15 +84,27 @@ def event_time_ms(torch, fn, reps: int, warm: int = 3) -> float:
     return s.elapsed_time(e) / reps
 
 
-def graph_of(torch, fn):
-    """Capture fn (which launches on the current stream) into a HIP graph."""
+def graph_of(torch, fn, inner: int = 1):
+    """Capture `inner` back-to-back calls of fn (which launches on the
+    current stream) into one HIP graph."""
     fn()
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        fn()
+        for _ in range(inner):
+            fn()
     torch.cuda.synchronize()
     return g
+
+
+def kernel_time_ms(torch, fn, reps: int, graphs: bool = True, inner: int = 20) -> float:
+    """Average device time per launch of fn: `inner` launches captured in one
+    graph and replayed, HIP events around the replays on the launch stream,
+    so that host-side argument marshalling does not enter the figure."""
+    if not graphs:
+        return event_time_ms(torch, fn, reps)
+    g = graph_of(torch, fn, inner)
+    return event_time_ms(torch, g.replay, max(2, reps // inner + 1)) / inner
 
 
 class LayerRun:
@@ -133,7 +145,7 @@ class LayerRun:
 
     def im2col(self):
         L = self.layer
-        return lambda: self.isc.isc_im2col(self.x, L.R, L.S, L.T, L.P)
+        return lambda: self.isc.isc_im2col(self.x, L.R, L.S, L.T, L.P, out=self.col)
 
     def measure(self, steps, warmup, graphs=True):
         torch = self.torch
@@ -144,10 +156,10 @@ class LayerRun:
                 g = graph_of(torch, fn)
                 fn = g.replay
             res["t_%s_ms" % path] = event_time_ms(torch, fn, steps, warmup)
-        reps = max(20, steps // 2)
-        res["t_compact_ms"] = event_time_ms(torch, self.compact(), reps)
-        res["t_sparse_kernel_ms"] = event_time_ms(torch, self.sparse_kernel(), reps)
-        res["t_im2col_ms"] = event_time_ms(torch, self.im2col(), max(5, reps // 4))
+        reps = max(100, steps)
+        res["t_compact_ms"] = kernel_time_ms(torch, self.compact(), reps, graphs)
+        res["t_sparse_kernel_ms"] = kernel_time_ms(torch, self.sparse_kernel(), reps, graphs)
+        res["t_im2col_ms"] = kernel_time_ms(torch, self.im2col(), reps // 4, graphs, inner=5)
         res["t_gemm_ms"] = max(0.0, res["t_dense_ms"] - res["t_im2col_ms"])
         return res
 
@@ -175,23 +187,44 @@ class LayerRun:
 
 
 def cpu_baseline(layer, budget_s=10.0):
-    """The oracle (fp64 direct convolution, all host threads) on the first n
-    images of the workload, n sized for about budget_s seconds."""
+    """The oracle (fp64 direct convolution) on the headline workload, timed on
+    this host: with all its threads, repeated over the whole batch (or the
+    first n images when one pass is longer than budget_s) until about budget_s
+    seconds have passed; and with one thread on a few images."""
     import oracle
     x, w = workloads.make_inputs(layer)
+    all_threads = oracle.threads()
+
+    def rate(n, min_s):
+        oracle.conv2d_f64(x[:1], w, layer.T, layer.P)  # warm
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            out = oracle.conv2d_f64(x[:n], w, layer.T, layer.P)
+            reps += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_s:
+                break
+        Ho, Wo = out.shape[2], out.shape[3]
+        flops = 2.0 * n * layer.K * layer.C * layer.R * layer.S * Ho * Wo
+        return flops * reps / dt / 1e12, reps, dt
+
     t0 = time.perf_counter()
     oracle.conv2d_f64(x[:1], w, layer.T, layer.P)
     t1 = time.perf_counter() - t0
     n = int(max(1, min(layer.N, budget_s / max(t1, 1e-6))))
-    t0 = time.perf_counter()
-    out = oracle.conv2d_f64(x[:n], w, layer.T, layer.P)
-    dt = time.perf_counter() - t0
-    Ho, Wo = out.shape[2], out.shape[3]
-    flops = 2.0 * n * layer.K * layer.C * layer.R * layer.S * Ho * Wo
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": oracle.threads(),
-            "kind": "oracle",
-            "sample": "first %d of %d images of %s at sparsity %g (fp64 direct convolution, "
-                      "%.2f s, dense-equivalent flops)" % (n, layer.N, layer.name, layer.sparsity, dt),
+    value, reps, dt = rate(n, budget_s)
+    oracle.set_threads(1)
+    try:
+        n1 = int(max(1, min(layer.N, 1.0 / max(t1 * all_threads, 1e-6))))
+        value1, reps1, dt1 = rate(n1, 1.0)
+    finally:
+        oracle.set_threads(all_threads)
+    return {"value": round(value, 6), "unit": "TFLOP/s", "cores": all_threads, "kind": "oracle",
+            "sample": "%d x images 0..%d of %s (N=%d, sparsity %g), fp64 direct convolution over "
+                      "%d threads, %.2f s; dense-equivalent flops" % (
+                          reps, n - 1, layer.name, layer.N, layer.sparsity, all_threads, dt),
+            "one_thread": {"value": round(value1, 6), "unit": "TFLOP/s", "cores": 1,
+                           "sample": "%d x images 0..%d, %.2f s" % (reps1, n1 - 1, dt1)},
             "cpu_model": _cpu_model()}
 
 
@@ -215,6 +248,10 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--all", action="store_true", help="also measure every workload layer")
     ap.add_argument("--out", default=None, help="JSONL file for --all rows")
+    ap.add_argument("--probe", type=int, default=0, metavar="N",
+                    help="only launch each kernel of the headline layer N times, eagerly, after "
+                         "a copy kernel of known size, and print their algorithmic bytes "
+                         "(a short program for hardware-counter runs)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -231,6 +268,9 @@ def main():
 
     sweep_layers = workloads.WORKLOADS["lenet_conv2_batch"].layers
     head_layer = [l for l in sweep_layers if l.sparsity == 0.9][0]
+    if args.probe:
+        probe(torch, isc, head_layer, args.probe)
+        return
 
     # headline: whole hot path, AUTO, K timed steps bracketed by synchronize
     head = LayerRun(torch, isc, head_layer)
@@ -252,12 +292,22 @@ def main():
     hs = head.summary(res)
     t_kernel = res["t_sparse_kernel_ms"]
     achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
-    roofline = {"bound": "alu", "kernel": "sparse_conv_kernel", "achieved": round(achieved, 3),
-                "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4), "traffic": None,
+    traffic = counted_traffic()
+    roofline = {"bound": "alu", "kernel": "sparse_conv_reg_kernel (isc_sparse_conv)",
+                "achieved": round(achieved, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4),
+                "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
                 "per_launch": {"nonzero_macs": head.nz_macs, "flops": 2 * head.nz_macs,
                                "avg_duration_ms": round(t_kernel, 6)},
                 "frac_vs_packed_peak": round(achieved / VALU_F32_PACKED_PEAK_TFLOPS, 4)}
+
+    alg = algorithmic_bytes(head)
+    hbm = {}
+    for kern, t_key in (("compact", "t_compact_ms"), ("sparse_kernel", "t_sparse_kernel_ms"),
+                        ("im2col", "t_im2col_ms")):
+        gbs = alg[kern] / (res[t_key] * 1e-3) / 1e9
+        hbm[kern] = {"algorithmic_bytes": alg[kern], "ms": round(res[t_key], 6),
+                     "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
 
     sweep = []
     if not args.no_sweep:
@@ -291,6 +341,7 @@ def main():
         "measured_sparsity": hs["measured_sparsity"],
         "dense_path_tflops": hs["tflops_dense"],
         "roofline": roofline,
+        "hbm": hbm,
         "timings_ms": {k: hs[k] for k in hs if k.startswith("t_")},
         "sweep": sweep,
     }

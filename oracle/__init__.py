@@ -67,6 +67,8 @@ def load_library(path: str):
     lib.oracle_im2col.restype = None
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = i32
+    lib.oracle_set_threads.argtypes = [i32]
+    lib.oracle_set_threads.restype = None
     return lib
 
 
@@ -99,6 +101,11 @@ def _ptr(a: np.ndarray):
 def threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Thread count of the oracle's parallel loops from now on (timing only)."""
+    _load().oracle_set_threads(int(n))
 
 
 def out_size(n_in: int, k: int, pad: int, stride: int) -> int:

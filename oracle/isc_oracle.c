@@ -42,6 +42,17 @@ int oracle_threads(void)
 #endif
 }
 
+/* Set the thread count of the parallel loops (n >= 1); timing only. */
+void oracle_set_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* Output extent along one axis: floor((in + 2*pad - k) / stride) + 1, or 0
  * when the padded input is shorter than the filter. */
 int oracle_out_size(int in, int k, int pad, int stride)

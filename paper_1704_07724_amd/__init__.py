@@ -271,15 +271,22 @@ def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):
     return out
 
 
-def isc_im2col(x, R, S, stride=1, pad=0, ldc=None, stream=None):
-    """The unrolled input matrix M_I (Fig. 3) on the GPU: [C*R*S, ldc] float32."""
+def isc_im2col(x, R, S, stride=1, pad=0, ldc=None, out=None, stream=None):
+    """The unrolled input matrix M_I (Fig. 3) on the GPU: [C*R*S, ldc] float32
+    (written into `out` when given: contiguous, that shape)."""
     torch = _torch()
     x = _dev_f32(x, "x")
     N, C, H, W = (int(v) for v in x.shape)
     desc = make_desc(N, C, H, W, 1, int(R), int(S), int(stride), int(pad))
     ho, wo = isc_out_shape(desc)
     ldc = N * ho * wo if ldc is None else int(ldc)
-    col = torch.empty((C * R * S, ldc), dtype=torch.float32, device=x.device)
+    if out is None:
+        col = torch.empty((C * R * S, ldc), dtype=torch.float32, device=x.device)
+    else:
+        col = out
+        if (not isinstance(col, torch.Tensor) or col.dtype != torch.float32 or not col.is_contiguous()
+                or tuple(col.shape) != (C * R * S, ldc) or col.device != x.device):
+            raise ValueError("out must be a contiguous float32 [C*R*S, ldc] tensor on x's device")
     _check(lib().isc_im2col(ctypes.byref(desc), x.data_ptr(), col.data_ptr(), ldc,
                             _stream(stream)), "isc_im2col")
     return col
