@@ -4,10 +4,11 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--all --out FILE]
 
 A step is one pass of the whole hot path over one batch of synthetic input
-already resident in HBM: isc_conv2d on the AUTO path, i.e. compaction of the
-input (ISC step 1), the device-side sparse/dense decision, and the
-zero-skipping convolution with its transposed write-out (ISC steps 2-3); the
-dense kernels are launched too and exit on the decision.  Steps are replayed
+already resident in HBM: isc_conv2d on the AUTO path, i.e. the nonzero count
+of the input and the device-side sparse/dense decision, then the
+zero-skipping convolution (ISC steps 1-3: compaction on the fly for this
+layer, the multiply-adds over nonzeros only, the write-out to NCHW); the
+dense kernel is launched too and exits on the decision.  Steps are replayed
 from a HIP graph (the layer is launch-bound at microseconds per step).
 
 Workload: LeNet conv2 (20 -> 50 maps, 12 x 12, 5 x 5, stride 1, no pad) at
@@ -16,7 +17,7 @@ weights), the sweep configuration whose 0.9 point the metric is quoted at.
 
 Prints ONE JSON line: value = dense-equivalent TFLOP/s of the step
 (2*N*K*C*R*S*Ho*Wo per step), speedup against the same GPU's dense path
-(im2col + fp32-MFMA GEMM), the sparsity sweep 0.5 .. 0.99, the roofline of
+(fp32-MFMA GEMM with the im2col gather inside), the sparsity sweep 0.5 .. 0.99, the roofline of
 the dominant kernel (timed with HIP events on the launch stream), and the
 CPU oracle timed on a bounded sample of the same workload.
 """
@@ -121,9 +122,10 @@ class LayerRun:
         self.Ho, self.Wo = isc.isc_out_shape(self.desc)
         self.y = torch.empty((L.N, L.K, self.Ho, self.Wo), device="cuda")
         self.ws = {p: isc.workspace(self.desc, p) for p in ("auto", "sparse", "dense")}
+        self.kernel = isc.isc_sparse_kernel(self.desc)  # the sparse path's main kernel
         self.lists = isc.isc_compact(self.x)
         self.wt = isc.isc_repack_filter(self.w)
-        self.col = torch.empty((L.C * L.R * L.S, L.N * self.Ho * self.Wo), device="cuda")
+        self.col = None  # im2col matrix, allocated by im2col() when first used
         torch.cuda.synchronize()
         self.nnz = int(self.lists[2].item())
         self.sparsity = 1.0 - self.nnz / x.size
@@ -139,12 +141,21 @@ class LayerRun:
         return lambda: self.isc.isc_compact(self.x, out=self.lists)
 
     def sparse_kernel(self):
+        """The sparse path's main kernel alone, through its own entry point:
+        on-the-fly compaction (isc_sparse_conv_fused) or the kernel over
+        compacted lists (isc_sparse_conv)."""
         L = self.layer
+        if self.kernel == "fused":
+            return lambda: self.isc.isc_sparse_conv_fused(self.x, self.w, L.T, L.P, out=self.y)
         return lambda: self.isc.isc_sparse_conv(self.x.shape, self.lists, self.wt, L.T, L.P,
                                                 out=self.y)
 
     def im2col(self):
+        """The stand-alone im2col entry point (not on the dense path, which
+        gathers inside its GEMM); kept for the counter runs."""
         L = self.layer
+        if self.col is None:
+            self.col = self.torch.empty((L.C * L.R * L.S, L.N * self.Ho * self.Wo), device="cuda")
         return lambda: self.isc.isc_im2col(self.x, L.R, L.S, L.T, L.P, out=self.col)
 
     def measure(self, steps, warmup, graphs=True):
@@ -159,8 +170,6 @@ class LayerRun:
         reps = max(100, steps)
         res["t_compact_ms"] = kernel_time_ms(torch, self.compact(), reps, graphs)
         res["t_sparse_kernel_ms"] = kernel_time_ms(torch, self.sparse_kernel(), reps, graphs)
-        res["t_im2col_ms"] = kernel_time_ms(torch, self.im2col(), reps // 4, graphs, inner=5)
-        res["t_gemm_ms"] = max(0.0, res["t_dense_ms"] - res["t_im2col_ms"])
         return res
 
     def summary(self, res):
@@ -179,10 +188,8 @@ class LayerRun:
         out["nonzero_mac_per_s_auto"] = nzm / (res["t_auto_ms"] * 1e-3)
         out["speedup_auto_vs_dense"] = round(res["t_dense_ms"] / res["t_auto_ms"], 3)
         out["speedup_sparse_vs_dense"] = round(res["t_dense_ms"] / res["t_sparse_ms"], 3)
-        out["speedup_sparse_vs_gemm_only"] = round(res["t_gemm_ms"] / res["t_sparse_ms"], 3)
         out["sparse_kernel_tflops_nonzero"] = round(2 * nzm / (res["t_sparse_kernel_ms"] * 1e-3) / 1e12, 3)
-        out["gemm_frac_mfma_peak"] = round(f / (res["t_gemm_ms"] * 1e-3) / 1e12 / MFMA_F32_PEAK_TFLOPS, 4) \
-            if res["t_gemm_ms"] > 0 else None
+        out["dense_frac_mfma_peak"] = round(f / (res["t_dense_ms"] * 1e-3) / 1e12 / MFMA_F32_PEAK_TFLOPS, 4)
         return out
 
 
@@ -226,6 +233,82 @@ def cpu_baseline(layer, budget_s=10.0):
             "one_thread": {"value": round(value1, 6), "unit": "TFLOP/s", "cores": 1,
                            "sample": "%d x images 0..%d, %.2f s" % (reps1, n1 - 1, dt1)},
             "cpu_model": _cpu_model()}
+
+
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "lenet_conv2_s0.9_hbm_counters.md")
+SPARSE_SOURCES = [os.path.join(ROOT, "paper_1704_07724_amd", "csrc", f)
+                  for f in ("sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp")]
+
+
+def sparse_source_hash() -> str:
+    """First 16 hex digits of the SHA-256 of the headline sparse kernel's
+    sources, concatenated in SPARSE_SOURCES order."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in SPARSE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def counted_traffic():
+    """HBM bytes per launch of the sparse kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a copy kernel), or None when
+    the kernel's sources have changed since the counters were taken."""
+    import re
+    try:
+        text = open(COUNTERS_FILE).read()
+    except OSError:
+        return None
+    m = re.search(r"^traffic_bytes_per_launch (\S+): read=(\d+) write=(\d+) source_sha256=([0-9a-f]+)",
+                  text, re.M)
+    if not m or m.group(4) != sparse_source_hash():
+        return None
+    return {"kernel": m.group(1), "read_bytes": int(m.group(2)), "write_bytes": int(m.group(3)),
+            "bytes": int(m.group(2)) + int(m.group(3)), "source": os.path.relpath(COUNTERS_FILE, ROOT)}
+
+
+def algorithmic_bytes(run) -> dict:
+    """Bytes each kernel of the path must move at least once, per launch:
+    compaction reads the input and writes the lists, the sparse kernel reads
+    lists, row offsets and repacked weights and writes the output (the fused
+    kernel reads the input and the filter instead), im2col
+    reads the input and writes the unrolled matrix."""
+    L = run.layer
+    planes = L.N * L.C
+    row_ptr = planes * (L.H + 1) * 4
+    x_bytes = run.x_host.size * 4
+    y_bytes = L.N * L.K * run.Ho * run.Wo * 4
+    kp = (L.K + 63) // 64 * 64
+    if run.kernel == "fused":   # reads x and the KCRS filter once, writes y
+        sparse = x_bytes + L.K * L.C * L.R * L.S * 4 + y_bytes
+    else:                       # lists, row offsets, repacked filter; writes y
+        sparse = run.nnz * 8 + row_ptr + L.C * L.R * L.S * kp * 4 + y_bytes
+    return {
+        "compact": x_bytes + run.nnz * 8 + row_ptr,
+        "sparse_kernel": sparse,
+        "im2col": x_bytes + L.C * L.R * L.S * L.N * run.Ho * run.Wo * 4,
+    }
+
+
+def probe(torch, isc, layer, n):
+    """Short eager program for counter runs: a copy kernel moving a known
+    number of bytes (the scale of the HBM counters), then each kernel of the
+    layer n times."""
+    run = LayerRun(torch, isc, layer)
+    src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
+    dst = torch.empty_like(src)
+    steps = [("copy", lambda: torch.mul(src, 1.0, out=dst)), ("compact", run.compact()),
+             ("sparse_kernel", run.sparse_kernel()), ("im2col", run.im2col())]
+    for name, fn in steps:
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        print("# probe %s x%d done" % (name, n), file=sys.stderr, flush=True)
+    alg = algorithmic_bytes(run)
+    alg["copy"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
+    print(json.dumps({"probe": layer.name, "launches_each": n, "nnz": run.nnz,
+                      "algorithmic_bytes": alg}), flush=True)
 
 
 def _cpu_model():
@@ -293,7 +376,7 @@ def main():
     t_kernel = res["t_sparse_kernel_ms"]
     achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
     traffic = counted_traffic()
-    roofline = {"bound": "alu", "kernel": "sparse_conv_reg_kernel (isc_sparse_conv)",
+    roofline = {"bound": "alu", "kernel": "sparse_conv_%s_kernel" % head.kernel,
                 "achieved": round(achieved, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4),
                 "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
@@ -303,8 +386,7 @@ def main():
 
     alg = algorithmic_bytes(head)
     hbm = {}
-    for kern, t_key in (("compact", "t_compact_ms"), ("sparse_kernel", "t_sparse_kernel_ms"),
-                        ("im2col", "t_im2col_ms")):
+    for kern, t_key in (("compact", "t_compact_ms"), ("sparse_kernel", "t_sparse_kernel_ms")):
         gbs = alg[kern] / (res[t_key] * 1e-3) / 1e9
         hbm[kern] = {"algorithmic_bytes": alg[kern], "ms": round(res[t_key], 6),
                      "GB/s": round(gbs, 1), "frac": round(gbs / HBM_PEAK_GBS, 4)}
@@ -318,7 +400,7 @@ def main():
             s = run.summary(r)
             sweep.append({k: s[k] for k in (
                 "target_sparsity", "measured_sparsity", "t_auto_ms", "t_sparse_ms", "t_dense_ms",
-                "t_compact_ms", "t_sparse_kernel_ms", "t_gemm_ms", "tflops_auto", "tflops_sparse",
+                "t_compact_ms", "t_sparse_kernel_ms", "tflops_auto", "tflops_sparse",
                 "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense",
                 "speedup_sparse_vs_dense", "sparse_kernel_tflops_nonzero")})
             if run is not head:
@@ -336,7 +418,6 @@ def main():
                    "sparsity": head_layer.sparsity, "path": "auto", "threshold": 0.9,
                    "launch": "eager" if args.no_graph else "hip_graph"},
         "speedup_vs_dense": hs["speedup_auto_vs_dense"],
-        "speedup_vs_dense_gemm_only": round(res["t_gemm_ms"] / res["t_auto_ms"], 3),
         "nonzero_mac_per_s": hs["nonzero_mac_per_s_auto"],
         "measured_sparsity": hs["measured_sparsity"],
         "dense_path_tflops": hs["tflops_dense"],

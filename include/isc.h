@@ -9,8 +9,9 @@
  * Convolution") and multiplies only those with K-contiguous weight vectors
  * (ISC step 2), accumulating an output tile that is written out transposed
  * to NCHW (ISC step 3).  The dense path is the matrix-multiplication
- * formulation M_K x M_I = M_O of Fig. 3 (im2col followed by a GEMM), the
- * paper's baseline.  A dispatcher picks one by measured input sparsity.
+ * formulation M_K x M_I = M_O of Fig. 3 (the im2col matrix M_I times the
+ * filter matrix M_K), the paper's baseline; here M_I is gathered from the
+ * input inside the GEMM rather than written out.  A dispatcher picks one by measured input sparsity.
  *
  * Conventions shared by every entry point
  *   - All tensors are fp32 (indices int32/uint32), dense and row-major:
@@ -27,9 +28,10 @@
  *     validation error nothing is enqueued and no output is touched.  No C++
  *     exception crosses the ABI and nothing is printed.
  *   - Limits: every dimension >= 1, stride >= 1, pad >= 0, Ho and Wo >= 1,
- *     H and W <= 65535, and N*C*H*W, N*K*Ho*Wo, K*C*R*S and the im2col
- *     matrix (C*R*S rows of the padded column count) each below 2^31
- *     elements.  Float pointers must be 4-byte aligned, workspaces 256-byte
+ *     H and W <= 65535, and N*C*H*W, N*K*Ho*Wo, K*C*R*S and N*Ho*Wo each
+ *     below 2^31 elements; when C*R*S >= 2^16 the dense path materialises
+ *     the im2col matrix (C*R*S rows of N*Ho*Wo rounded up to 256 columns),
+ *     which must then be below 2^31 elements too.  Float pointers must be 4-byte aligned, workspaces 256-byte
  *     aligned.
  *   - Calls that share a workspace must not overlap in time (same stream, or
  *     synchronised).
@@ -61,7 +63,7 @@ typedef struct isc_conv_desc {
 typedef enum isc_path {
     ISC_PATH_AUTO = 0,   /* compact, then sparse if sparsity >= threshold else dense */
     ISC_PATH_SPARSE = 1, /* compaction + zero-skipping convolution */
-    ISC_PATH_DENSE = 2   /* im2col + MFMA GEMM */
+    ISC_PATH_DENSE = 2   /* MFMA GEMM of Fig. 3 (im2col gathered in the GEMM) */
 } isc_path;
 
 /* One entry of the nonzero list of ISC step 1: the value (bit-exact copy of
@@ -91,7 +93,8 @@ enum isc_status {
 int isc_out_shape(const isc_conv_desc *d, int32_t *Ho, int32_t *Wo);
 
 /* Bytes of device workspace isc_conv2d needs for this descriptor and path
- * (AUTO needs the sparse and dense buffers).  Host-only.  Errors: NULL,
+ * (AUTO needs the sparse and dense buffers; the dense path needs an im2col
+ * buffer only when C*R*S >= 2^16).  Host-only.  Errors: NULL,
  * SHAPE, LIMIT, PATH. */
 int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes);
 
@@ -171,6 +174,35 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
  * HIP. */
 int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz *nz,
                     const float *wt, float *y, void *stream);
+
+/* ISC steps 1-3 (Sec. "Sparse Convolution") in one launch with no workspace:
+ * each wavefront compacts the input rows it needs on the fly (a ballot of
+ * the zero test, walked in row-major order) and the filter is read in its
+ * KCRS layout.  The kernel isc_conv2d's sparse path runs when
+ * isc_sparse_kernel reports ISC_KERNEL_FUSED; no sparse/dense decision.
+ *   x, w: device inputs as for isc_conv2d.  y: device output, fully
+ *     written, must not overlap x or w.
+ * Errors: NULL, SHAPE, LIMIT (shape not eligible: stride 1, square 1x1/3x3/
+ * 5x5 filter, K <= 64, Wo <= 28, filter within LDS), ALIAS, ALIGN, DEVICE,
+ * HIP. */
+int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w, float *y,
+                          void *stream);
+
+/* Which kernel isc_conv2d's sparse path runs for this descriptor, reported in
+ * *kernel: ISC_KERNEL_FUSED (compaction on the fly, isc_sparse_conv_fused),
+ * else the kernel over compacted lists that isc_sparse_conv also runs:
+ * ISC_KERNEL_RESIDENT (filter resident in LDS), ISC_KERNEL_RING (filter
+ * streamed through LDS) or ISC_KERNEL_GENERIC (any filter and stride);
+ * ISC_KERNEL_NONE if no sparse kernel fits (AUTO then runs dense).
+ * Host-only.  Errors: NULL, SHAPE, LIMIT. */
+enum isc_kernel {
+    ISC_KERNEL_NONE = 0,
+    ISC_KERNEL_FUSED = 1,
+    ISC_KERNEL_RESIDENT = 2,
+    ISC_KERNEL_RING = 3,
+    ISC_KERNEL_GENERIC = 4
+};
+int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel);
 
 /* The unrolled input matrix M_I of the matrix-multiplication formulation
  * (Sec. "Sparse Convolution", Fig. 3), with the batch as extra columns:

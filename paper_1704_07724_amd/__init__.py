@@ -28,7 +28,8 @@ STATUS = {
 }
 EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
-           "isc_im2col", "isc_gemm_f32", "isc_status_str", "isc_version")
+           "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
+           "isc_status_str", "isc_version")
 
 
 class IscError(RuntimeError):
@@ -70,7 +71,9 @@ def lib():
     L.isc_sparse_conv.argtypes = [dp, vp, vp, vp, vp, vp]
     L.isc_im2col.argtypes = [dp, vp, vp, i64, vp]
     L.isc_gemm_f32.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
-    for name in EXPORTS[:10]:
+    L.isc_sparse_conv_fused.argtypes = [dp, vp, vp, vp, vp]
+    L.isc_sparse_kernel.argtypes = [dp, ctypes.POINTER(i32)]
+    for name in EXPORTS[:12]:
         getattr(L, name).restype = ctypes.c_int
     L.isc_status_str.argtypes = [ctypes.c_int]
     L.isc_status_str.restype = ctypes.c_char_p
@@ -250,6 +253,40 @@ def isc_repack_filter(w, out=None, stream=None):
     _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), data.data_ptr(),
                                    _stream(stream)), "isc_repack_filter")
     return RepackedFilter(data, K, C, R, S)
+
+
+KERNEL_NAMES = {0: "none", 1: "fused", 2: "resident", 3: "ring", 4: "generic"}
+
+
+def isc_sparse_kernel(desc: ConvDesc) -> str:
+    """Which kernel isc_conv2d's sparse path runs for desc: "fused" (on-the-fly
+    compaction), "resident", "ring" or "generic" (over compacted lists), or
+    "none"."""
+    which = ctypes.c_int32(-1)
+    _check(lib().isc_sparse_kernel(ctypes.byref(desc), ctypes.byref(which)), "isc_sparse_kernel")
+    return KERNEL_NAMES[which.value]
+
+
+def isc_sparse_conv_fused(x, w, stride=1, pad=0, out=None, stream=None):
+    """ISC steps 1-3 in one launch (compaction on the fly, KCRS filter), no
+    workspace; returns y [N, K, Ho, Wo].  Raises IscError (LIMIT) for shapes
+    the kernel does not take."""
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    w = _dev_f32(w, "w")
+    N, C, H, W = (int(v) for v in x.shape)
+    K, C2, R, S = (int(v) for v in w.shape)
+    if C != C2:
+        raise ValueError("channel mismatch")
+    desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
+    ho, wo = isc_out_shape(desc)
+    if out is None:
+        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=x.device)
+    elif not out.is_contiguous() or tuple(out.shape) != (N, K, ho, wo):
+        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+    _check(lib().isc_sparse_conv_fused(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                                       _stream(stream)), "isc_sparse_conv_fused")
+    return out
 
 
 def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):

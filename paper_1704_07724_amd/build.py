@@ -11,6 +11,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -37,28 +38,47 @@ DEVICE_FLAGS = [
 ]
 
 
-# Per-file extra flags.  sparse_reg.hip keeps accumulator tiles in registers
-# through a compile-time dispatch tree on a wave-uniform value:
+# Per-file extra flags.  The register-tile kernels (sparse_reg, sparse_res,
+# sparse_fused) keep accumulator tiles in registers through a compile-time
+# dispatch tree on a wave-uniform value:
 #  - SimplifyCFG's sinking of the common tails of the tree's leaves turns
 #    constant register indices into selected pointers and forces the tile to
 #    scratch memory, so sinking is disabled;
 #  - every branch of the tree is uniform, so the CFG structurizer is told to
 #    leave uniform regions alone (otherwise its flow blocks add scalar work
 #    per level and break the in-place accumulate into copy chains).
-FILE_FLAGS = {
-    "sparse_reg.hip": ["-mllvm", "-simplifycfg-sink-common=false",
-                       "-mllvm", "-structurizecfg-skip-uniform-regions"],
-}
+_TILE_FLAGS = ["-mllvm", "-simplifycfg-sink-common=false",
+               "-mllvm", "-structurizecfg-skip-uniform-regions"]
+FILE_FLAGS = {"sparse_reg.hip": _TILE_FLAGS, "sparse_res.hip": _TILE_FLAGS, "sparse_fused.hip": _TILE_FLAGS}
+
+
+def _spills(remarks: str) -> list:
+    """Kernels whose resource-usage remark reports scratch (register spills
+    or stack) -- a performance bug for the register-tile kernels."""
+    out, name = [], None
+    for line in remarks.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and name and int(m.group(1)) > 0:
+            out.append((name, int(m.group(1))))
+    return out
 
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + DEVICE_FLAGS + FILE_FLAGS.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
+    cmd = ([HIPCC] + DEVICE_FLAGS + FILE_FLAGS.get(os.path.basename(src), []) +
+           ["-Rpass-analysis=kernel-resource-usage", "-c", src, "-o", obj])
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr))
+    for name, size in _spills(r.stderr):
+        sys.stderr.write("warning: %s: kernel %s uses %d bytes of scratch per lane\n"
+                         % (os.path.basename(src), name, size))
     warn = "\n".join(l for l in r.stderr.splitlines()
-                     if "packed-fp32-ops" not in l and l.strip())
+                     if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l
+                     and "remark:" not in l and l.strip())
     if warn:
         sys.stderr.write(warn + "\n")
     return obj

@@ -9,9 +9,17 @@
 // the first element of a row writes that row's offset.  The per-plane lists
 // are dense in fixed H*W slots, so the output is unique and needs no second
 // pass.  Traffic: 4 bytes read per input element, 8 bytes written per
-// nonzero, 4 bytes per row offset.  A second, one-workgroup kernel adds the
-// per-plane counts into the total the dispatcher reads.
+// nonzero, 4 bytes per row offset.
+//
+// The sparse path runs the compaction inside one "prep" launch together with
+// the filter repack (ISC step 2's K-contiguous layout: extra workgroups each
+// transpose a 64 x 64 tile), and each compaction workgroup stores its own
+// nonzero count; the kernels after it add those counts for the sparse/dense
+// decision.  The stand-alone entry point instead sums the per-plane counts
+// with a one-workgroup kernel.
 #include "isc_internal.hpp"
+
+#include <algorithm>
 
 namespace isc {
 namespace {
@@ -24,11 +32,12 @@ __device__ __forceinline__ uint32_t lanes_below(unsigned long long mask) {
                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-__global__ __launch_bounds__(kWaves * 64)
-void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
-                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz) {
+// Compact planes p = first, first + stride, ... (< planes) with the calling
+// wavefront; returns the number of nonzeros it listed (wave-uniform).
+__device__ __forceinline__ uint32_t compact_planes(const float *__restrict__ x, int planes, int H, int W,
+                                                   int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz,
+                                                   int first, int stride) {
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
     const int HW = H * W;
     // (row, column) of this lane's element in the first chunk, and the step
     // that moves it 64 elements further in row-major order
@@ -36,8 +45,9 @@ void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
     const int x_first = lane - y_first * W;
     const int dy = 64 / W;
     const int dx = 64 - dy * W;
+    uint32_t listed = 0;
 
-    for (int p = blockIdx.x * kWaves + wave; p < planes; p += gridDim.x * kWaves) {
+    for (int p = first; p < planes; p += stride) {
         const float *xp = x + static_cast<size_t>(p) * HW;
         NzEntry *np = nz + static_cast<size_t>(p) * HW;
         int32_t *rp = row_ptr + static_cast<size_t>(p) * (H + 1);
@@ -75,7 +85,16 @@ void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
             }
         }
         if (lane == 0) rp[H] = static_cast<int32_t>(base);
+        listed += base;
     }
+    return listed;
+}
+
+__global__ __launch_bounds__(kWaves * 64)
+void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
+                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz) {
+    const int wave = threadIdx.x >> 6;
+    compact_planes(x, planes, H, W, row_ptr, nz, blockIdx.x * kWaves + wave, gridDim.x * kWaves);
 }
 
 // Total of the per-plane counts (row_ptr[p][H]) by one workgroup, written
@@ -101,15 +120,146 @@ void count_kernel(const int32_t *__restrict__ row_ptr, int planes, int H,
     }
 }
 
+// One 64 x 64 tile of the filter repack through LDS: reads along q = (c, r,
+// s), writes along k:  wt[q * Kp + k] = w[k * CRS + q]  (0 for k >= K).
+__device__ __forceinline__ void repack_tile(const float *__restrict__ w, int K, int Kp, int CRS,
+                                            float *__restrict__ wt, int qt, int kt, float (&tile)[64][65]) {
+    const int q0 = qt * 64, k0 = kt * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += kWaves) {
+        const int k = k0 + i, q = q0 + tx;
+        tile[i][tx] = (k < K && q < CRS) ? w[static_cast<size_t>(k) * CRS + q] : 0.0f;
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += kWaves) {
+        const int q = q0 + i, k = k0 + tx;
+        if (q < CRS && k < Kp) wt[static_cast<size_t>(q) * Kp + k] = tile[tx][i];
+    }
+}
+
+__global__ __launch_bounds__(kWaves * 64)
+void repack_filter_kernel(const float *__restrict__ w, int K, int Kp, int CRS, float *__restrict__ wt) {
+    __shared__ float tile[64][65];
+    repack_tile(w, K, Kp, CRS, wt, blockIdx.x, blockIdx.y, tile);
+}
+
+// Workgroups [0, groups) compact (grid-stride over planes) and store their
+// count in parts[b]; workgroup 0 also zeroes parts[groups .. nparts).
+// Workgroups from `groups` on repack one filter tile each.
+__global__ __launch_bounds__(kWaves * 64)
+void prep_kernel(const float *__restrict__ x, int planes, int H, int W, int32_t *__restrict__ row_ptr,
+                 NzEntry *__restrict__ nz, uint32_t *__restrict__ parts, int groups, int nparts,
+                 const float *__restrict__ w, int K, int Kp, int CRS, int qtiles, float *__restrict__ wt) {
+    __shared__ float tile[64][65];
+    __shared__ uint32_t wave_count[kWaves];
+    const int b = blockIdx.x;
+    if (b >= groups) {
+        const int t = b - groups;
+        repack_tile(w, K, Kp, CRS, wt, t % qtiles, t / qtiles, tile);
+        return;
+    }
+    const int wave = threadIdx.x >> 6;
+    const uint32_t listed = compact_planes(x, planes, H, W, row_ptr, nz, b * kWaves + wave, groups * kWaves);
+    if ((threadIdx.x & 63) == 0) wave_count[wave] = listed;
+    if (b == 0) {
+        for (int i = groups + static_cast<int>(threadIdx.x); i < nparts; i += kWaves * 64) parts[i] = 0u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t s = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) s += wave_count[i];
+        parts[b] = s;
+    }
+}
+
+// Nonzero count of x (total elements) in per-workgroup parts, for the
+// sparse/dense decision when no compaction runs: workgroup b counts one
+// contiguous chunk; workgroup 0 also zeroes parts[groups .. nparts).
+constexpr int kCountUnroll = 8;
+
+__global__ __launch_bounds__(kWaves * 64)
+void count_parts_kernel(const float *__restrict__ x, int64_t total, uint32_t *__restrict__ parts, int groups,
+                        int nparts) {
+    __shared__ uint32_t wave_count[kWaves];
+    const int b = blockIdx.x;
+    const int64_t chunk = (total + groups - 1) / groups;
+    const int64_t beg = b * chunk;
+    const int64_t end = min(total, beg + chunk);
+    uint32_t cnt = 0;
+    for (int64_t e0 = beg + threadIdx.x; e0 < end; e0 += static_cast<int64_t>(kWaves) * 64 * kCountUnroll) {
+        uint32_t bits[kCountUnroll];
+#pragma unroll
+        for (int u = 0; u < kCountUnroll; ++u) {
+            const int64_t e = e0 + static_cast<int64_t>(u) * kWaves * 64;
+            bits[u] = e < end ? __float_as_uint(x[e]) : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kCountUnroll; ++u) cnt += (bits[u] & 0x7fffffffu) != 0u ? 1u : 0u;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    if ((threadIdx.x & 63) == 0) wave_count[threadIdx.x >> 6] = cnt;
+    if (b == 0) {
+        for (int i = groups + static_cast<int>(threadIdx.x); i < nparts; i += kWaves * 64) parts[i] = 0u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t s = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i) s += wave_count[i];
+        parts[b] = s;
+    }
+}
+
+int compact_groups(int planes) {
+    // one wavefront per plane, enough workgroups to cover 256 CUs many times
+    return std::max(1, std::min((planes + kWaves - 1) / kWaves, 8192));
+}
+
 }  // namespace
 
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s) {
-    // one wavefront per plane; enough workgroups to cover 256 CUs many times
-    int groups = (planes + kWaves - 1) / kWaves;
-    if (groups > 8192) groups = 8192;
-    compact_kernel<<<groups, kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz);
+    compact_kernel<<<compact_groups(planes), kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz);
     count_kernel<<<1, kCountThreads, 0, s>>>(row_ptr, planes, H, counter);
+    return hipGetLastError();
+}
+
+size_t repacked_filter_floats(int K, int C, int R, int S) {
+    const size_t Kp = (static_cast<size_t>(K) + 63) / 64 * 64;
+    return static_cast<size_t>(C) * R * S * Kp;
+}
+
+hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, float *wt, hipStream_t s) {
+    const int CRS = C * R * S;
+    const int Kp = (K + 63) / 64 * 64;
+    dim3 grid((CRS + 63) / 64, Kp / 64);
+    repack_filter_kernel<<<grid, kWaves * 64, 0, s>>>(w, K, Kp, CRS, wt);
+    return hipGetLastError();
+}
+
+hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s) {
+    const int64_t per = static_cast<int64_t>(kWaves) * 64 * kCountUnroll * 2;  // elements per workgroup, at least
+    const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxParts, (total + per - 1) / per)));
+    const int np = (groups + 3) / 4 * 4;
+    count_parts_kernel<<<groups, kWaves * 64, 0, s>>>(x, total, parts, groups, np);
+    *nparts = np;
+    return hipGetLastError();
+}
+
+hipError_t launch_prep(const float *x, int planes, int H, int W, int32_t *row_ptr, NzEntry *nz,
+                       uint32_t *parts, int *nparts, const float *w, int K, int C, int R, int S,
+                       float *wt, hipStream_t s) {
+    const int groups = std::min(compact_groups(planes), kMaxParts);
+    const int np = (groups + 3) / 4 * 4;
+    const int CRS = C * R * S;
+    const int Kp = (K + 63) / 64 * 64;
+    const int qtiles = (CRS + 63) / 64;
+    const int tiles = qtiles * (Kp / 64);
+    prep_kernel<<<groups + tiles, kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz, parts, groups, np, w, K, Kp,
+                                                       CRS, qtiles, wt);
+    *nparts = np;
     return hipGetLastError();
 }
 

@@ -2,10 +2,13 @@
 // (Sec. "Sparse Convolution", Fig. 3), M_K [K x RSC] * M_I [RSC x HoWo] =
 // M_O [K x HoWo], with the batch appended as extra columns of M_I.
 //
-// im2col writes M_I to the workspace (row (c, r, s), column (n, i, j)); the
-// GEMM multiplies the filter tensor, read in place as the row-major K x CRS
-// matrix M_K, by M_I on the fp32 matrix cores (v_mfma_f32_32x32x2_f32) and
-// scatters each output column back to NCHW in its epilogue.
+// M_I has row (c, r, s) and column (n, i, j).  The GEMM multiplies the
+// filter tensor, read in place as the row-major K x CRS matrix M_K, by M_I on
+// the fp32 matrix cores (v_mfma_f32_32x32x2_f32) and scatters each output
+// column back to NCHW in its epilogue.  For convolutions it gathers M_I from
+// the input while loading its B tiles (implicit im2col: no M_I in memory);
+// im2col_kernel writes M_I out for the stand-alone entry point and for
+// C*R*S >= 2^16.
 #include "isc_internal.hpp"
 
 #include <algorithm>
@@ -21,12 +24,7 @@ __global__ __launch_bounds__(256)
 void im2col_kernel(const float *__restrict__ x, int C, int H, int W, int R, int S, int T, int P,
                    int Ho, int Wo, int ncols, float *__restrict__ col, int64_t ldc, int rows_total,
                    Decision dec) {
-    if (!decision_says_run(dec)) return;
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0 && dec.record) {
-        // dense-only call: no compaction ran, so there is no count
-        dec.record->nnz_total = ~0ull;
-        dec.record->path_taken = 2u;
-    }
+    if (!decision_gate(dec, 2u)) return;
     const int64_t j = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
     if (j >= ldc) return;
     const bool real = j < ncols;
@@ -82,12 +80,22 @@ struct GemmArgs {
     int64_t ldc;
     int conv_hw;  // > 0: scatter column n to NCHW with Ho*Wo = conv_hw
     Decision dec;
+    // implicit im2col: B[k][j] is gathered from the input x instead of read
+    // from b (k = (c, r, s), j = (n, oy, ox))
+    const float *x;
+    int C, H, W, T, P, Wo, RS, S;
+    uint32_t mRS, mS;  // ceil(2^32 / RS), ceil(2^32 / S) (unused when the divisor is 1)
 };
 
-template <int WAVES_M, int WM, int WN, bool A_VEC, bool B_PADDED>
+// k / d for k < 2^16, d < 2^16, with m = ceil(2^32 / d) (d > 1)
+__device__ __forceinline__ int divm(int k, int d, uint32_t m) {
+    return d == 1 ? k : static_cast<int>(__umulhi(static_cast<uint32_t>(k), m));
+}
+
+template <int WAVES_M, int WM, int WN, bool A_VEC, bool B_PADDED, bool IMPLICIT>
 __global__ __launch_bounds__(256)
 void gemm_f32_kernel(GemmArgs g) {
-    if (!decision_says_run(g.dec)) return;
+    if (!decision_gate(g.dec, 2u)) return;
     constexpr int WAVES_N = 4 / WAVES_M;
     constexpr int BM = WAVES_M * WM * 32;
     constexpr int BN = WAVES_N * WN * 32;
@@ -111,6 +119,34 @@ void gemm_f32_kernel(GemmArgs g) {
     constexpr int B_PER = (B_F4 + 255) / 256;
     float4 ra[A_PER];
     float4 rb[B_PER];
+
+    // implicit im2col: this thread's B columns are fixed for the whole
+    // K loop; keep each column's input offset and top-left input position
+    int coff[IMPLICIT ? B_PER : 1][4], iy0[IMPLICIT ? B_PER : 1][4], ix0[IMPLICIT ? B_PER : 1][4];
+    if constexpr (IMPLICIT) {
+        const int HW = g.H * g.W;
+#pragma unroll
+        for (int i = 0; i < B_PER; ++i) {
+            const int nq = (tid + i * 256) % (BN / 4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int j = n0 + nq * 4 + e;
+                if (j < N) {
+                    const int img = j / g.conv_hw;
+                    const int p = j - img * g.conv_hw;
+                    const int oy = p / g.Wo;
+                    const int ox = p - oy * g.Wo;
+                    iy0[i][e] = oy * g.T - g.P;
+                    ix0[i][e] = ox * g.T - g.P;
+                    coff[i][e] = img * g.C * HW + iy0[i][e] * g.W + ix0[i][e];
+                } else {
+                    iy0[i][e] = -(1 << 30);  // fails every bounds test
+                    ix0[i][e] = 0;
+                    coff[i][e] = 0;
+                }
+            }
+        }
+    }
 
     auto load_slice = [&](int k0) {
         const bool full_k = k0 + BK <= Kd;
@@ -146,7 +182,24 @@ void gemm_f32_kernel(GemmArgs g) {
                 const int nq = idx % (BN / 4);
                 const int k = k0 + row;
                 const int nn = n0 + nq * 4;
-                if (k < Kd) {
+                if (IMPLICIT) {
+                    if (k < Kd) {
+                        const int c = divm(k, g.RS, g.mRS);
+                        const int rs = k - c * g.RS;
+                        const int r = divm(rs, g.S, g.mS);
+                        const int sx = rs - r * g.S;
+                        const int roff = (c * g.H + r) * g.W + sx;
+                        float e4[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int iy = iy0[i][e] + r, ix = ix0[i][e] + sx;
+                            const bool in = static_cast<unsigned>(iy) < static_cast<unsigned>(g.H) &&
+                                            static_cast<unsigned>(ix) < static_cast<unsigned>(g.W);
+                            e4[e] = in ? g.x[static_cast<int64_t>(coff[i][e]) + roff] : 0.f;
+                        }
+                        v = make_float4(e4[0], e4[1], e4[2], e4[3]);
+                    }
+                } else if (k < Kd) {
                     const float *src = g.b + static_cast<size_t>(k) * g.ldb + nn;
                     if (B_PADDED) {
                         v = *reinterpret_cast<const float4 *>(src);
@@ -248,19 +301,31 @@ void gemm_f32_kernel(GemmArgs g) {
 }
 
 template <int WAVES_M, int WM, int WN>
-hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, hipStream_t s) {
+hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, bool implicit, hipStream_t s) {
     constexpr int BM = WAVES_M * WM * 32;
     constexpr int BN = (4 / WAVES_M) * WN * 32;
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
-    if (a_vec) {
-        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, true, true><<<grid, 256, 0, s>>>(g);
-        else gemm_f32_kernel<WAVES_M, WM, WN, true, false><<<grid, 256, 0, s>>>(g);
+    if (implicit) {
+        if (a_vec) gemm_f32_kernel<WAVES_M, WM, WN, true, false, true><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, true><<<grid, 256, 0, s>>>(g);
+    } else if (a_vec) {
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, true, true, false><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, true, false, false><<<grid, 256, 0, s>>>(g);
     } else {
-        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, false, true><<<grid, 256, 0, s>>>(g);
-        else gemm_f32_kernel<WAVES_M, WM, WN, false, false><<<grid, 256, 0, s>>>(g);
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, false, true, false><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, false><<<grid, 256, 0, s>>>(g);
     }
     return hipGetLastError();
 }
+
+hipError_t launch_gemm_any(const GemmArgs &g, bool a_vec, bool b_vec, bool implicit, hipStream_t s) {
+    // tile height follows M: 32 (skinny), 64, or 128 rows per workgroup
+    if (g.M <= 32) return launch_gemm_t<1, 1, 2>(g, a_vec, b_vec, implicit, s);   // 32 x 256
+    if (g.M <= 64) return launch_gemm_t<2, 1, 2>(g, a_vec, b_vec, implicit, s);   // 64 x 128
+    return launch_gemm_t<2, 2, 2>(g, a_vec, b_vec, implicit, s);                // 128 x 128
+}
+
+uint32_t div_magic(int d) { return d <= 1 ? 0u : static_cast<uint32_t>((0x100000000ull + d - 1) / d); }
 
 }  // namespace
 
@@ -277,13 +342,33 @@ hipError_t launch_im2col(const float *x, int N, int C, int H, int W, int R, int 
 hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda, const float *b,
                            int64_t ldb, float *c, int64_t ldc, int conv_hw, bool b_padded,
                            const Decision &dec, hipStream_t s) {
-    GemmArgs g{M, Ncols, Kd, a, lda, b, ldb, c, ldc, conv_hw, dec};
+    GemmArgs g{};
+    g.M = M; g.N = Ncols; g.Kd = Kd; g.a = a; g.lda = lda; g.b = b; g.ldb = ldb; g.c = c; g.ldc = ldc;
+    g.conv_hw = conv_hw; g.dec = dec;
     const bool a_vec = (lda % 4 == 0) && (reinterpret_cast<uintptr_t>(a) % 16 == 0);
     const bool b_vec = b_padded && (ldb % 4 == 0) && (reinterpret_cast<uintptr_t>(b) % 16 == 0);
-    // tile height follows M: 32 (skinny), 64, or 128 rows per workgroup
-    if (M <= 32) return launch_gemm_t<1, 1, 2>(g, a_vec, b_vec, s);   // 32 x 256
-    if (M <= 64) return launch_gemm_t<2, 1, 2>(g, a_vec, b_vec, s);   // 64 x 128
-    return launch_gemm_t<2, 2, 2>(g, a_vec, b_vec, s);                // 128 x 128
+    return launch_gemm_any(g, a_vec, b_vec, false, s);
+}
+
+bool conv_gemm_implicit_ok(int C, int R, int S) { return static_cast<int64_t>(C) * R * S < (1 << 16); }
+
+hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
+                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s) {
+    GemmArgs g{};
+    g.M = K;
+    g.N = N * Ho * Wo;
+    g.Kd = C * R * S;
+    g.a = w;
+    g.lda = g.Kd;
+    g.c = y;
+    g.conv_hw = Ho * Wo;
+    g.dec = dec;
+    g.x = x;
+    g.C = C; g.H = H; g.W = W; g.T = T; g.P = P; g.Wo = Wo; g.RS = R * S; g.S = S;
+    g.mRS = div_magic(R * S);
+    g.mS = div_magic(S);
+    const bool a_vec = (g.lda % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
+    return launch_gemm_any(g, a_vec, false, true, s);
 }
 
 }  // namespace isc

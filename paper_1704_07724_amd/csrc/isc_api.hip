@@ -52,7 +52,11 @@ int check_desc(const isc_conv_desc *d, Shape *sh) {
     if (s.Ho < 1 || s.Wo < 1) return ISC_ERR_SHAPE;
     if (s.H > 65535 || s.W > 65535) return ISC_ERR_LIMIT;
     if (s.in_elems() > kI32Max || s.out_elems() > kI32Max || s.filt_elems() > kI32Max ||
-        s.ncols() > kI32Max || s.crs() * s.ldcol() > kI32Max || s.Ho > kI32Max || s.Wo > kI32Max)
+        s.ncols() > kI32Max || s.Ho > kI32Max || s.Wo > kI32Max)
+        return ISC_ERR_LIMIT;
+    // the dense path materialises the im2col matrix only when C*R*S >= 2^16
+    if (!isc::conv_gemm_implicit_ok(static_cast<int>(s.C), static_cast<int>(s.R), static_cast<int>(s.S)) &&
+        s.crs() * s.ldcol() > kI32Max)
         return ISC_ERR_LIMIT;
     if ((s.K + 31) / 32 > 65535) return ISC_ERR_LIMIT;  // GEMM grid rows
     *sh = s;
@@ -61,9 +65,18 @@ int check_desc(const isc_conv_desc *d, Shape *sh) {
 
 bool valid_path(int32_t p) { return p == ISC_PATH_AUTO || p == ISC_PATH_SPARSE || p == ISC_PATH_DENSE; }
 
+isc::SparseShape sparse_shape(const Shape &s) {
+    return isc::SparseShape{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
+                            static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
+                            static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
+                            static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
+}
+
 struct Layout {
-    size_t ctrl = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, total = 0;
+    size_t ctrl = 0, parts = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, total = 0;
     bool sparse = false, dense = false;
+    bool implicit = false;  // dense path gathers im2col inside the GEMM (no col buffer)
+    bool fused = false;     // sparse path compacts on the fly (no lists, no repacked filter)
 };
 
 Layout layout_for(const Shape &s, int32_t path) {
@@ -71,7 +84,12 @@ Layout layout_for(const Shape &s, int32_t path) {
     L.sparse = path != ISC_PATH_DENSE;
     L.dense = path != ISC_PATH_SPARSE;
     size_t off = align_up(sizeof(Ctrl), kAlign);
+    L.fused = isc::sparse_fused_applies(sparse_shape(s));
     if (L.sparse) {
+        L.parts = off;
+        off = align_up(off + sizeof(uint32_t) * isc::kMaxParts, kAlign);
+    }
+    if (L.sparse && !L.fused) {
         L.row_ptr = off;
         off = align_up(off + sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1)), kAlign);
         L.nz = off;
@@ -81,7 +99,8 @@ Layout layout_for(const Shape &s, int32_t path) {
                                                                          static_cast<int>(s.R), static_cast<int>(s.S)),
                        kAlign);
     }
-    if (L.dense) {
+    L.implicit = isc::conv_gemm_implicit_ok(static_cast<int>(s.C), static_cast<int>(s.R), static_cast<int>(s.S));
+    if (L.dense && !L.implicit) {
         L.col = off;
         off = align_up(off + sizeof(float) * static_cast<size_t>(s.crs() * s.ldcol()), kAlign);
     }
@@ -192,11 +211,8 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
         overlap(y, ybytes, ws, L.total))
         return ISC_ERR_ALIAS;
 
-    isc::SparseShape sh{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
-                        static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
-                        static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
-                        static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
-    const bool sparse_fits = isc::sparse_conv_feasible(sh);
+    const isc::SparseShape sh = sparse_shape(s);
+    const bool sparse_fits = L.fused || isc::sparse_conv_feasible(sh);
     if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
     if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
 
@@ -207,38 +223,84 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
     char *base = static_cast<char *>(ws);
     Ctrl *ctrl = reinterpret_cast<Ctrl *>(base);
     hipError_t e = hipSuccess;
+    uint32_t *parts = L.sparse ? reinterpret_cast<uint32_t *>(base + L.parts) : nullptr;
+    int nparts = 0;
+    const unsigned long long limit = nnz_limit_for(s.in_elems(), threshold);
 
     if (path != ISC_PATH_DENSE) {
-        int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
-        NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
-        float *wt = reinterpret_cast<float *>(base + L.wt);
-        // prologue: repack the filter to K-contiguous
-        if ((e = isc::launch_repack_filter(w, sh.K, sh.C, sh.R, sh.S, wt, hs)) != hipSuccess)
-            return hip_status(e);
-        // step 1
-        if ((e = isc::launch_compact(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz,
-                                     &ctrl->nnz_total, hs)) != hipSuccess)
-            return hip_status(e);
-        // steps 2-3, gated by the device-side decision in AUTO
-        isc::Decision dec{ctrl, nnz_limit_for(s.in_elems(), threshold),
-                          path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways, ctrl};
-        if ((e = isc::launch_sparse_conv(sh, row_ptr, nz, wt, y, dec, hs)) != hipSuccess)
-            return hip_status(e);
+        // steps 2-3 are gated by the device-side decision in AUTO and record
+        // the count and the path taken
+        if (L.fused) {
+            // the count for the decision, then steps 1-3 in one launch
+            if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs)) != hipSuccess)
+                return hip_status(e);
+            isc::Decision dec{parts, nparts, limit, path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways,
+                              ctrl};
+            if ((e = isc::launch_sparse_fused(sh, x, w, y, dec, hs)) != hipSuccess) return hip_status(e);
+        } else {
+            int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
+            NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
+            float *wt = reinterpret_cast<float *>(base + L.wt);
+            // step 1 and the filter repack to K-contiguous, one launch
+            if ((e = isc::launch_prep(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz, parts, &nparts, w,
+                                      sh.K, sh.C, sh.R, sh.S, wt, hs)) != hipSuccess)
+                return hip_status(e);
+            isc::Decision dec{parts, nparts, limit, path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways,
+                              ctrl};
+            if ((e = isc::launch_sparse_conv(sh, row_ptr, nz, wt, y, dec, hs)) != hipSuccess)
+                return hip_status(e);
+        }
     }
     if (path != ISC_PATH_SPARSE) {
-        float *col = reinterpret_cast<float *>(base + L.col);
-        isc::Decision dec{ctrl, nnz_limit_for(s.in_elems(), threshold),
-                          path == ISC_PATH_AUTO ? isc::kGateIfDense : isc::kGateAlways,
-                          path == ISC_PATH_DENSE ? ctrl : nullptr};
-        if ((e = isc::launch_im2col(x, sh.N, sh.C, sh.H, sh.W, sh.R, sh.S, sh.T, sh.P, sh.Ho, sh.Wo, col,
-                                    s.ldcol(), dec, hs)) != hipSuccess)
-            return hip_status(e);
-        dec.record = nullptr;
-        if ((e = isc::launch_gemm_f32(sh.K, static_cast<int>(s.ncols()), static_cast<int>(s.crs()), w,
-                                      s.crs(), col, s.ldcol(), y, 0, sh.Ho * sh.Wo, true, dec, hs)) !=
-            hipSuccess)
-            return hip_status(e);
+        // AUTO: run iff the sparse kernel, launched before on this stream,
+        // recorded the dense path; DENSE alone: no count, recorded as such
+        isc::Decision dec{nullptr, 0, limit, path == ISC_PATH_AUTO ? isc::kGateIfDense : isc::kGateAlways,
+                          path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
+        if (L.implicit) {
+            // one launch: the GEMM gathers the im2col matrix from x
+            if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
+                                           sh.Wo, dec, hs)) != hipSuccess)
+                return hip_status(e);
+        } else {
+            float *col = reinterpret_cast<float *>(base + L.col);
+            if ((e = isc::launch_im2col(x, sh.N, sh.C, sh.H, sh.W, sh.R, sh.S, sh.T, sh.P, sh.Ho, sh.Wo, col,
+                                        s.ldcol(), dec, hs)) != hipSuccess)
+                return hip_status(e);
+            dec.record = nullptr;
+            if ((e = isc::launch_gemm_f32(sh.K, static_cast<int>(s.ncols()), static_cast<int>(s.crs()), w,
+                                          s.crs(), col, s.ldcol(), y, 0, sh.Ho * sh.Wo, true, dec, hs)) !=
+                hipSuccess)
+                return hip_status(e);
+        }
     }
+    return ISC_OK;
+}
+
+int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w, float *y, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !w || !y) return ISC_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
+    const isc::SparseShape sh = sparse_shape(s);
+    if (!isc::sparse_fused_applies(sh)) return ISC_ERR_LIMIT;
+    const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
+    if (overlap(y, ybytes, x, sizeof(float) * static_cast<size_t>(s.in_elems())) ||
+        overlap(y, ybytes, w, sizeof(float) * static_cast<size_t>(s.filt_elems())))
+        return ISC_ERR_ALIAS;
+    st = check_device();
+    if (st) return st;
+    isc::Decision dec{nullptr, 0, 0, isc::kGateAlways, nullptr};
+    return hip_status(isc::launch_sparse_fused(sh, x, w, y, dec, static_cast<hipStream_t>(stream)));
+}
+
+int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {
+    if (!kernel) return ISC_ERR_NULL;
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    const isc::SparseShape sh = sparse_shape(s);
+    *kernel = isc::sparse_fused_applies(sh) ? ISC_KERNEL_FUSED : isc::list_kernel_for(sh);
     return ISC_OK;
 }
 
@@ -335,7 +397,7 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
     if (!isc::sparse_conv_feasible(sh)) return ISC_ERR_LIMIT;
     st = check_device();
     if (st) return st;
-    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    isc::Decision dec{nullptr, 0, 0, isc::kGateAlways, nullptr};
     return hip_status(isc::launch_sparse_conv(sh, row_ptr, reinterpret_cast<const NzEntry *>(nz), wt, y, dec,
                                               static_cast<hipStream_t>(stream)));
 }
@@ -352,7 +414,7 @@ int isc_im2col(const isc_conv_desc *d, const float *x, float *col, int64_t ldc, 
         return ISC_ERR_ALIAS;
     st = check_device();
     if (st) return st;
-    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    isc::Decision dec{nullptr, 0, 0, isc::kGateAlways, nullptr};
     return hip_status(isc::launch_im2col(x, static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
                                          static_cast<int>(s.W), static_cast<int>(s.R), static_cast<int>(s.S),
                                          static_cast<int>(s.T), static_cast<int>(s.P), static_cast<int>(s.Ho),
@@ -375,7 +437,7 @@ int isc_gemm_f32(int32_t M, int32_t Ncols, int32_t Kd, const float *a, int64_t l
         return ISC_ERR_ALIAS;
     int st = check_device();
     if (st) return st;
-    isc::Decision dec{nullptr, 0, isc::kGateAlways, nullptr};
+    isc::Decision dec{nullptr, 0, 0, isc::kGateAlways, nullptr};
     return hip_status(isc::launch_gemm_f32(M, Ncols, Kd, a, lda, b, ldb, c, ldc, 0, false, dec,
                                            static_cast<hipStream_t>(stream)));
 }

@@ -25,18 +25,49 @@ struct alignas(16) Ctrl {
 // device-side decision picks its path.
 enum Gate : int { kGateAlways = 0, kGateIfSparse = 1, kGateIfDense = 2 };
 
-// Device-side decision: sparse iff nnz <= nnz_limit.
+// Per-workgroup nonzero counts written by the compaction, at most this many
+// (a multiple of 4; unused entries are zero).
+constexpr int kMaxParts = 1024;
+
+// Device-side decision: sparse iff the input's nonzero count, the sum of the
+// compaction's per-workgroup counts, is <= nnz_limit.  A kernel launched
+// after the one that recorded the decision reads the recorded path instead.
 struct Decision {
-    const Ctrl *ctrl;             // nnz_total source (unused when gate == Always)
-    unsigned long long nnz_limit; // largest nonzero count that still picks sparse
+    const uint32_t *parts;         // per-workgroup counts (nullptr: no compaction ran)
+    int nparts;                    // entries of parts, a multiple of 4
+    unsigned long long nnz_limit;  // largest nonzero count that still picks sparse
     int gate;
-    Ctrl *record;                 // where block 0 records the path taken (may be nullptr)
+    Ctrl *record;                  // where block 0 records count and path (may be nullptr)
+    const Ctrl *recorded = nullptr;  // decision recorded by an earlier kernel on the stream
 };
 
-__device__ __forceinline__ bool decision_says_run(const Decision &d) {
-    if (d.gate == kGateAlways) return true;
-    const bool sparse = d.ctrl->nnz_total <= d.nnz_limit;
-    return d.gate == kGateIfSparse ? sparse : !sparse;
+// Sum of the per-workgroup counts, by the calling wavefront (every lane gets
+// the total).
+__device__ __forceinline__ unsigned long long decision_total(const Decision &d) {
+    unsigned long long s = 0;
+    const uint4 *p = reinterpret_cast<const uint4 *>(d.parts);
+    for (int i = threadIdx.x & 63; i < d.nparts / 4; i += 64) {
+        const uint4 v = p[i];
+        s += static_cast<unsigned long long>(v.x) + v.y + v.z + v.w;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    return s;
+}
+
+// Gate of a kernel on path `mine` (1 sparse, 2 dense): whether it runs.
+// Block 0 records the count (all ones when no compaction ran) and the path
+// taken when asked.  Called by whole wavefronts.
+__device__ __forceinline__ bool decision_gate(const Decision &d, uint32_t mine) {
+    if (d.recorded) return d.recorded->path_taken == mine;
+    const unsigned long long total = d.parts ? decision_total(d) : ~0ull;
+    const bool sparse = d.parts != nullptr && total <= d.nnz_limit;
+    const bool run = d.gate == kGateAlways || (d.gate == kGateIfSparse ? sparse : !sparse);
+    if (d.record && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+        d.record->nnz_total = total;
+        d.record->path_taken = run ? mine : 3u - mine;
+    }
+    return run;
 }
 
 // --- launchers (each returns hipGetLastError() of its launches) ------------
@@ -45,15 +76,37 @@ __device__ __forceinline__ bool decision_says_run(const Decision &d) {
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s);
 
-// Filter repack KCRS -> ISC step 2's K-contiguous kernel matrix, blocked by
-// 64 output maps: wt[((c*ceil(K/64) + kb)*64 + l)*RSP + t], RSP = R*S
-// rounded up to 4, zero padded.
+// Nonzero count of x[0 .. total) as per-workgroup parts (the decision's input
+// when the sparse path compacts on the fly).
+hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s);
+
+// The sparse path's first kernel: ISC step 1 with per-workgroup counts in
+// parts (kMaxParts entries; *nparts gets the number in use), and the filter
+// repack into wt in the same launch.
+hipError_t launch_prep(const float *x, int planes, int H, int W, int32_t *row_ptr, NzEntry *nz,
+                       uint32_t *parts, int *nparts, const float *w, int K, int C, int R, int S,
+                       float *wt, hipStream_t s);
+
+// Filter repack KCRS -> ISC step 2's K-contiguous layout:
+// wt[((c*R + r)*S + s)*Kp + k], Kp = K rounded up to 64, zero padded.
 size_t repacked_filter_floats(int K, int C, int R, int S);
 hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, float *wt, hipStream_t s);
 
 struct SparseShape {
     int N, C, H, W, K, R, S, T, P, Ho, Wo;
 };
+
+// ISC steps 1-3 in one launch, compacting on the fly from x and reading the
+// filter in its KCRS layout (stride 1, square 1x1/3x3/5x5 filters, K <= 64,
+// filter within LDS, Wo <= 28).
+bool sparse_fused_applies(const SparseShape &sh);
+hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *w, float *y, const Decision &dec,
+                               hipStream_t s);
+
+// Which kernel runs over compacted lists for a shape (the values are those
+// of isc_sparse_kernel in the C ABI).
+enum ListKernel : int { kListNone = 0, kListResident = 2, kListRing = 3, kListGeneric = 4 };
+int list_kernel_for(const SparseShape &sh);
 
 // ISC steps 2 and 3: zero-skipping convolution over the compacted lists.
 hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr,
@@ -73,5 +126,12 @@ hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda
                            const float *b, int64_t ldb, float *c, int64_t ldc,
                            int conv_hw, bool b_padded, const Decision &dec,
                            hipStream_t s);
+
+// The dense baseline as one implicit GEMM: the fp32 MFMA GEMM of Fig. 3 with
+// the im2col matrix gathered from x while loading (C*R*S < 2^16), output
+// scattered to NCHW.
+bool conv_gemm_implicit_ok(int C, int R, int S);
+hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
+                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s);
 
 }  // namespace isc

@@ -25,6 +25,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cstdlib>
+#include <cstring>
 
 namespace isc {
 namespace {
@@ -185,11 +186,7 @@ __device__ __forceinline__ void write_tile(const SparseArgs &a, const Tile &t, c
     }
 }
 
-__device__ __forceinline__ bool gate_and_record(const SparseArgs &a) {
-    const bool run = decision_says_run(a.dec);
-    if (blockIdx.x == 0 && threadIdx.x == 0 && a.dec.record) a.dec.record->path_taken = run ? 1u : 2u;
-    return run;
-}
+__device__ __forceinline__ bool gate_and_record(const SparseArgs &a) { return decision_gate(a.dec, 1u); }
 
 // ---------------------------------------------------------------------------
 // Generic kernel: any R x S (runtime), one channel at a time, weights read
@@ -308,24 +305,39 @@ hipError_t launch_with(Kern kern, std::atomic<int> &granted, const SparseArgs &a
 
 }  // namespace
 
-bool sparse_reg_applies(const SparseShape &sh);
-hipError_t launch_sparse_reg(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz, const float *wt,
+bool sparse_ring_applies(const SparseShape &sh);
+hipError_t launch_sparse_ring(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz, const float *wt,
+                              float *y, const Decision &dec, hipStream_t s);
+bool sparse_res_applies(const SparseShape &sh);
+hipError_t launch_sparse_res(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz, const float *wt,
                              float *y, const Decision &dec, hipStream_t s);
 
 bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *ctiles, int *WA, int *hx) {
     return tiling_for(sh, 0, TH, bands, TW, ctiles, WA, hx);
 }
 
-bool sparse_conv_feasible(const SparseShape &sh) {
+bool sparse_conv_feasible(const SparseShape &sh) { return list_kernel_for(sh) != kListNone; }
+
+// Kernel over compacted lists: the filter-resident register kernel when the
+// filter of 64 output maps fits in LDS, else the filter-ring register kernel,
+// else the LDS-accumulator kernel (any filter, any stride).
+// ISC_SPARSE_KERNEL = "generic" | "ring" | "res" restricts the choice (for
+// measurements).
+int list_kernel_for(const SparseShape &sh) {
+    const char *env = std::getenv("ISC_SPARSE_KERNEL");
+    const bool any = env == nullptr || env[0] == 0;
+    if ((any || std::strcmp(env, "res") == 0) && sparse_res_applies(sh)) return kListResident;
+    if ((any || std::strcmp(env, "ring") == 0) && sparse_ring_applies(sh)) return kListRing;
     int th, bands, tw, ct, wa, hx;
-    return sparse_reg_applies(sh) || tiling_for(sh, 0, &th, &bands, &tw, &ct, &wa, &hx);
+    return tiling_for(sh, 0, &th, &bands, &tw, &ct, &wa, &hx) ? kListGeneric : kListNone;
 }
 
 hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr, const NzEntry *nz,
                               const float *wt, float *y, const Decision &dec, hipStream_t s) {
-    const char *force = std::getenv("ISC_SPARSE_KERNEL");  // "lds" forces the general kernel
-    const bool use_reg = sparse_reg_applies(sh) && !(force && force[0] == 'l');
-    if (use_reg) return launch_sparse_reg(sh, row_ptr, nz, wt, y, dec, s);
+    const int which = list_kernel_for(sh);
+    if (which == kListResident) return launch_sparse_res(sh, row_ptr, nz, wt, y, dec, s);
+    if (which == kListRing) return launch_sparse_ring(sh, row_ptr, nz, wt, y, dec, s);
+    if (which == kListNone) return hipErrorInvalidValue;
     SparseArgs a{};
     a.row_ptr = row_ptr;
     a.nz = nz;
@@ -338,46 +350,6 @@ hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr, con
     a.kblocks = (sh.K + kLanes - 1) / kLanes;
     static std::atomic<int> granted{0};
     return launch_with(sparse_conv_generic_kernel, granted, a, 0, s);
-}
-
-// --- filter repack ----------------------------------------------------------
-//
-// ISC step 2's kernel matrix in the paper's K-contiguous ("column-major")
-// order: for one input channel and tap the weights of consecutive output maps
-// are adjacent, padded to Kp = K rounded up to 64 so that every block of 64
-// output maps is a 256-byte run:
-//   wt[((c * R + r) * S + s) * Kp + k] = w[k][c][r][s]   (0 for k >= K)
-
-namespace {
-__global__ __launch_bounds__(256)
-void repack_filter_kernel(const float *__restrict__ w, int K, int Kp, int CRS, float *__restrict__ wt) {
-    // 64 x 64 tile through LDS: reads along q = (c, r, s), writes along k
-    __shared__ float tile[64][65];
-    const int q0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < 64; i += 4) {
-        const int k = k0 + i, q = q0 + tx;
-        tile[i][tx] = (k < K && q < CRS) ? w[static_cast<size_t>(k) * CRS + q] : 0.0f;
-    }
-    __syncthreads();
-    for (int i = ty; i < 64; i += 4) {
-        const int q = q0 + i, k = k0 + tx;
-        if (q < CRS && k < Kp) wt[static_cast<size_t>(q) * Kp + k] = tile[tx][i];
-    }
-}
-}  // namespace
-
-size_t repacked_filter_floats(int K, int C, int R, int S) {
-    const size_t Kp = (static_cast<size_t>(K) + 63) / 64 * 64;
-    return static_cast<size_t>(C) * R * S * Kp;
-}
-
-hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, float *wt, hipStream_t s) {
-    const int CRS = C * R * S;
-    const int Kp = (K + 63) / 64 * 64;
-    dim3 grid((CRS + 63) / 64, Kp / 64);
-    repack_filter_kernel<<<grid, 256, 0, s>>>(w, K, Kp, CRS, wt);
-    return hipGetLastError();
 }
 
 }  // namespace isc

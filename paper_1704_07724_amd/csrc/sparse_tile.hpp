@@ -1,0 +1,186 @@
+// Register-tile machinery shared by the zero-skipping kernels (ISC steps 2
+// and 3, Sec. "Sparse Convolution"), stride 1, square R x S filters.
+//
+// A wavefront owns an output tile of TH rows x TW columns x 64*KPL output
+// maps: lane l accumulates maps kbase + l*KPL + j (j < KPL) in registers
+// acc[oy][ox][j].  Lanes run over output maps as the paper's SIMD lanes do
+// (step 2 multiplies one nonzero input by a K-contiguous weight vector), so
+// every nonzero input is a wave-uniform scalar.  With the current channel's
+// weights w[r][s][j] in registers, a nonzero at window row wy and shifted
+// column xp adds v * w[r][s][j] to acc[wy - r][xp - s][j] for every tap that
+// lands in the tile.  The position is data-dependent, so a compile-time
+// binary dispatch on (wy, xp) selects a straight-line block whose register
+// indices are constants: the inner loop has no memory operations, only the
+// block's fused multiply-adds and a few scalar compares.
+#pragma once
+
+#include "isc_internal.hpp"
+
+#include <type_traits>
+
+namespace isc {
+namespace tile {
+
+constexpr int kLanes = 64;
+
+template <int R_, int S_, int KPL_, int TH_, int TW_>
+struct Shape {
+    static constexpr int R = R_, S = S_, KPL = KPL_, TH = TH_, TW = TW_;
+    static constexpr int KW = kLanes * KPL;     // output maps per wavefront
+    static constexpr int WROWS = TH + R - 1;    // input rows the tile sees
+    static constexpr int WCOLS = TW + S - 1;    // shifted input columns it sees
+    // list entries of the tile's window, staged kLanes per register
+    static constexpr int EPL = (WROWS * WCOLS + kLanes - 1) / kLanes;
+};
+
+template <typename SH>
+using Acc = float[SH::TH][SH::TW][SH::KPL];
+template <typename SH>
+using Wts = float[SH::R][SH::S][SH::KPL];
+
+// Straight-line block for a nonzero at window row WY, shifted column XP.
+template <typename SH, int WY, int XP>
+__device__ __forceinline__ void leaf(Acc<SH> &acc, const Wts<SH> &w, float v) {
+#pragma unroll
+    for (int r = 0; r < SH::R; ++r) {
+        const int oy = WY - r;
+        if (oy < 0 || oy >= SH::TH) continue;
+#pragma unroll
+        for (int s = 0; s < SH::S; ++s) {
+            const int ox = XP - s;
+            if (ox < 0 || ox >= SH::TW) continue;
+#pragma unroll
+            for (int j = 0; j < SH::KPL; ++j) acc[oy][ox][j] = __builtin_fmaf(v, w[r][s][j], acc[oy][ox][j]);
+        }
+    }
+}
+
+// Binary dispatch of the leaf key q = wy * WCOLS + xp in [LO, HI).
+template <typename SH, int LO, int HI>
+__device__ __forceinline__ void dispatch(int q, Acc<SH> &acc, const Wts<SH> &w, float v) {
+    if constexpr (HI - LO == 1) {
+        leaf<SH, LO / SH::WCOLS, LO % SH::WCOLS>(acc, w, v);
+    } else {
+        constexpr int MID = (LO + HI) / 2;
+        if (q < MID)
+            dispatch<SH, LO, MID>(q, acc, w, v);
+        else
+            dispatch<SH, MID, HI>(q, acc, w, v);
+    }
+}
+
+// Walk the first len entries of a run staged in registers (entry
+// q*kLanes + l in lane l of run[q]); every entry lies in the tile's window
+// rows [ybase, ybase + WROWS).  The lanes first turn their entries into leaf
+// keys (wy * WCOLS + x + xshift, or -1 for a column outside [xlo, xlo +
+// xspan] when CHECK_X), so that per nonzero the scalar unit only walks the
+// dispatch tree.  Callers inline this once per kernel: the tree is most of
+// the kernel's code.
+template <typename SH, bool CHECK_X>
+__device__ __forceinline__ void walk(const NzEntry (&run)[SH::EPL], int len, int ybase, int xshift, int xlo,
+                                     int xspan, Acc<SH> &acc, const Wts<SH> &w) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+#pragma unroll
+    for (int q = 0; q < SH::EPL; ++q) {
+        const int cnt = min(len - q * kLanes, kLanes);
+        if (cnt <= 0) break;
+        const int yx = static_cast<int>(run[q].yx);
+        const int x = yx & 0xffff;
+        int key = ((yx >> 16) - ybase) * SH::WCOLS + x + xshift;
+        if (CHECK_X && static_cast<unsigned>(x - xlo) > static_cast<unsigned>(xspan)) key = -1;
+        const int vbits = __float_as_int(run[q].v);
+#pragma unroll 1
+        for (int jj = 0; jj < cnt; ++jj) {
+            const int k = __builtin_amdgcn_readlane(key, jj);
+            const float v = __int_as_float(__builtin_amdgcn_readlane(vbits, jj));
+            if (!CHECK_X || k >= 0) dispatch<SH, 0, NQ>(k, acc, w, v);
+        }
+    }
+}
+
+// Walk the nonzeros flagged in a 64-bit wavefront mask (bit l: lane l holds
+// a nonzero whose leaf key is keyv and whose value bits are vbits), in lane
+// order.  Per nonzero: find-first-set, clear, two lane reads, the tree.
+template <typename SH>
+__device__ __forceinline__ void walk_mask(unsigned long long mask, int keyv, int vbits, Acc<SH> &acc,
+                                          const Wts<SH> &w) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+#pragma unroll 1
+    while (mask) {
+        const int j = __builtin_ctzll(mask);
+        mask &= mask - 1;
+        const int k = __builtin_amdgcn_readlane(keyv, j);
+        const float v = __int_as_float(__builtin_amdgcn_readlane(vbits, j));
+        dispatch<SH, 0, NQ>(k, acc, w, v);
+    }
+}
+
+// Load one channel's weights for this lane: w[r][s][j] = wc[(r*S+s)*ld + lane*KPL + j]
+// (ld = KW for the ring's layout, padded for the transposed one).
+template <typename SH>
+__device__ __forceinline__ void load_weights(const float *wc, int lane, Wts<SH> &w, int ld = SH::KW) {
+#pragma unroll
+    for (int r = 0; r < SH::R; ++r)
+#pragma unroll
+        for (int s = 0; s < SH::S; ++s)
+#pragma unroll
+            for (int j = 0; j < SH::KPL; ++j) w[r][s][j] = wc[(r * SH::S + s) * ld + lane * SH::KPL + j];
+}
+
+// 16 bytes per lane from global memory straight into LDS at dst + 16 * lane
+// (dst wave-uniform).  A device function: the builtin has no host form, and
+// host-side instantiation of a lambda calling it would drop the kernel.
+__device__ __forceinline__ void load_lds16(const float *src, float4 *dst) {
+    __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
+}
+
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+// s_waitcnt vmcnt(VM) with lgkmcnt(0) when LGKM0, expcnt untouched.
+template <int VM, bool LGKM0>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt field");
+    constexpr int imm = (VM & 0xF) | ((VM >> 4) << 14) | ((LGKM0 ? 0x0 : 0xF) << 8) | (0x7 << 4);
+    __builtin_amdgcn_s_waitcnt(imm);
+}
+
+// s_waitcnt lgkmcnt(0): LDS reads issued so far have landed (placed after a
+// channel's weight loads so that the dispatch tree's leaves need no waits).
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt((0x3F & 0xF) | (0x3 << 14) | (0x7 << 4)); }
+
+// wait_vm<VM, lgkmcnt 0>, then a workgroup barrier that the compiler may not
+// move memory operations across.
+template <int VM>
+__device__ __forceinline__ void wait_vm_and_barrier() {
+    wait_vm<VM, true>();
+    asm volatile("s_barrier" ::: "memory");
+}
+
+// Store the tile rows/columns inside the output (rows < rows_ok, columns <
+// cols_ok) and maps < K to NCHW; yrow points at y[n][0][oy0][ox0].
+template <typename SH>
+__device__ __forceinline__ void store_tile(const Acc<SH> &acc, float *yrow, size_t plane_out, int Wo, int kbase,
+                                           int lane, int K, int rows_ok, int cols_ok) {
+#pragma unroll
+    for (int j = 0; j < SH::KPL; ++j) {
+        const int k = kbase + lane * SH::KPL + j;
+        if (k >= K) continue;
+        float *dst = yrow + static_cast<size_t>(k) * plane_out;
+#pragma unroll
+        for (int oy = 0; oy < SH::TH; ++oy) {
+            if (oy >= rows_ok) break;
+#pragma unroll
+            for (int ox = 0; ox < SH::TW; ++ox)
+                if (ox < cols_ok) dst[oy * Wo + ox] = acc[oy][ox][j];
+        }
+    }
+}
+
+}  // namespace tile
+}  // namespace isc

@@ -57,8 +57,17 @@ def test_workspace_sizes_ordered():
     au = isc.isc_workspace_size(d, "auto")
     assert sp > 0 and de > 0
     assert au >= max(sp, de)
-    # the dense path holds the unrolled matrix: C*R*S rows of >= N*Ho*Wo floats
-    assert de >= 20 * 25 * 8 * 8 * 8 * 4
+    # the dense path gathers the unrolled matrix inside its GEMM (C*R*S <
+    # 2^16): control block only; this shape compacts on the fly (K <= 64,
+    # filter within LDS): control block and per-workgroup counts only
+    assert de < 4096 and sp < 8192
+    # more output maps than one pass holds: the sparse path keeps the lists (8
+    # bytes per input element) and the repacked filter
+    d2 = isc.make_desc(2, 96, 27, 27, 256, 5, 5, 1, 2)
+    assert isc.isc_workspace_size(d2, "sparse") >= 2 * 96 * 27 * 27 * 8 + 96 * 25 * 256 * 4
+    # C*R*S >= 2^16: the dense path materialises C*R*S rows of >= N*Ho*Wo floats
+    big = isc.make_desc(1, 2700, 6, 6, 8, 5, 5, 1, 0)
+    assert isc.isc_workspace_size(big, "dense") >= 2700 * 25 * 2 * 2 * 4
 
 
 def _conv(desc, x=0x1000, w=0x200000, y=0x400000, ws=0x800000, ws_bytes=1 << 30, path=0,
@@ -119,3 +128,31 @@ def test_dispatch_threshold_reading():
     sig = inspect.signature(isc.isc_conv2d)
     assert sig.parameters["threshold"].default == 0.9
     assert sig.parameters["path"].default == "auto"
+
+
+def test_sparse_kernel_choice(monkeypatch):
+    """Host-side choice of the sparse kernel for the workload shapes."""
+    monkeypatch.delenv("ISC_SPARSE_KERNEL", raising=False)
+    d = isc.make_desc
+    assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused"    # LeNet conv2
+    assert isc.isc_sparse_kernel(d(128, 16, 28, 28, 32, 5, 5, 1, 2)) == "fused"    # inception 5x5
+    assert isc.isc_sparse_kernel(d(128, 96, 27, 27, 256, 5, 5, 1, 2)) == "ring"    # AlexNet conv2
+    assert isc.isc_sparse_kernel(d(128, 96, 28, 28, 128, 3, 3, 1, 1)) == "ring"    # inception 3x3
+    assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 64, 5, 5, 2, 1)) == "generic"     # stride 2
+    assert isc.isc_sparse_kernel(d(1, 3, 10, 9, 9, 2, 3, 1, 1)) == "generic"       # 2 x 3 filter
+    assert isc.isc_sparse_kernel(d(1, 3, 20, 200, 66, 3, 3, 1, 1)) == "generic"    # rows too wide to stage
+
+
+def test_fused_entry_validation():
+    L = isc.lib()
+    ok = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 1, 0)
+    big_k = isc.make_desc(1, 2, 12, 12, 65, 5, 5, 1, 0)       # K > 64: not taken
+    strided = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 2, 0)      # stride 2: not taken
+    x, w, y = 0x1000, 0x200000, 0x400000
+    assert L.isc_sparse_conv_fused(None, x, w, y, None) == 1
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), None, w, y, None) == 1
+    assert L.isc_sparse_conv_fused(ctypes.byref(big_k), x, w, y, None) == 3
+    assert L.isc_sparse_conv_fused(ctypes.byref(strided), x, w, y, None) == 3
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, x + 4, None) == 5   # y overlaps x
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x + 2, w, y, None) == 9   # misaligned
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, y, None) == 7       # no gfx950 here

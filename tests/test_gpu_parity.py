@@ -178,6 +178,18 @@ def test_conv_matches_oracle(torch, isc, case, path):
     assert_conv_close(y, want, "%s %s" % (path, case))
 
 
+@pytest.mark.parametrize("path", ["dense", "auto"])
+def test_conv_dense_with_im2col_matrix(torch, isc, path):
+    """C*R*S >= 2^16: the dense path writes the im2col matrix and runs the
+    explicit GEMM instead of gathering inside the GEMM."""
+    case = (1, 2700, 6, 6, 8, 5, 5, 1, 0, 0.5)
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("conv explicit im2col", path, case)
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=27)
+    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), T, P, path=path).cpu().numpy()
+    assert_conv_close(y, oracle.conv2d_f64(x, w, T, P), "%s %s" % (path, case))
+
+
 @pytest.mark.parametrize("path", ["sparse", "dense"])
 @pytest.mark.parametrize("case", [(2, 6, 12, 12, 50, 5, 5, 1, 0), (2, 16, 13, 13, 130, 3, 3, 1, 1),
                                   (1, 5, 11, 11, 20, 5, 5, 2, 1), (2, 3, 9, 9, 7, 2, 4, 1, 1)])
@@ -382,3 +394,28 @@ def test_full_size_sampled(torch, isc, layer):
         assert_conv_close(got, want, "%s %s" % (layer.name, path))
         del y
     torch.cuda.empty_cache()
+
+
+FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (1, 3, 5) and c[4] <= 64]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES)
+def test_sparse_conv_fused_entry(torch, isc, case):
+    """The workspace-free entry point (on-the-fly compaction) against the
+    oracle, and the AUTO path on the same shape runs it."""
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("fused entry", case)
+    desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
+    assert isc.isc_sparse_kernel(desc) == "fused"
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=11 + sum(case[:9]))
+    y = isc.isc_sparse_conv_fused(to_dev(torch, x), to_dev(torch, w), T, P).cpu().numpy()
+    assert_conv_close(y, oracle.conv2d_f64(x, w, T, P), "fused %s" % (case,))
+
+
+def test_sparse_conv_fused_rejects_ineligible(torch, isc):
+    note("fused ineligible")
+    x = torch.zeros((1, 2, 12, 12), device="cuda")
+    w = torch.zeros((65, 2, 5, 5), device="cuda")
+    with pytest.raises(isc.IscError) as e:
+        isc.isc_sparse_conv_fused(x, w, 1, 0)
+    assert e.value.status == 3
