@@ -229,15 +229,25 @@ size_t fused_lds(const SparseShape &sh, int th, int tw, int cs) {
     return sizeof(float) * std::max(filt, tiles);
 }
 
-// Tallest tile (up to 32 accumulators per lane), then the fewest channel
-// phases whose row groups still fit the output height, within LDS.
+constexpr int kMaxTile = 32;  // accumulators per lane
+constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
+
+constexpr int max_tile(int) { return kMaxTile; }
+
+// Tallest tile (up to max_tile accumulators per lane), then the fewest
+// channel phases whose row groups still fit the output height, within LDS;
+// a plan with fewer than kMinGroups workgroups is kept only if no other fits.
+// ISC_FUSED_TH caps the tile height (for measurements).
 bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     if (sh.Wo > 28 || sh.K > kLanes) return false;
     if (static_cast<int64_t>(sh.K) * sh.C * sh.R * sh.S >= (int64_t(1) << 30)) return false;
     const int tw = fused_tw(sh.Wo);
-    for (int th : {4, 2, 1}) {
-        if (th * tw > 32) continue;
+    int th_cap = 8;
+    if (const char *env = std::getenv("ISC_FUSED_TH")) th_cap = std::max(1, std::atoi(env));
+    bool found = false;
+    for (int th : {8, 4, 2, 1}) {
+        if (th * tw > max_tile(sh.R) || th > th_cap) continue;
         const int rows_need = (sh.Ho + th - 1) / th;
         for (int cs = 1; cs <= kWaves; cs *= 2) {
             const int rg = kWaves / cs;
@@ -245,16 +255,21 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
             if (cs > sh.C) break;
             const size_t lds = fused_lds(sh, th, tw, cs);
             if (lds > kLdsMax) continue;
-            *plan = FusedPlan{th, tw, cs, lds};
-            return true;
+            const int64_t groups = static_cast<int64_t>(sh.N) * ((sh.Ho + rg * th - 1) / (rg * th));
+            if (!found || groups >= kMinGroups) {
+                *plan = FusedPlan{th, tw, cs, lds};
+                found = true;
+            }
+            if (groups >= kMinGroups) return true;
+            break;
         }
     }
-    return false;
+    return found;
 }
 
 template <int RS_, int TH, int TW>
 hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
-    if constexpr (TH * TW > 32) {
+    if constexpr (TH * TW > max_tile(RS_)) {
         return hipErrorInvalidValue;
     } else {
         auto kern = sparse_conv_fused_kernel<RS_, TH, TW>;
@@ -271,6 +286,7 @@ hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
 template <int RS_, int TW>
 hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s) {
     switch (th) {
+    case 8: return launch_fused_t<RS_, 8, TW>(a, lds, s);
     case 4: return launch_fused_t<RS_, 4, TW>(a, lds, s);
     case 2: return launch_fused_t<RS_, 2, TW>(a, lds, s);
     default: return launch_fused_t<RS_, 1, TW>(a, lds, s);

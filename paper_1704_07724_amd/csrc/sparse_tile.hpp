@@ -15,6 +15,7 @@
 #pragma once
 
 #include "isc_internal.hpp"
+#include "dispatch_gen.hpp"
 
 #include <type_traits>
 
@@ -69,6 +70,19 @@ __device__ __forceinline__ void dispatch(int q, Acc<SH> &acc, const Wts<SH> &w, 
     }
 }
 
+// One nonzero: the computed-jump dispatch (generated inline assembly) for
+// single-row tiles, whose leaves are short and whose trees are deepest; the
+// binary tree otherwise (measured faster for taller tiles, whose leaves are
+// long).
+template <typename SH>
+__device__ __forceinline__ void dispatch_one(int key, int vbits, Acc<SH> &acc, const Wts<SH> &w) {
+    if constexpr (SH::KPL == 1 && SH::R == SH::S && SH::TH == 1 && AsmDispatch<SH::R, SH::TH, SH::TW>::kAvailable) {
+        AsmDispatch<SH::R, SH::TH, SH::TW>::run(key, vbits, acc, w);
+    } else {
+        dispatch<SH, 0, SH::WROWS * SH::WCOLS>(key, acc, w, __int_as_float(vbits));
+    }
+}
+
 // Walk the first len entries of a run staged in registers (entry
 // q*kLanes + l in lane l of run[q]); every entry lies in the tile's window
 // rows [ybase, ybase + WROWS).  The lanes first turn their entries into leaf
@@ -79,7 +93,6 @@ __device__ __forceinline__ void dispatch(int q, Acc<SH> &acc, const Wts<SH> &w, 
 template <typename SH, bool CHECK_X>
 __device__ __forceinline__ void walk(const NzEntry (&run)[SH::EPL], int len, int ybase, int xshift, int xlo,
                                      int xspan, Acc<SH> &acc, const Wts<SH> &w) {
-    constexpr int NQ = SH::WROWS * SH::WCOLS;
 #pragma unroll
     for (int q = 0; q < SH::EPL; ++q) {
         const int cnt = min(len - q * kLanes, kLanes);
@@ -92,8 +105,8 @@ __device__ __forceinline__ void walk(const NzEntry (&run)[SH::EPL], int len, int
 #pragma unroll 1
         for (int jj = 0; jj < cnt; ++jj) {
             const int k = __builtin_amdgcn_readlane(key, jj);
-            const float v = __int_as_float(__builtin_amdgcn_readlane(vbits, jj));
-            if (!CHECK_X || k >= 0) dispatch<SH, 0, NQ>(k, acc, w, v);
+            const int vb = __builtin_amdgcn_readlane(vbits, jj);
+            if (!CHECK_X || k >= 0) dispatch_one<SH>(k, vb, acc, w);
         }
     }
 }
@@ -104,14 +117,11 @@ __device__ __forceinline__ void walk(const NzEntry (&run)[SH::EPL], int len, int
 template <typename SH>
 __device__ __forceinline__ void walk_mask(unsigned long long mask, int keyv, int vbits, Acc<SH> &acc,
                                           const Wts<SH> &w) {
-    constexpr int NQ = SH::WROWS * SH::WCOLS;
 #pragma unroll 1
     while (mask) {
         const int j = __builtin_ctzll(mask);
         mask &= mask - 1;
-        const int k = __builtin_amdgcn_readlane(keyv, j);
-        const float v = __int_as_float(__builtin_amdgcn_readlane(vbits, j));
-        dispatch<SH, 0, NQ>(k, acc, w, v);
+        dispatch_one<SH>(__builtin_amdgcn_readlane(keyv, j), __builtin_amdgcn_readlane(vbits, j), acc, w);
     }
 }
 
