@@ -146,7 +146,7 @@ class LayerRun:
         compacted lists (isc_sparse_conv)."""
         L = self.layer
         if self.kernel == "fused":
-            return lambda: self.isc.isc_sparse_conv_fused(self.x, self.w, L.T, L.P, out=self.y)
+            return lambda: self.isc.isc_sparse_conv_fused(self.x, self.wt, L.T, L.P, out=self.y)
         return lambda: self.isc.isc_sparse_conv(self.x.shape, self.lists, self.wt, L.T, L.P,
                                                 out=self.y)
 
@@ -272,7 +272,7 @@ def algorithmic_bytes(run) -> dict:
     """Bytes each kernel of the path must move at least once, per launch:
     compaction reads the input and writes the lists, the sparse kernel reads
     lists, row offsets and repacked weights and writes the output (the fused
-    kernel reads the input and the filter instead), im2col
+    kernel reads the input and the repacked filter instead), im2col
     reads the input and writes the unrolled matrix."""
     L = run.layer
     planes = L.N * L.C
@@ -280,8 +280,8 @@ def algorithmic_bytes(run) -> dict:
     x_bytes = run.x_host.size * 4
     y_bytes = L.N * L.K * run.Ho * run.Wo * 4
     kp = (L.K + 63) // 64 * 64
-    if run.kernel == "fused":   # reads x and the KCRS filter once, writes y
-        sparse = x_bytes + L.K * L.C * L.R * L.S * 4 + y_bytes
+    if run.kernel == "fused":   # reads x and the repacked filter once, writes y
+        sparse = x_bytes + L.C * L.R * L.S * kp * 4 + y_bytes
     else:                       # lists, row offsets, repacked filter; writes y
         sparse = run.nnz * 8 + row_ptr + L.C * L.R * L.S * kp * 4 + y_bytes
     return {

@@ -177,15 +177,20 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
 
 /* ISC steps 1-3 (Sec. "Sparse Convolution") in one launch with no workspace:
  * each wavefront compacts the input rows it needs on the fly (a ballot of
- * the zero test, walked in row-major order) and the filter is read in its
- * KCRS layout.  The kernel isc_conv2d's sparse path runs when
- * isc_sparse_kernel reports ISC_KERNEL_FUSED; no sparse/dense decision.
- *   x, w: device inputs as for isc_conv2d.  y: device output, fully
- *     written, must not overlap x or w.
- * Errors: NULL, SHAPE, LIMIT (shape not eligible: stride 1, square 1x1/3x3/
- * 5x5 filter, K <= 64, Wo <= 28, filter within LDS), ALIAS, ALIGN, DEVICE,
- * HIP. */
-int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w, float *y,
+ * the zero test, walked in row-major order) and multiplies each nonzero by
+ * the K-contiguous weight vectors of step 2, which it holds in registers.
+ * The kernel isc_conv2d's sparse path runs when isc_sparse_kernel reports
+ * ISC_KERNEL_FUSED (isc_conv2d repacks the filter itself, in the launch that
+ * counts the nonzeros); no sparse/dense decision here.
+ *   x: device input as for isc_conv2d.
+ *   wt: the repacked filter of isc_repack_filter for K, C, R, S of d.
+ *   y: device output N x K x Ho x Wo, fully written, must not overlap x or
+ *     wt.
+ * Deterministic (fixed summation order per output).  Errors: NULL, SHAPE,
+ * LIMIT (shape not eligible: stride 1, square 1x1/3x3/5x5 filter, K <= 64,
+ * Wo <= 28, at most 24 (5x5), 64 (3x3) or 256 (1x1) input maps), ALIAS,
+ * ALIGN, DEVICE, HIP. */
+int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y,
                           void *stream);
 
 /* Which kernel isc_conv2d's sparse path runs for this descriptor, reported in

@@ -267,16 +267,15 @@ def isc_sparse_kernel(desc: ConvDesc) -> str:
     return KERNEL_NAMES[which.value]
 
 
-def isc_sparse_conv_fused(x, w, stride=1, pad=0, out=None, stream=None):
-    """ISC steps 1-3 in one launch (compaction on the fly, KCRS filter), no
-    workspace; returns y [N, K, Ho, Wo].  Raises IscError (LIMIT) for shapes
-    the kernel does not take."""
+def isc_sparse_conv_fused(x, wt, stride=1, pad=0, out=None, stream=None):
+    """ISC steps 1-3 in one launch (compaction on the fly) with a
+    RepackedFilter (isc_repack_filter), no workspace; returns y [N, K, Ho,
+    Wo].  Raises IscError (LIMIT) for shapes the kernel does not take."""
     torch = _torch()
     x = _dev_f32(x, "x")
-    w = _dev_f32(w, "w")
     N, C, H, W = (int(v) for v in x.shape)
-    K, C2, R, S = (int(v) for v in w.shape)
-    if C != C2:
+    K, R, S = wt.K, wt.R, wt.S
+    if C != wt.C:
         raise ValueError("channel mismatch")
     desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
     ho, wo = isc_out_shape(desc)
@@ -284,7 +283,7 @@ def isc_sparse_conv_fused(x, w, stride=1, pad=0, out=None, stream=None):
         out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=x.device)
     elif not out.is_contiguous() or tuple(out.shape) != (N, K, ho, wo):
         raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
-    _check(lib().isc_sparse_conv_fused(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+    _check(lib().isc_sparse_conv_fused(ctypes.byref(desc), x.data_ptr(), wt.data.data_ptr(), out.data_ptr(),
                                        _stream(stream)), "isc_sparse_conv_fused")
     return out
 

@@ -180,9 +180,16 @@ constexpr int kCountUnroll = 8;
 
 __global__ __launch_bounds__(kWaves * 64)
 void count_parts_kernel(const float *__restrict__ x, int64_t total, uint32_t *__restrict__ parts, int groups,
-                        int nparts) {
+                        int nparts, const float *__restrict__ w, int K, int Kp, int CRS, int qtiles,
+                        float *__restrict__ wt) {
     __shared__ uint32_t wave_count[kWaves];
+    __shared__ float tile[64][65];
     const int b = blockIdx.x;
+    if (b >= groups) {  // filter repack, one 64 x 64 tile per workgroup
+        const int t = b - groups;
+        repack_tile(w, K, Kp, CRS, wt, t % qtiles, t / qtiles, tile);
+        return;
+    }
     const int64_t chunk = (total + groups - 1) / groups;
     const int64_t beg = b * chunk;
     const int64_t end = min(total, beg + chunk);
@@ -239,11 +246,17 @@ hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, floa
     return hipGetLastError();
 }
 
-hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s) {
+hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s,
+                              const float *w, int K, int C, int R, int S, float *wt) {
     const int64_t per = static_cast<int64_t>(kWaves) * 64 * kCountUnroll * 2;  // elements per workgroup, at least
     const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxParts, (total + per - 1) / per)));
     const int np = (groups + 3) / 4 * 4;
-    count_parts_kernel<<<groups, kWaves * 64, 0, s>>>(x, total, parts, groups, np);
+    const int CRS = C * R * S;
+    const int Kp = (K + 63) / 64 * 64;
+    const int qtiles = (CRS + 63) / 64;
+    const int tiles = w ? qtiles * (Kp / 64) : 0;
+    count_parts_kernel<<<groups + tiles, kWaves * 64, 0, s>>>(x, total, parts, groups, np, w, K, Kp, CRS, qtiles,
+                                                              wt);
     *nparts = np;
     return hipGetLastError();
 }

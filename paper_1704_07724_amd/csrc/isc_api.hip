@@ -76,7 +76,7 @@ struct Layout {
     size_t ctrl = 0, parts = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, total = 0;
     bool sparse = false, dense = false;
     bool implicit = false;  // dense path gathers im2col inside the GEMM (no col buffer)
-    bool fused = false;     // sparse path compacts on the fly (no lists, no repacked filter)
+    bool fused = false;     // sparse path compacts on the fly (no lists; the repacked filter only)
 };
 
 Layout layout_for(const Shape &s, int32_t path) {
@@ -94,6 +94,8 @@ Layout layout_for(const Shape &s, int32_t path) {
         off = align_up(off + sizeof(int32_t) * static_cast<size_t>(s.N * s.C * (s.H + 1)), kAlign);
         L.nz = off;
         off = align_up(off + sizeof(NzEntry) * static_cast<size_t>(s.in_elems() + kNzTail), kAlign);
+    }
+    if (L.sparse) {
         L.wt = off;
         off = align_up(off + sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
                                                                          static_cast<int>(s.R), static_cast<int>(s.S)),
@@ -230,17 +232,19 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
     if (path != ISC_PATH_DENSE) {
         // steps 2-3 are gated by the device-side decision in AUTO and record
         // the count and the path taken
+        float *wt = reinterpret_cast<float *>(base + L.wt);
         if (L.fused) {
-            // the count for the decision, then steps 1-3 in one launch
-            if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs)) != hipSuccess)
+            // the count for the decision and the filter repack to
+            // K-contiguous in one launch, then steps 1-3 in one launch
+            if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs, w, sh.K, sh.C, sh.R, sh.S,
+                                             wt)) != hipSuccess)
                 return hip_status(e);
             isc::Decision dec{parts, nparts, limit, path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways,
                               ctrl};
-            if ((e = isc::launch_sparse_fused(sh, x, w, y, dec, hs)) != hipSuccess) return hip_status(e);
+            if ((e = isc::launch_sparse_fused(sh, x, wt, y, dec, hs)) != hipSuccess) return hip_status(e);
         } else {
             int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
             NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
-            float *wt = reinterpret_cast<float *>(base + L.wt);
             // step 1 and the filter repack to K-contiguous, one launch
             if ((e = isc::launch_prep(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz, parts, &nparts, w,
                                       sh.K, sh.C, sh.R, sh.S, wt, hs)) != hipSuccess)
@@ -276,22 +280,22 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
     return ISC_OK;
 }
 
-int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w, float *y, void *stream) {
+int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y, void *stream) {
     Shape s;
     int st = check_desc(d, &s);
     if (st) return st;
-    if (!x || !w || !y) return ISC_ERR_NULL;
-    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
+    if (!x || !wt || !y) return ISC_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(wt, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
     const isc::SparseShape sh = sparse_shape(s);
     if (!isc::sparse_fused_applies(sh)) return ISC_ERR_LIMIT;
     const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
-    if (overlap(y, ybytes, x, sizeof(float) * static_cast<size_t>(s.in_elems())) ||
-        overlap(y, ybytes, w, sizeof(float) * static_cast<size_t>(s.filt_elems())))
+    const size_t wtbytes = sizeof(float) * isc::repacked_filter_floats(sh.K, sh.C, sh.R, sh.S);
+    if (overlap(y, ybytes, x, sizeof(float) * static_cast<size_t>(s.in_elems())) || overlap(y, ybytes, wt, wtbytes))
         return ISC_ERR_ALIAS;
     st = check_device();
     if (st) return st;
     isc::Decision dec{nullptr, 0, 0, isc::kGateAlways, nullptr};
-    return hip_status(isc::launch_sparse_fused(sh, x, w, y, dec, static_cast<hipStream_t>(stream)));
+    return hip_status(isc::launch_sparse_fused(sh, x, wt, y, dec, static_cast<hipStream_t>(stream)));
 }
 
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {

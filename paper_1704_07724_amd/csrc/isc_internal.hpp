@@ -77,8 +77,12 @@ hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row
                           NzEntry *nz, unsigned long long *counter, hipStream_t s);
 
 // Nonzero count of x[0 .. total) as per-workgroup parts (the decision's input
-// when the sparse path compacts on the fly).
-hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s);
+// when the sparse path compacts on the fly); with w, extra workgroups of the
+// same launch repack the K x C x R x S filter into wt (layout of
+// launch_repack_filter).
+hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s,
+                              const float *w = nullptr, int K = 0, int C = 0, int R = 0, int S = 0,
+                              float *wt = nullptr);
 
 // The sparse path's first kernel: ISC step 1 with per-workgroup counts in
 // parts (kMaxParts entries; *nparts gets the number in use), and the filter
@@ -96,11 +100,11 @@ struct SparseShape {
     int N, C, H, W, K, R, S, T, P, Ho, Wo;
 };
 
-// ISC steps 1-3 in one launch, compacting on the fly from x and reading the
-// filter in its KCRS layout (stride 1, square 1x1/3x3/5x5 filters, K <= 64,
-// filter within LDS, Wo <= 28).
+// ISC steps 1-3 in one launch, compacting on the fly from x, with the filter
+// repacked K-contiguous (launch_repack_filter's layout; stride 1, square
+// 1x1/3x3/5x5 filters, K <= 64, Wo <= 28, few enough input maps).
 bool sparse_fused_applies(const SparseShape &sh);
-hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *w, float *y, const Decision &dec,
+hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s);
 
 // Which kernel runs over compacted lists for a shape (the values are those

@@ -34,6 +34,14 @@ struct Shape {
     static constexpr int EPL = (WROWS * WCOLS + kLanes - 1) / kLanes;
 };
 
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
 template <typename SH>
 using Acc = float[SH::TH][SH::TW][SH::KPL];
 template <typename SH>
@@ -71,12 +79,17 @@ __device__ __forceinline__ void dispatch(int q, Acc<SH> &acc, const Wts<SH> &w, 
 }
 
 // One nonzero: the computed-jump dispatch (generated inline assembly) for
-// single-row tiles, whose leaves are short and whose trees are deepest; the
-// binary tree otherwise (measured faster for taller tiles, whose leaves are
-// long).
+// one-map-per-lane tiles; the binary tree otherwise.  ISC_TREE_DISPATCH
+// selects the tree everywhere (for measurements).
+#ifdef ISC_TREE_DISPATCH
+constexpr bool kJumpDispatch = false;
+#else
+constexpr bool kJumpDispatch = true;
+#endif
+
 template <typename SH>
 __device__ __forceinline__ void dispatch_one(int key, int vbits, Acc<SH> &acc, const Wts<SH> &w) {
-    if constexpr (SH::KPL == 1 && SH::R == SH::S && SH::TH == 1 && AsmDispatch<SH::R, SH::TH, SH::TW>::kAvailable) {
+    if constexpr (kJumpDispatch && SH::KPL == 1 && SH::R == SH::S && AsmDispatch<SH::R, SH::TH, SH::TW>::kAvailable) {
         AsmDispatch<SH::R, SH::TH, SH::TW>::run(key, vbits, acc, w);
     } else {
         dispatch<SH, 0, SH::WROWS * SH::WCOLS>(key, acc, w, __int_as_float(vbits));
@@ -125,6 +138,53 @@ __device__ __forceinline__ void walk_mask(unsigned long long mask, int keyv, int
     }
 }
 
+// Static scan of a window laid out in leaf-key order (element q of the
+// window, q = wy * WCOLS + xp, is lane q % 64 of xv[q / 64]): the positions
+// are visited in order, in groups of 16, then 4, then one, each group tested
+// against the mask and skipped when empty; a set position runs its
+// straight-line block.  The tests are wave-uniform scalar branches laid out
+// so that an empty group falls through (no fetch redirect), and there is no
+// dependent chain from one nonzero to the next.
+template <typename SH, int Q>
+__device__ __forceinline__ void scan_one(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                         Acc<SH> &acc, const Wts<SH> &w) {
+    constexpr int E = Q / kLanes, L = Q % kLanes;
+    if (__builtin_expect((mask[E] & (1ull << L)) != 0ull, 0)) {
+        const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xv[E]), L));
+        leaf<SH, Q / SH::WCOLS, Q % SH::WCOLS>(acc, w, v);
+    }
+}
+
+// Positions [Q0, Q0 + G) (G a power of two dividing 64, clipped to the
+// window), then the next level down.
+template <typename SH, int Q0, int G>
+__device__ __forceinline__ void scan_group(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                           Acc<SH> &acc, const Wts<SH> &w) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+    if constexpr (Q0 < NQ) {
+        if constexpr (G == 1) {
+            scan_one<SH, Q0>(mask, xv, acc, w);
+        } else {
+            constexpr int E = Q0 / kLanes, L = Q0 % kLanes;
+            constexpr int N = (NQ - Q0) < G ? (NQ - Q0) : G;
+            constexpr unsigned long long gm = (N == 64 ? ~0ull : ((1ull << N) - 1)) << L;
+            if (__builtin_expect((mask[E] & gm) != 0ull, 0)) {
+                constexpr int G2 = G == 16 ? 4 : 1;
+                static_for<0, G / G2>([&](auto ic) {
+                    scan_group<SH, Q0 + decltype(ic)::value * G2, G2>(mask, xv, acc, w);
+                });
+            }
+        }
+    }
+}
+
+template <typename SH>
+__device__ __forceinline__ void walk_scan(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                          Acc<SH> &acc, const Wts<SH> &w) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group<SH, decltype(gc)::value * 16, 16>(mask, xv, acc, w); });
+}
+
 // Load one channel's weights for this lane: w[r][s][j] = wc[(r*S+s)*ld + lane*KPL + j]
 // (ld = KW for the ring's layout, padded for the transposed one).
 template <typename SH>
@@ -144,12 +204,9 @@ __device__ __forceinline__ void load_lds16(const float *src, float4 *dst) {
     __builtin_amdgcn_global_load_lds(src, dst, 16, 0, 0);
 }
 
-template <int B, int E, typename F>
-__device__ __forceinline__ void static_for(F &&f) {
-    if constexpr (B < E) {
-        f(std::integral_constant<int, B>{});
-        static_for<B + 1, E>(f);
-    }
+// 4 bytes per lane from global memory straight into LDS at dst + 4 * lane.
+__device__ __forceinline__ void load_lds4(const float *src, float *dst) {
+    __builtin_amdgcn_global_load_lds(src, dst, 4, 0, 0);
 }
 
 // s_waitcnt vmcnt(VM) with lgkmcnt(0) when LGKM0, expcnt untouched.

@@ -58,9 +58,11 @@ def test_workspace_sizes_ordered():
     assert sp > 0 and de > 0
     assert au >= max(sp, de)
     # the dense path gathers the unrolled matrix inside its GEMM (C*R*S <
-    # 2^16): control block only; this shape compacts on the fly (K <= 64,
-    # filter within LDS): control block and per-workgroup counts only
-    assert de < 4096 and sp < 8192
+    # 2^16): control block only; this shape compacts on the fly (K <= 64, few
+    # input maps): control block, per-workgroup counts and the repacked
+    # filter (C*R*S x 64 floats) only
+    assert de < 4096
+    assert 20 * 25 * 64 * 4 <= sp < 20 * 25 * 64 * 4 + 8192
     # more output maps than one pass holds: the sparse path keeps the lists (8
     # bytes per input element) and the repacked filter
     d2 = isc.make_desc(2, 96, 27, 27, 256, 5, 5, 1, 2)

@@ -396,7 +396,16 @@ def test_full_size_sampled(torch, isc, layer):
     torch.cuda.empty_cache()
 
 
-FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (1, 3, 5) and c[4] <= 64]
+FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (1, 3, 5) and c[4] <= 64] + [
+    # N, C, H, W, K, R, S, T, P, sparsity: the fused kernel's plans
+    (3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9),     # LeNet conv2: 8 phases (3 or 2 maps each), one 8 x 8 tile
+    (2, 24, 11, 11, 33, 5, 5, 1, 1, 0.85),    # 3 input maps per wavefront, ragged 8 x 8 tile
+    (2, 9, 20, 20, 64, 5, 5, 1, 2, 0.9),      # Wo 20: 16-column tiles, several row groups
+    (1, 64, 9, 9, 17, 3, 3, 1, 1, 0.9),       # 3x3: 8 maps per wavefront
+    (2, 13, 30, 30, 64, 3, 3, 1, 0, 0.8),     # Wo 28: single-row tiles, ragged phases
+    (1, 100, 6, 6, 64, 1, 1, 1, 0, 0.9),      # 1x1, many input maps
+    (300, 2, 5, 5, 3, 5, 5, 1, 2, 0.5),       # many images, 5 x 5 maps padded
+]
 
 
 @pytest.mark.parametrize("case", FUSED_CASES)
@@ -408,8 +417,16 @@ def test_sparse_conv_fused_entry(torch, isc, case):
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
     assert isc.isc_sparse_kernel(desc) == "fused"
     x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=11 + sum(case[:9]))
-    y = isc.isc_sparse_conv_fused(to_dev(torch, x), to_dev(torch, w), T, P).cpu().numpy()
-    assert_conv_close(y, oracle.conv2d_f64(x, w, T, P), "fused %s" % (case,))
+    wt = isc.isc_repack_filter(to_dev(torch, w))
+    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+    want = oracle.conv2d_f64(x, w, T, P)
+    assert_conv_close(y, want, "fused %s" % (case,))
+    y2 = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), T, P, path="sparse").cpu().numpy()
+    assert np.array_equal(y, y2), "the sparse path and the fused entry point differ"
+    # integer-valued inputs: every fp32 sum is exact, so the result is bitwise
+    xi, wi = workloads.integer_case(N, C, H, W, K, R, S, seed=5 + sum(case[:9]))
+    yi = isc.isc_sparse_conv_fused(to_dev(torch, xi), isc.isc_repack_filter(to_dev(torch, wi)), T, P)
+    assert np.array_equal(yi.cpu().numpy().astype(np.float64), oracle.conv2d_f64(xi, wi, T, P))
 
 
 def test_sparse_conv_fused_rejects_ineligible(torch, isc):
@@ -417,5 +434,5 @@ def test_sparse_conv_fused_rejects_ineligible(torch, isc):
     x = torch.zeros((1, 2, 12, 12), device="cuda")
     w = torch.zeros((65, 2, 5, 5), device="cuda")
     with pytest.raises(isc.IscError) as e:
-        isc.isc_sparse_conv_fused(x, w, 1, 0)
+        isc.isc_sparse_conv_fused(x, isc.isc_repack_filter(w), 1, 0)
     assert e.value.status == 3
