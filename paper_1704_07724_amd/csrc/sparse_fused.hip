@@ -11,13 +11,12 @@
 // lists or row offsets in memory.
 //
 // The filter comes in the K-contiguous layout of ISC step 2 (wt[crs][64],
-// written by the repack).  Wavefront w owns a TH x TW output tile (tile
-// machinery in sparse_tile.hpp) of row group w / cs and the input channels
-// c = (w mod cs) + i*cs, at most MAXCH of them: at the start it copies those
-// channels' weight blocks into its own LDS region by direct global->LDS
-// loads (no registers, no workgroup barrier), and per channel it reads the
-// channel's R*S weights (64 output maps, one per lane) into registers.  The
-// cs partial tiles of a row group are then summed through LDS in phase order
+// written by the repack); the workgroup copies all of it into LDS by direct
+// global->LDS loads (no registers), and per channel a wavefront reads the
+// channel's R*S weights (64 output maps, one per lane) into registers.
+// Wavefront w owns a TH x TW output tile (tile machinery in sparse_tile.hpp)
+// of row group w / cs and the input channels c = (w mod cs) + i*cs.  The cs
+// partial tiles of a row group are then summed through LDS in phase order
 // and stored to NCHW (step 3) with consecutive threads on consecutive
 // columns of one output map.
 // Summation order per output is fixed for a given launch shape, so results
@@ -38,10 +37,6 @@ constexpr int kMaxTile = 64;     // accumulators per lane
 constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
 constexpr int kWPitch = 64;      // maps per filter column in the repacked layout (K <= 64)
 
-// Channels a wavefront may own: their weight blocks (R*S*64 floats each)
-// sit in the wavefront's LDS region for the whole walk.
-constexpr int max_channels(int RS2) { return RS2 == 25 ? 3 : (RS2 == 9 ? 8 : 32); }
-constexpr size_t weights_lds_bytes(int RS2) { return sizeof(float) * kWaves * max_channels(RS2) * RS2 * kWPitch; }
 
 struct FusedArgs {
     const float *x;   // N x C x H x W
@@ -59,11 +54,10 @@ __global__ __launch_bounds__(kWaves * kLanes)
 void sparse_conv_fused_kernel(FusedArgs a) {
     using T = tile::Shape<RS_, RS_, 1, TH, TW>;
     constexpr int R = RS_, S = RS_, RS2 = RS_ * RS_, EPL = T::EPL;
-    constexpr int MAXCH = max_channels(RS2);
     constexpr int NS = 4;  // input-window register ring
 
-    // [wave][MAXCH][R*S][64] weight blocks during the walk, then the phase
-    // tiles [wave][TH*TW][kRPad]
+    // the filter [C*R*S][64] during the walk, then the phase tiles
+    // [wave][TH*TW][kRPad]
     extern __shared__ float lds[];
 
     const int tid = threadIdx.x;
@@ -79,7 +73,7 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     const bool rows_ok = oy0 < a.Ho;
     const size_t HW = static_cast<size_t>(H) * W;
     const float *x_n = a.x + static_cast<size_t>(n) * C * HW;
-    // this wavefront's channels: phase, phase + cs, ... (at most MAXCH)
+    // this wavefront's channels: phase, phase + cs, ...
     const int ncw = phase < C ? (C - 1 - phase) / cs + 1 : 0;
 
     // lane l of register q holds window element e = q*64 + l in leaf-key
@@ -108,28 +102,24 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     };
     if (ncw > 0) tile::static_for<0, NS - 1>([&](auto sl) { issue(sl, decltype(sl)::value); });
 
-    // this wavefront's channels' weight blocks into its LDS region, in flight
-    // before the decision is read so that the two latencies overlap: RS2/4
-    // direct loads of 1 KB and RS2%4 of 256 bytes per channel, copying the
-    // block as laid out in wt
-    float *wlds = lds + static_cast<size_t>(wave) * MAXCH * RS2 * kWPitch;
-#pragma unroll
-    for (int i = 0; i < MAXCH; ++i)
-        if (i < ncw) {
-            const float *wc = a.wt + static_cast<size_t>(phase + i * cs) * RS2 * kWPitch;
-            float *dstc = wlds + i * RS2 * kWPitch;
-#pragma unroll
-            for (int d = 0; d < RS2 / 4; ++d)
-                tile::load_lds16(wc + d * 4 * kWPitch + lane * 4, reinterpret_cast<float4 *>(dstc + d * 4 * kWPitch));
-#pragma unroll
-            for (int d = (RS2 / 4) * 4; d < RS2; ++d)
-                tile::load_lds4(wc + d * kWPitch + lane, dstc + d * kWPitch);
-        }
+    // the filter into LDS, in flight before the decision is read so that the
+    // two latencies overlap: 1 KB blocks (4 filter columns) spread over the
+    // wavefronts, then single 256-byte columns for a remainder
+    {
+        const int ncol = C * RS2;
+        const int nblk = ncol >> 2;
+        for (int b = wave; b < nblk; b += kWaves)
+            tile::load_lds16(a.wt + b * 4 * kWPitch + lane * 4, reinterpret_cast<float4 *>(lds + b * 4 * kWPitch));
+        for (int t = nblk * 4 + wave; t < ncol; t += kWaves)
+            tile::load_lds4(a.wt + t * kWPitch + lane, lds + t * kWPitch);
+    }
 
-    if (!decision_gate(a.dec, 1u)) return;
-    // the weight blocks have landed in LDS (every load issued so far)
+    const bool run = decision_gate(a.dec, 1u);
+    // every wavefront's part of the filter has landed in LDS (also before an
+    // early exit: no load into LDS may outlive the workgroup)
     tile::wait_vm<0, true>();
-    asm volatile("" ::: "memory");
+    if (!run) return;
+    __syncthreads();
 
     tile::Acc<T> acc;
 #pragma unroll
@@ -160,7 +150,7 @@ void sparse_conv_fused_kernel(FusedArgs a) {
             any |= mask[q] != 0ull;
         }
         if (!any) continue;
-        tile::load_weights<T>(wlds + i * RS2 * kWPitch, lane, w, kWPitch);
+        tile::load_weights<T>(lds + static_cast<size_t>(phase + i * cs) * RS2 * kWPitch, lane, w, kWPitch);
         tile::wait_lgkm0();
         tile::walk_scan<T>(mask, cur, acc, w);
     }
@@ -216,43 +206,47 @@ struct FusedPlan {
 
 int fused_tw(int Wo) { return Wo <= 8 ? 8 : (Wo <= 16 ? 16 : 28); }
 
-size_t fused_lds(int rs2, int th, int tw) {
-    return std::max(weights_lds_bytes(rs2), sizeof(float) * kWaves * th * tw * kRPad);
+size_t fused_lds(int crs, int th, int tw) {
+    return std::max(sizeof(float) * crs * kWPitch, sizeof(float) * kWaves * th * tw * kRPad);
 }
 
-// Fewest channel phases that keep every wavefront within max_channels(R*S),
-// then the tallest tile (up to kMaxTile accumulators per lane) whose
-// workgroups still number at least kMinGroups (else the one with most
-// workgroups).  ISC_FUSED_TH caps the tile height and ISC_FUSED_CS raises
-// the phases (for measurements).
+// The filter must fit in LDS.  Tile height and channel phases: the tallest
+// tile (up to kMaxTile accumulators per lane), then the fewest phases that
+// leave no row group of a workgroup idle (rg <= ceil(Ho / TH)), preferring
+// plans with at least kMinGroups workgroups; else the plan with most
+// workgroups.  ISC_FUSED_TH caps the tile height and ISC_FUSED_CS fixes the
+// phases (for measurements).
 bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     if (sh.Wo > 28 || sh.K > kLanes) return false;
-    const int maxch = max_channels(sh.R * sh.S);
-    int cs = 1;
-    while (cs <= kWaves && (sh.C + cs - 1) / cs > maxch) cs *= 2;
-    if (cs > kWaves) return false;
-    if (const char *env = std::getenv("ISC_FUSED_CS")) {
-        const int v = std::atoi(env);
-        if (v >= cs && v <= kWaves && kWaves % v == 0) cs = v;
-    }
+    const int crs = sh.C * sh.R * sh.S;
+    if (static_cast<size_t>(crs) * kWPitch * sizeof(float) > kLdsMax) return false;
     const int tw = fused_tw(sh.Wo);
-    int th_cap = 8;
+    int th_cap = 8, cs_fix = 0;
     if (const char *env = std::getenv("ISC_FUSED_TH")) th_cap = std::max(1, std::atoi(env));
-    const int rg = kWaves / cs;
+    if (const char *env = std::getenv("ISC_FUSED_CS")) cs_fix = std::atoi(env);
     bool found = false;
     int64_t best_groups = 0;
     for (int th : {8, 4, 2, 1}) {
         if (th * tw > kMaxTile || th > th_cap) continue;
-        const int64_t groups = static_cast<int64_t>(sh.N) * ((sh.Ho + rg * th - 1) / (rg * th));
-        if (!found || groups > best_groups) {
-            *plan = FusedPlan{th, tw, cs, fused_lds(sh.R * sh.S, th, tw)};
-            best_groups = groups;
-            found = true;
+        const int rows_need = (sh.Ho + th - 1) / th;
+        for (int cs : {1, 2, 4, 8}) {
+            if (cs_fix > 0 && cs != cs_fix) continue;
+            const int rg = kWaves / cs;
+            if (cs_fix == 0 && rg > rows_need && cs < kWaves) continue;  // idle row groups
+            const int64_t groups = static_cast<int64_t>(sh.N) * ((sh.Ho + rg * th - 1) / (rg * th));
+            const size_t lds = fused_lds(crs, th, tw);
+            if (lds > kLdsMax) continue;
+            if (!found || groups > best_groups) {
+                *plan = FusedPlan{th, tw, cs, lds};
+                best_groups = groups;
+                found = true;
+            }
+            if (groups >= kMinGroups) return true;
+            break;  // more phases only add partial tiles
         }
-        if (groups >= kMinGroups) break;
     }
-    return found && plan->lds <= kLdsMax;
+    return found;
 }
 
 template <int RS_, int TH, int TW>

@@ -79,8 +79,10 @@ __device__ __forceinline__ void dispatch(int q, Acc<SH> &acc, const Wts<SH> &w, 
 }
 
 // One nonzero: the computed-jump dispatch (generated inline assembly) for
-// one-map-per-lane tiles; the binary tree otherwise.  ISC_TREE_DISPATCH
-// selects the tree everywhere (for measurements).
+// single-row one-map-per-lane tiles, whose leaves are short and whose trees
+// are deepest; the binary tree otherwise (measured faster for taller tiles,
+// whose leaves are long: the jump lands on a cold fetch of a padded leaf).
+// ISC_TREE_DISPATCH selects the tree everywhere (for measurements).
 #ifdef ISC_TREE_DISPATCH
 constexpr bool kJumpDispatch = false;
 #else
@@ -89,7 +91,8 @@ constexpr bool kJumpDispatch = true;
 
 template <typename SH>
 __device__ __forceinline__ void dispatch_one(int key, int vbits, Acc<SH> &acc, const Wts<SH> &w) {
-    if constexpr (kJumpDispatch && SH::KPL == 1 && SH::R == SH::S && AsmDispatch<SH::R, SH::TH, SH::TW>::kAvailable) {
+    if constexpr (kJumpDispatch && SH::KPL == 1 && SH::R == SH::S && SH::TH == 1 &&
+                  AsmDispatch<SH::R, SH::TH, SH::TW>::kAvailable) {
         AsmDispatch<SH::R, SH::TH, SH::TW>::run(key, vbits, acc, w);
     } else {
         dispatch<SH, 0, SH::WROWS * SH::WCOLS>(key, acc, w, __int_as_float(vbits));

@@ -26,7 +26,7 @@ def disassembly(tmp_path_factory):
     B.generate()
     out = tmp_path_factory.mktemp("dispatch")
     texts = {}
-    for name in ("sparse_fused.hip", "sparse_res.hip"):
+    for name in ("sparse_reg.hip", "sparse_res.hip"):
         obj = str(out / (name + ".o"))
         cmd = ([B.HIPCC] + B.DEVICE_FLAGS + B.FILE_FLAGS.get(name, []) +
                ["--offload-device-only", "--no-gpu-bundle-output", "-c", os.path.join(B.CSRC, name), "-o", obj])
@@ -67,7 +67,7 @@ def dispatch_sites(text):
     return sites
 
 
-@pytest.mark.parametrize("name", ["sparse_fused.hip", "sparse_res.hip"])
+@pytest.mark.parametrize("name", ["sparse_reg.hip", "sparse_res.hip"])
 def test_jump_tables_exact(disassembly, name):
     text = disassembly[name]
     sites = dispatch_sites(text)
