@@ -177,25 +177,27 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
 
 /* ISC steps 1-3 (Sec. "Sparse Convolution") in one launch with no workspace:
  * each wavefront compacts the input rows it needs on the fly (a ballot of
- * the zero test, walked in row-major order) and multiplies each nonzero by
- * the K-contiguous weight vectors of step 2, which it holds in registers.
- * The kernel isc_conv2d's sparse path runs when isc_sparse_kernel reports
- * ISC_KERNEL_FUSED (isc_conv2d repacks the filter itself, in the launch that
- * counts the nonzeros); no sparse/dense decision here.
+ * the zero test over its window, scanned in row-major order) and multiplies
+ * each nonzero by the K-contiguous weight vectors of step 2, which it holds
+ * in registers.  The filter is resident in LDS when it fits (K <= 64:
+ * ISC_KERNEL_FUSED) and streamed through LDS otherwise
+ * (ISC_KERNEL_FUSED_RING).  The kernels isc_conv2d's sparse path runs when
+ * isc_sparse_kernel reports either (isc_conv2d repacks the filter itself, in
+ * the launch that counts the nonzeros); no sparse/dense decision here.
  *   x: device input as for isc_conv2d.
  *   wt: the repacked filter of isc_repack_filter for K, C, R, S of d.
  *   y: device output N x K x Ho x Wo, fully written, must not overlap x or
  *     wt.
  * Deterministic (fixed summation order per output).  Errors: NULL, SHAPE,
- * LIMIT (shape not eligible: stride 1, square 1x1/3x3/5x5 filter, K <= 64,
- * Wo <= 28, at most 24 (5x5), 64 (3x3) or 256 (1x1) input maps), ALIAS,
- * ALIGN, DEVICE, HIP. */
+ * LIMIT (shape not eligible: stride 1 and a square 1x1, 3x3 or 5x5 filter
+ * are required), ALIAS, ALIGN, DEVICE, HIP. */
 int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y,
                           void *stream);
 
 /* Which kernel isc_conv2d's sparse path runs for this descriptor, reported in
- * *kernel: ISC_KERNEL_FUSED (compaction on the fly, isc_sparse_conv_fused),
- * else the kernel over compacted lists that isc_sparse_conv also runs:
+ * *kernel: ISC_KERNEL_FUSED or ISC_KERNEL_FUSED_RING (compaction on the fly,
+ * isc_sparse_conv_fused; filter resident in or streamed through LDS), else
+ * the kernel over compacted lists that isc_sparse_conv also runs:
  * ISC_KERNEL_RESIDENT (filter resident in LDS), ISC_KERNEL_RING (filter
  * streamed through LDS) or ISC_KERNEL_GENERIC (any filter and stride);
  * ISC_KERNEL_NONE if no sparse kernel fits (AUTO then runs dense).
@@ -205,7 +207,8 @@ enum isc_kernel {
     ISC_KERNEL_FUSED = 1,
     ISC_KERNEL_RESIDENT = 2,
     ISC_KERNEL_RING = 3,
-    ISC_KERNEL_GENERIC = 4
+    ISC_KERNEL_GENERIC = 4,
+    ISC_KERNEL_FUSED_RING = 5
 };
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel);
 

@@ -304,7 +304,8 @@ int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {
     int st = check_desc(d, &s);
     if (st) return st;
     const isc::SparseShape sh = sparse_shape(s);
-    *kernel = isc::sparse_fused_applies(sh) ? ISC_KERNEL_FUSED : isc::list_kernel_for(sh);
+    const int fused = isc::sparse_fused_kernel(sh);
+    *kernel = fused ? fused : isc::list_kernel_for(sh);
     return ISC_OK;
 }
 

@@ -102,9 +102,16 @@ struct SparseShape {
 
 // ISC steps 1-3 in one launch, compacting on the fly from x, with the filter
 // repacked K-contiguous (launch_repack_filter's layout; stride 1, square
-// 1x1/3x3/5x5 filters, K <= 64, Wo <= 28, few enough input maps).
+// 1x1/3x3/5x5 filters).
+// The filter-resident kernel takes filters that fit in LDS (K <= 64); the
+// filter-ring kernel (sparse_fring.hip) streams larger ones through LDS.
 bool sparse_fused_applies(const SparseShape &sh);
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
+                               hipStream_t s);
+bool sparse_fring_applies(const SparseShape &sh);
+// 1 (filter-resident), 5 (filter-ring) or 0 (neither): isc_sparse_kernel's ids.
+int sparse_fused_kernel(const SparseShape &sh);
+hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s);
 
 // Which kernel runs over compacted lists for a shape (the values are those

@@ -288,13 +288,20 @@ hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s
 
 bool sparse_fused_applies(const SparseShape &sh) {
     FusedPlan p;
-    return fused_plan(sh, &p);
+    return fused_plan(sh, &p) || sparse_fring_applies(sh);
 }
 
+int sparse_fused_kernel(const SparseShape &sh) {
+    FusedPlan p;
+    return fused_plan(sh, &p) ? 1 : (sparse_fring_applies(sh) ? 5 : 0);
+}
+
+// The filter-resident kernel when the filter fits in LDS, else the
+// filter-ring kernel.
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s) {
     FusedPlan p;
-    if (!fused_plan(sh, &p)) return hipErrorInvalidValue;
+    if (!fused_plan(sh, &p)) return launch_sparse_fring(sh, x, wt, y, dec, s);
     FusedArgs a{};
     a.x = x;
     a.wt = wt;

@@ -63,10 +63,14 @@ def test_workspace_sizes_ordered():
     # filter (C*R*S x 64 floats) only
     assert de < 4096
     assert 20 * 25 * 64 * 4 <= sp < 20 * 25 * 64 * 4 + 8192
-    # more output maps than one pass holds: the sparse path keeps the lists (8
-    # bytes per input element) and the repacked filter
+    # more output maps than one pass holds: the filter is streamed, the input
+    # still compacted on the fly -- the repacked filter and no lists
     d2 = isc.make_desc(2, 96, 27, 27, 256, 5, 5, 1, 2)
-    assert isc.isc_workspace_size(d2, "sparse") >= 2 * 96 * 27 * 27 * 8 + 96 * 25 * 256 * 4
+    assert 96 * 25 * 256 * 4 <= isc.isc_workspace_size(d2, "sparse") < 96 * 25 * 256 * 4 + 8192
+    # a shape no on-the-fly kernel takes (stride 2): the lists (8 bytes per
+    # input element) and the repacked filter
+    d3 = isc.make_desc(2, 96, 27, 27, 256, 5, 5, 2, 2)
+    assert isc.isc_workspace_size(d3, "sparse") >= 2 * 96 * 27 * 27 * 8 + 96 * 25 * 256 * 4
     # C*R*S >= 2^16: the dense path materialises C*R*S rows of >= N*Ho*Wo floats
     big = isc.make_desc(1, 2700, 6, 6, 8, 5, 5, 1, 0)
     assert isc.isc_workspace_size(big, "dense") >= 2700 * 25 * 2 * 2 * 4
@@ -138,17 +142,19 @@ def test_sparse_kernel_choice(monkeypatch):
     d = isc.make_desc
     assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused"    # LeNet conv2
     assert isc.isc_sparse_kernel(d(128, 16, 28, 28, 32, 5, 5, 1, 2)) == "fused"    # inception 5x5
-    assert isc.isc_sparse_kernel(d(128, 96, 27, 27, 256, 5, 5, 1, 2)) == "ring"    # AlexNet conv2
-    assert isc.isc_sparse_kernel(d(128, 96, 28, 28, 128, 3, 3, 1, 1)) == "ring"    # inception 3x3
+    assert isc.isc_sparse_kernel(d(128, 96, 27, 27, 256, 5, 5, 1, 2)) == "fused_ring"  # AlexNet conv2
+    assert isc.isc_sparse_kernel(d(128, 384, 13, 13, 256, 3, 3, 1, 1)) == "fused_ring"  # AlexNet conv5
+    assert isc.isc_sparse_kernel(d(128, 96, 28, 28, 128, 3, 3, 1, 1)) == "fused_ring"  # inception 3x3
+    assert isc.isc_sparse_kernel(d(1, 3, 20, 200, 66, 3, 3, 1, 1)) == "fused_ring"     # column tiles
     assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 64, 5, 5, 2, 1)) == "generic"     # stride 2
     assert isc.isc_sparse_kernel(d(1, 3, 10, 9, 9, 2, 3, 1, 1)) == "generic"       # 2 x 3 filter
-    assert isc.isc_sparse_kernel(d(1, 3, 20, 200, 66, 3, 3, 1, 1)) == "generic"    # rows too wide to stage
+    assert isc.isc_sparse_kernel(d(1, 3, 9, 9, 9, 7, 7, 1, 3)) == "generic"        # 7 x 7 filter
 
 
 def test_fused_entry_validation():
     L = isc.lib()
     ok = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 1, 0)
-    big_k = isc.make_desc(1, 2, 12, 12, 65, 5, 5, 1, 0)       # K > 64: not taken
+    big_k = isc.make_desc(1, 2, 12, 12, 65, 7, 7, 1, 0)       # 7 x 7 filter: not taken
     strided = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 2, 0)      # stride 2: not taken
     x, w, y = 0x1000, 0x200000, 0x400000
     assert L.isc_sparse_conv_fused(None, x, w, y, None) == 1

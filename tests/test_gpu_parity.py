@@ -396,7 +396,7 @@ def test_full_size_sampled(torch, isc, layer):
     torch.cuda.empty_cache()
 
 
-FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (1, 3, 5) and c[4] <= 64] + [
+FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (1, 3, 5)] + [
     # N, C, H, W, K, R, S, T, P, sparsity: the fused kernel's plans
     (3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9),     # LeNet conv2: 8 phases (3 or 2 maps each), one 8 x 8 tile
     (2, 24, 11, 11, 33, 5, 5, 1, 1, 0.85),    # 3 input maps per wavefront, ragged 8 x 8 tile
@@ -405,6 +405,14 @@ FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (
     (2, 13, 30, 30, 64, 3, 3, 1, 0, 0.8),     # Wo 28: single-row tiles, ragged phases
     (1, 100, 6, 6, 64, 1, 1, 1, 0, 0.9),      # 1x1, many input maps
     (300, 2, 5, 5, 3, 5, 5, 1, 2, 0.5),       # many images, 5 x 5 maps padded
+    # filter streamed through LDS (K > 64 or a filter larger than LDS)
+    (2, 9, 27, 27, 256, 5, 5, 1, 2, 0.9),     # AlexNet conv2-like: 4 maps per lane
+    (2, 11, 13, 13, 384, 3, 3, 1, 1, 0.95),   # conv3/4-like: 6 maps per lane
+    (1, 7, 13, 13, 200, 3, 3, 1, 1, 0.9),     # ragged last map group
+    (2, 5, 28, 28, 128, 3, 3, 1, 1, 0.9),     # inception 3x3-like
+    (1, 4, 9, 70, 96, 5, 5, 1, 2, 0.8),       # column tiles, ragged last tile
+    (3, 3, 6, 6, 130, 1, 1, 1, 0, 0.7),       # 1x1
+    (1, 300, 5, 5, 20, 5, 5, 1, 2, 0.9),      # filter of 64 maps larger than LDS
 ]
 
 
@@ -415,7 +423,7 @@ def test_sparse_conv_fused_entry(torch, isc, case):
     N, C, H, W, K, R, S, T, P, sp = case
     note("fused entry", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
-    assert isc.isc_sparse_kernel(desc) == "fused"
+    assert isc.isc_sparse_kernel(desc) in ("fused", "fused_ring")
     x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=11 + sum(case[:9]))
     wt = isc.isc_repack_filter(to_dev(torch, w))
     y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
@@ -432,7 +440,7 @@ def test_sparse_conv_fused_entry(torch, isc, case):
 def test_sparse_conv_fused_rejects_ineligible(torch, isc):
     note("fused ineligible")
     x = torch.zeros((1, 2, 12, 12), device="cuda")
-    w = torch.zeros((65, 2, 5, 5), device="cuda")
+    w = torch.zeros((65, 2, 7, 7), device="cuda")
     with pytest.raises(isc.IscError) as e:
         isc.isc_sparse_conv_fused(x, isc.isc_repack_filter(w), 1, 0)
     assert e.value.status == 3
