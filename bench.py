@@ -145,7 +145,7 @@ class LayerRun:
         on-the-fly compaction (isc_sparse_conv_fused) or the kernel over
         compacted lists (isc_sparse_conv)."""
         L = self.layer
-        if self.kernel == "fused":
+        if self.kernel in ("fused", "fused_ring"):
             return lambda: self.isc.isc_sparse_conv_fused(self.x, self.wt, L.T, L.P, out=self.y)
         return lambda: self.isc.isc_sparse_conv(self.x.shape, self.lists, self.wt, L.T, L.P,
                                                 out=self.y)
@@ -270,36 +270,44 @@ def counted_traffic():
 
 def algorithmic_bytes(run) -> dict:
     """Bytes each kernel of the path must move at least once, per launch:
-    compaction reads the input and writes the lists, the sparse kernel reads
-    lists, row offsets and repacked weights and writes the output (the fused
-    kernel reads the input and the repacked filter instead), im2col
-    reads the input and writes the unrolled matrix."""
+    the AUTO step's count-and-repack kernel reads the input and the filter and
+    writes the repacked filter (and, on shapes the on-the-fly kernels do not
+    take, the compaction writes the lists); the sparse kernel reads the input
+    and the repacked filter and writes the output (over lists: lists, row
+    offsets and repacked filter); the dense GEMM reads the input and the
+    filter and writes the output."""
     L = run.layer
     planes = L.N * L.C
     row_ptr = planes * (L.H + 1) * 4
     x_bytes = run.x_host.size * 4
     y_bytes = L.N * L.K * run.Ho * run.Wo * 4
+    w_bytes = L.K * L.C * L.R * L.S * 4
     kp = (L.K + 63) // 64 * 64
-    if run.kernel == "fused":   # reads x and the repacked filter once, writes y
-        sparse = x_bytes + L.C * L.R * L.S * kp * 4 + y_bytes
-    else:                       # lists, row offsets, repacked filter; writes y
-        sparse = run.nnz * 8 + row_ptr + L.C * L.R * L.S * kp * 4 + y_bytes
+    wt_bytes = L.C * L.R * L.S * kp * 4
+    if run.kernel in ("fused", "fused_ring"):   # reads x and the repacked filter once, writes y
+        sparse = x_bytes + wt_bytes + y_bytes
+        prep = x_bytes + w_bytes + wt_bytes
+    else:                                        # lists, row offsets, repacked filter; writes y
+        sparse = run.nnz * 8 + row_ptr + wt_bytes + y_bytes
+        prep = x_bytes + run.nnz * 8 + row_ptr + w_bytes + wt_bytes
     return {
+        "count_repack": prep,
         "compact": x_bytes + run.nnz * 8 + row_ptr,
         "sparse_kernel": sparse,
-        "im2col": x_bytes + L.C * L.R * L.S * L.N * run.Ho * run.Wo * 4,
+        "dense_gemm": x_bytes + w_bytes + y_bytes,
     }
 
 
 def probe(torch, isc, layer, n):
     """Short eager program for counter runs: a copy kernel moving a known
-    number of bytes (the scale of the HBM counters), then each kernel of the
-    layer n times."""
+    number of bytes (the scale of the HBM counters), then n launches each of
+    the sparse kernel alone, the whole AUTO step (count and repack, sparse
+    kernel, the dense kernel that exits on the decision) and the dense path."""
     run = LayerRun(torch, isc, layer)
     src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
     dst = torch.empty_like(src)
-    steps = [("copy", lambda: torch.mul(src, 1.0, out=dst)), ("compact", run.compact()),
-             ("sparse_kernel", run.sparse_kernel()), ("im2col", run.im2col())]
+    steps = [("copy", lambda: torch.mul(src, 1.0, out=dst)), ("sparse_kernel", run.sparse_kernel()),
+             ("auto", run.conv("auto")), ("dense", run.conv("dense"))]
     for name, fn in steps:
         for _ in range(n):
             fn()

@@ -61,14 +61,14 @@ void im2col_kernel(const float *__restrict__ x, int C, int H, int W, int R, int 
 //
 // Workgroup tile BM x BN = (WAVES_M * WM * 32) x (WAVES_N * WN * 32), four
 // wavefronts, each owning WM x WN blocks of 32 x 32 accumulated by
-// v_mfma_f32_32x32x2_f32.  K-slices of BK = 16 go through two LDS buffers;
+// v_mfma_f32_32x32x2_f32.  K-slices of BK (16, or 32 for the 64 x 64 tile of
+// small grids, whose K loop is latency-bound) go through two LDS buffers;
 // the next slice's global loads are in flight while the current one feeds
 // the matrix cores.  A slices are stored transposed ([k][m]) so that both
 // operands are read by 32 consecutive lanes at consecutive addresses.
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int BK = 16;
 
 struct GemmArgs {
     int M, N, Kd;
@@ -92,7 +92,7 @@ __device__ __forceinline__ int divm(int k, int d, uint32_t m) {
     return d == 1 ? k : static_cast<int>(__umulhi(static_cast<uint32_t>(k), m));
 }
 
-template <int WAVES_M, int WM, int WN, bool A_VEC, bool B_PADDED, bool IMPLICIT>
+template <int WAVES_M, int WM, int WN, bool A_VEC, bool B_PADDED, bool IMPLICIT, int BK>
 __global__ __launch_bounds__(256)
 void gemm_f32_kernel(GemmArgs g) {
     if (!decision_gate(g.dec, 2u)) return;
@@ -300,28 +300,37 @@ void gemm_f32_kernel(GemmArgs g) {
     }
 }
 
-template <int WAVES_M, int WM, int WN>
+template <int WAVES_M, int WM, int WN, int BK = 16>
 hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, bool implicit, hipStream_t s) {
     constexpr int BM = WAVES_M * WM * 32;
     constexpr int BN = (4 / WAVES_M) * WN * 32;
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
     if (implicit) {
-        if (a_vec) gemm_f32_kernel<WAVES_M, WM, WN, true, false, true><<<grid, 256, 0, s>>>(g);
-        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, true><<<grid, 256, 0, s>>>(g);
+        if (a_vec) gemm_f32_kernel<WAVES_M, WM, WN, true, false, true, BK><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, true, BK><<<grid, 256, 0, s>>>(g);
     } else if (a_vec) {
-        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, true, true, false><<<grid, 256, 0, s>>>(g);
-        else gemm_f32_kernel<WAVES_M, WM, WN, true, false, false><<<grid, 256, 0, s>>>(g);
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, true, true, false, BK><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, true, false, false, BK><<<grid, 256, 0, s>>>(g);
     } else {
-        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, false, true, false><<<grid, 256, 0, s>>>(g);
-        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, false><<<grid, 256, 0, s>>>(g);
+        if (b_padded) gemm_f32_kernel<WAVES_M, WM, WN, false, true, false, BK><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, false, BK><<<grid, 256, 0, s>>>(g);
     }
     return hipGetLastError();
 }
 
 hipError_t launch_gemm_any(const GemmArgs &g, bool a_vec, bool b_vec, bool implicit, hipStream_t s) {
-    // tile height follows M: 32 (skinny), 64, or 128 rows per workgroup
-    if (g.M <= 32) return launch_gemm_t<1, 1, 2>(g, a_vec, b_vec, implicit, s);   // 32 x 256
-    if (g.M <= 64) return launch_gemm_t<2, 1, 2>(g, a_vec, b_vec, implicit, s);   // 64 x 128
+    // tile height follows M: 32 (skinny), 64, or 128 rows per workgroup; the
+    // narrower tile of a height when the wider one leaves fewer than two
+    // workgroups per CU
+    constexpr int kWideGrid = 512;
+    if (g.M <= 32) {
+        if ((g.N + 255) / 256 >= kWideGrid) return launch_gemm_t<1, 1, 2>(g, a_vec, b_vec, implicit, s);  // 32 x 256
+        return launch_gemm_t<1, 1, 1>(g, a_vec, b_vec, implicit, s);                                       // 32 x 128
+    }
+    if (g.M <= 64) {
+        if ((g.N + 127) / 128 >= kWideGrid) return launch_gemm_t<2, 1, 2>(g, a_vec, b_vec, implicit, s);  // 64 x 128
+        return launch_gemm_t<2, 1, 1, 32>(g, a_vec, b_vec, implicit, s);                                   // 64 x 64
+    }
     return launch_gemm_t<2, 2, 2>(g, a_vec, b_vec, implicit, s);                // 128 x 128
 }
 
