@@ -1,0 +1,246 @@
+// Filter-ring kernel (declarations and, for the per-filter-size translation
+// units that define ISC_FRING_INSTANTIATE, the kernel and its launchers).
+//
+// ISC steps 1-3 (Sec. "Sparse Convolution") in one launch for stride-1
+// convolutions with square 1x1, 3x3 or 5x5 filters whose filter does not fit
+// in LDS (many input or output maps: AlexNet conv2-5, an inception 3x3
+// branch): the input is compacted on the fly as in the filter-resident kernel
+// (sparse_fused.hip), and the filter is streamed through LDS.
+//
+// The four wavefronts of a workgroup own TH consecutive output rows each (4*TH
+// rows of one image), TW columns and 64*KPL output maps in registers (tile
+// machinery in sparse_tile.hpp).  Input channels go in order through a ring
+// of NBUF stages: stage c holds channel c's R*S*64*KPL weights (from the
+// K-contiguous repacked filter, by direct global->LDS loads, no registers)
+// and, in each wavefront's registers, the channel's input window of that
+// wavefront -- (TH+R-1) rows x (TW+S-1) columns in leaf-key order, padding
+// read as zero.  Stages are issued NBUF-1 channels ahead; one barrier per
+// channel, after a wait for exactly the stage consumed.  Per channel a
+// wavefront reads the weights into registers, takes a ballot of the zero test
+// over its window and scans the window statically (walk_scan): every set
+// position runs the straight-line block of its (row, column).  Each lane
+// finally stores its accumulators to NCHW (step 3).  Summation order per
+// output is fixed (channels in order, window order within a channel), so
+// results are deterministic.
+#pragma once
+
+#include "sparse_tile.hpp"
+
+namespace isc {
+namespace fring {
+
+using tile::kLanes;
+constexpr int kWaves = 4;
+constexpr size_t kLdsMax = 160 * 1024;
+
+struct FringArgs {
+    const float *x;   // N x C x H x W
+    const float *wt;  // [C][R][S][Kp], K contiguous, zero past K
+    float *y;         // N x K x Ho x Wo
+    int N, C, H, W, K, Kp, P, Ho, Wo;
+    int TWr;          // output columns per tile in use (<= TW)
+    int ctiles;       // column tiles per row
+    int bands;        // groups of kWaves * TH output rows
+    int kgroups;      // groups of 64 * KPL output maps
+    Decision dec;
+};
+
+// Register tiles instantiated: (KPL, TH) per filter size and tile width,
+// with TH * TW * KPL accumulators and R*S*KPL weights per lane.
+struct TileChoice {
+    int kpl, th;
+};
+
+constexpr int kMaxAcc = 112;      // accumulators per lane
+constexpr int kMaxRegs = 212;     // accumulators + weights per lane
+
+constexpr bool fring_fits(int RS, int KPL, int TH, int TW) {
+    return TH * TW * KPL <= kMaxAcc && TH * TW * KPL + RS * RS * KPL <= kMaxRegs;
+}
+
+// Launchers of the kernels of one filter size (sparse_fring_r{1,3,5}.hip).
+hipError_t launch_r1(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
+hipError_t launch_r3(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
+hipError_t launch_r5(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
+
+}  // namespace fring
+}  // namespace isc
+
+#ifdef ISC_FRING_INSTANTIATE
+namespace isc {
+namespace fring {
+namespace {
+
+template <int RS_, int KPL, int TH, int TW>
+struct FringShape {
+    using T = tile::Shape<RS_, RS_, KPL, TH, TW>;
+    static constexpr int RS2 = RS_ * RS_;
+    static constexpr int CHF = RS2 * T::KW;                  // floats of one channel's weights
+    static constexpr int NDW = (CHF + 255) / 256;            // 1 KB direct-to-LDS blocks
+    static constexpr int SLOT4 = NDW * kLanes;               // float4 per ring slot
+    static constexpr int NBUF = SLOT4 * 16 <= 16384 ? 4 : (SLOT4 * 16 <= 32768 ? 3 : 2);
+    static constexpr int DPW = (NDW + kWaves - 1) / kWaves;  // weight blocks per wavefront per stage
+    static constexpr int VPS = DPW + T::EPL;                 // vector-memory operations per stage
+    static constexpr size_t lds = sizeof(float4) * NBUF * SLOT4;
+};
+
+template <int RS_, int KPL, int TH, int TW>
+__global__ __launch_bounds__(kWaves * kLanes)
+void sparse_conv_fring_kernel(FringArgs a) {
+    using SH = FringShape<RS_, KPL, TH, TW>;
+    using T = typename SH::T;
+    constexpr int KW = T::KW, NDW = SH::NDW, NBUF = SH::NBUF, DPW = SH::DPW, EPL = T::EPL;
+
+    // ring of NBUF slots, each one channel's weights [R*S][KW] (k = kbase +
+    // lane*KPL + j) padded to whole 1 KB blocks; static, so that the compiler
+    // can tell the slot being read from the slots being filled
+    __shared__ float4 wring[NBUF][SH::SLOT4];
+
+    const int lane = threadIdx.x & (kLanes - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+    int b = blockIdx.x;
+    const int kg = b % a.kgroups;
+    b /= a.kgroups;
+    const int ct = b % a.ctiles;
+    b /= a.ctiles;
+    const int band = b % a.bands;
+    const int n = b / a.bands;
+    const int oy0 = (band * kWaves + wave) * TH;
+    const int ox0 = ct * a.TWr;
+    const int kbase = kg * KW;
+    const int C = a.C, H = a.H, W = a.W, P = a.P, Kp = a.Kp;
+    const bool rows_ok = oy0 < a.Ho;
+    const int tw = min(a.TWr, a.Wo - ox0);
+    const size_t HW = static_cast<size_t>(H) * W;
+    const float *x_n = a.x + static_cast<size_t>(n) * C * HW;
+
+    // lane l of register q holds window element e = q*64 + l in leaf-key
+    // order, e = wy * WCOLS + xp: input row oy0 - P + wy, column ox0 - P + xp.
+    // Elements outside the map (padding) or past the window read the plane's
+    // first element and never count as nonzero.
+    int xoff[EPL];
+    bool inwin[EPL];
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+        const int e = q * kLanes + lane;
+        const int wy = e / T::WCOLS;
+        const int y = oy0 - P + wy, xx = ox0 - P + (e - wy * T::WCOLS);
+        inwin[q] = rows_ok && e < T::WROWS * T::WCOLS && y >= 0 && y < H && xx >= 0 && xx < W;
+        xoff[q] = inwin[q] ? y * W + xx : 0;
+    }
+
+    // input windows, one register ring slot per weight slot
+    float xw[NBUF][EPL];
+
+    // stage c -> slot SLOT: weights by direct global->LDS loads (every
+    // wavefront issues exactly DPW blocks and EPL window loads, so the number
+    // of vector-memory operations per stage is the same everywhere)
+    auto issue = [&](auto slot_c, int c) {
+        constexpr int SLOT = decltype(slot_c)::value;
+#pragma unroll
+        for (int i = 0; i < DPW; ++i) {
+            const int d = min(wave + i * kWaves, NDW - 1);
+            const int f = d * 256 + lane * 4;  // float offset in the slot
+            int tap = f / KW;
+            const int koff = f - tap * KW;
+            tap = min(tap, SH::RS2 - 1);       // padding of the last block
+            const int k = min(kbase + koff, Kp - 4);
+            const float *src = a.wt + (static_cast<size_t>(c) * SH::RS2 + tap) * Kp + k;
+            tile::load_lds16(src, &wring[SLOT][d * kLanes]);
+        }
+        const float *plane = x_n + static_cast<size_t>(c) * HW;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) xw[SLOT][q] = plane[xoff[q]];
+    };
+
+    // prologue: stages 0 .. NBUF-2 in flight before the decision is read
+    // (past the last channel the last channel is loaded again, keeping the
+    // per-stage operation count fixed)
+    tile::static_for<0, NBUF - 1>([&](auto sl) { issue(sl, min(decltype(sl)::value, C - 1)); });
+    const bool run = decision_gate(a.dec, 1u);
+    if (!run) {
+        __builtin_amdgcn_s_waitcnt(0);  // no load into LDS may outlive the workgroup
+        return;
+    }
+
+    tile::Acc<T> acc;
+#pragma unroll
+    for (int y = 0; y < TH; ++y)
+#pragma unroll
+        for (int x = 0; x < TW; ++x)
+#pragma unroll
+            for (int j = 0; j < KPL; ++j) acc[y][x][j] = 0.0f;
+
+    // per channel: wait for its stage and the barrier, issue the stage NBUF-1
+    // channels ahead, then read the channel's weights (LDS -> registers) and
+    // copy its window into one set of registers, so that the scan (most of
+    // the code) is inlined once
+    float cur[EPL];
+    tile::Wts<T> w;
+#pragma unroll 1
+    for (int c = 0; c < C; ++c) {
+        tile::static_for<0, NBUF>([&](auto sl) {
+            constexpr int B = decltype(sl)::value;
+            if (c % NBUF == B) {
+                // stage c complete for every wavefront; everyone is done with
+                // stage c - 1, whose slot is refilled next
+                tile::wait_vm_and_barrier<(NBUF - 2) * SH::VPS>();
+                issue(std::integral_constant<int, (B + NBUF - 1) % NBUF>{}, min(c + NBUF - 1, C - 1));
+                tile::load_weights<T>(reinterpret_cast<const float *>(&wring[B][0]), lane, w);
+#pragma unroll
+                for (int q = 0; q < EPL; ++q) cur[q] = xw[B][q];
+                tile::wait_lgkm0();
+            }
+        });
+        unsigned long long mask[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) mask[q] = __ballot(inwin[q] && (__float_as_uint(cur[q]) & 0x7fffffffu) != 0u);
+        tile::walk_scan<T>(mask, cur, acc, w);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // no load into LDS may outlive the workgroup
+
+    // step 3: each lane stores its accumulators to NCHW
+    if (rows_ok) {
+        const size_t plane_out = static_cast<size_t>(a.Ho) * a.Wo;
+        float *yrow = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oy0) * a.Wo + ox0;
+        tile::store_tile<T>(acc, yrow, plane_out, a.Wo, kbase, lane, a.K, a.Ho - oy0, tw);
+    }
+}
+
+template <int RS_, int KPL, int TH, int TW>
+hipError_t launch_fring_t(const FringArgs &a, hipStream_t s) {
+    if constexpr (!fring_fits(RS_, KPL, TH, TW)) {
+        return hipErrorInvalidValue;
+    } else {
+        using SH = FringShape<RS_, KPL, TH, TW>;
+        static_assert(SH::lds <= kLdsMax, "weight ring exceeds LDS");
+        const int grid = a.N * a.bands * a.ctiles * a.kgroups;
+        sparse_conv_fring_kernel<RS_, KPL, TH, TW><<<grid, kWaves * kLanes, 0, s>>>(a);
+        return hipGetLastError();
+    }
+}
+
+template <int RS_, int KPL, int TW>
+hipError_t launch_fring_th(const FringArgs &a, int th, hipStream_t s) {
+    return th == 2 ? launch_fring_t<RS_, KPL, 2, TW>(a, s) : launch_fring_t<RS_, KPL, 1, TW>(a, s);
+}
+
+template <int RS_, int TW>
+hipError_t launch_fring_kpl(const FringArgs &a, const TileChoice &tc, hipStream_t s) {
+    switch (tc.kpl) {
+    case 6: return launch_fring_th<RS_, 6, TW>(a, tc.th, s);
+    case 4: return launch_fring_th<RS_, 4, TW>(a, tc.th, s);
+    case 2: return launch_fring_th<RS_, 2, TW>(a, tc.th, s);
+    default: return launch_fring_th<RS_, 1, TW>(a, tc.th, s);
+    }
+}
+
+template <int RS_>
+hipError_t launch_fring_rs(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s) {
+    return tw == 16 ? launch_fring_kpl<RS_, 16>(a, tc, s) : launch_fring_kpl<RS_, 28>(a, tc, s);
+}
+
+}  // namespace
+}  // namespace fring
+}  // namespace isc
+#endif

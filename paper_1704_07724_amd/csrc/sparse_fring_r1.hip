@@ -1,0 +1,14 @@
+// Filter-ring kernels for 1x1 filters (one translation unit per filter size,
+// compiled in parallel); the kernel is in sparse_fring.hpp.
+#define ISC_FRING_INSTANTIATE
+#include "sparse_fring.hpp"
+
+namespace isc {
+namespace fring {
+
+hipError_t launch_r1(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s) {
+    return launch_fring_rs<1>(a, tw, tc, s);
+}
+
+}  // namespace fring
+}  // namespace isc

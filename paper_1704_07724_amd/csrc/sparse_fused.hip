@@ -1,208 +1,13 @@
-// ISC steps 1-3 (Sec. "Sparse Convolution") in one launch, for stride-1
-// convolutions with square 1x1, 3x3 or 5x5 filters and at most 64 output
-// maps (few input maps: LeNet conv2, an inception 5x5 branch).
-//
-// The paper builds each input map's nonzero list on the fly before using it.
-// Here the list never leaves the wavefront: a wavefront loads the input rows
-// its output tile needs straight from x (coalesced, one element per lane),
-// takes a 64-bit ballot of the zero test per 64 elements, and walks the set
-// bits in lane order -- row-major order, the paper's list order -- reading
-// each nonzero's value and leaf key from its lane.  There are no compacted
-// lists or row offsets in memory.
-//
-// The filter comes in the K-contiguous layout of ISC step 2 (wt[crs][64],
-// written by the repack); the workgroup copies all of it into LDS by direct
-// global->LDS loads (no registers), and per channel a wavefront reads the
-// channel's R*S weights (64 output maps, one per lane) into registers.
-// Wavefront w owns a TH x TW output tile (tile machinery in sparse_tile.hpp)
-// of row group w / cs and the input channels c = (w mod cs) + i*cs.  The cs
-// partial tiles of a row group are then summed through LDS in phase order
-// and stored to NCHW (step 3) with consecutive threads on consecutive
-// columns of one output map.
-// Summation order per output is fixed for a given launch shape, so results
-// are deterministic.
-#include "sparse_tile.hpp"
+// Filter-resident kernel (sparse_fused.hpp): the plan, the launch, and the
+// choice between it and the filter-ring kernel.
+#include "sparse_fused.hpp"
 
 #include <algorithm>
 #include <cstdlib>
 
 namespace isc {
+namespace fused {
 namespace {
-
-using tile::kLanes;
-constexpr int kWaves = 8;
-constexpr size_t kLdsMax = 160 * 1024;
-constexpr int kRPad = 65;        // LDS pitch of one tile position's output maps (reduction)
-constexpr int kMaxTile = 64;     // accumulators per lane
-constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
-constexpr int kWPitch = 64;      // maps per filter column in the repacked layout (K <= 64)
-
-
-struct FusedArgs {
-    const float *x;   // N x C x H x W
-    const float *wt;  // [C*R*S][64], output map fastest, zero past K
-    float *y;         // N x K x Ho x Wo
-    int N, C, H, W, K, P, Ho, Wo;
-    int cs;           // channel phases per row group
-    int rg;           // row groups per workgroup (kWaves / cs)
-    int bands;        // groups of rg * TH output rows
-    Decision dec;
-};
-
-template <int RS_, int TH, int TW>
-__global__ __launch_bounds__(kWaves * kLanes)
-void sparse_conv_fused_kernel(FusedArgs a) {
-    using T = tile::Shape<RS_, RS_, 1, TH, TW>;
-    constexpr int R = RS_, S = RS_, RS2 = RS_ * RS_, EPL = T::EPL;
-    constexpr int NS = 4;  // input-window register ring
-
-    // the filter [C*R*S][64] during the walk, then the phase tiles
-    // [wave][TH*TW][kRPad]
-    extern __shared__ float lds[];
-
-    const int tid = threadIdx.x;
-    const int lane = tid & (kLanes - 1);
-    const int wave = __builtin_amdgcn_readfirstlane(tid / kLanes);
-    const int cs = a.cs;
-    const int phase = wave % cs;
-    const int rgi = wave / cs;
-    const int band = blockIdx.x % a.bands;
-    const int n = blockIdx.x / a.bands;
-    const int oy0 = (band * a.rg + rgi) * TH;
-    const int C = a.C, H = a.H, W = a.W, P = a.P;
-    const bool rows_ok = oy0 < a.Ho;
-    const size_t HW = static_cast<size_t>(H) * W;
-    const float *x_n = a.x + static_cast<size_t>(n) * C * HW;
-    // this wavefront's channels: phase, phase + cs, ...
-    const int ncw = phase < C ? (C - 1 - phase) / cs + 1 : 0;
-
-    // lane l of register q holds window element e = q*64 + l in leaf-key
-    // order, e = wy * WCOLS + xp: input row oy0 - P + wy, column xp - P.
-    // Elements outside the map (padding) or past the window read the plane's
-    // first element and never count as nonzero.
-    int xoff[EPL];
-    bool inwin[EPL];
-#pragma unroll
-    for (int q = 0; q < EPL; ++q) {
-        const int e = q * kLanes + lane;
-        const int wy = e / T::WCOLS;
-        const int y = oy0 - P + wy, xx = e - wy * T::WCOLS - P;
-        inwin[q] = rows_ok && e < T::WROWS * T::WCOLS && y >= 0 && y < H && xx >= 0 && xx < W;
-        xoff[q] = inwin[q] ? y * W + xx : 0;
-    }
-
-    // ring of NS register slots of input windows
-    float xv[NS][EPL];
-    auto issue = [&](auto slot_c, int i) {
-        constexpr int SLOT = decltype(slot_c)::value;
-        const int c = phase + min(i, ncw - 1) * cs;
-        const float *plane = x_n + static_cast<size_t>(c) * HW;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) xv[SLOT][q] = plane[xoff[q]];
-    };
-    if (ncw > 0) tile::static_for<0, NS - 1>([&](auto sl) { issue(sl, decltype(sl)::value); });
-
-    // the filter into LDS, in flight before the decision is read so that the
-    // two latencies overlap: 1 KB blocks (4 filter columns) spread over the
-    // wavefronts, then single 256-byte columns for a remainder
-    {
-        const int ncol = C * RS2;
-        const int nblk = ncol >> 2;
-        for (int b = wave; b < nblk; b += kWaves)
-            tile::load_lds16(a.wt + b * 4 * kWPitch + lane * 4, reinterpret_cast<float4 *>(lds + b * 4 * kWPitch));
-        for (int t = nblk * 4 + wave; t < ncol; t += kWaves)
-            tile::load_lds4(a.wt + t * kWPitch + lane, lds + t * kWPitch);
-    }
-
-    const bool run = decision_gate(a.dec, 1u);
-    // every wavefront's part of the filter has landed in LDS (also before an
-    // early exit: no load into LDS may outlive the workgroup)
-    tile::wait_vm<0, true>();
-    if (!run) return;
-    __syncthreads();
-
-    tile::Acc<T> acc;
-#pragma unroll
-    for (int y = 0; y < TH; ++y)
-#pragma unroll
-        for (int x = 0; x < TW; ++x) acc[y][x][0] = 0.0f;
-
-    // channels in order; the window NS-1 channels ahead is loaded before each
-    // compute; the slot's values and the channel's weights are copied to one
-    // set of registers so that the walk (most of the code) is inlined once
-    float cur[EPL];
-    tile::Wts<T> w;
-#pragma unroll 1
-    for (int i = 0; i < ncw; ++i) {
-        tile::static_for<0, NS>([&](auto sl) {
-            constexpr int B = decltype(sl)::value;
-            if (i % NS == B) {
-                if (i + NS - 1 < ncw) issue(std::integral_constant<int, (B + NS - 1) % NS>{}, i + NS - 1);
-#pragma unroll
-                for (int q = 0; q < EPL; ++q) cur[q] = xv[B][q];
-            }
-        });
-        unsigned long long mask[EPL];
-        bool any = false;
-#pragma unroll
-        for (int q = 0; q < EPL; ++q) {
-            mask[q] = __ballot(inwin[q] && (__float_as_uint(cur[q]) & 0x7fffffffu) != 0u);
-            any |= mask[q] != 0ull;
-        }
-        if (!any) continue;
-        tile::load_weights<T>(lds + static_cast<size_t>(phase + i * cs) * RS2 * kWPitch, lane, w, kWPitch);
-        tile::wait_lgkm0();
-        tile::walk_scan<T>(mask, cur, acc, w);
-    }
-
-    // step 3: the cs phase tiles of each row group are summed through LDS
-    // and stored to NCHW.  Every wavefront writes its tile [position][map]
-    // with a padded pitch (conflict-free); then each thread takes one output
-    // position of the workgroup and the maps k0, k0 + ostep, ..., so that
-    // consecutive threads store consecutive positions of one map, and sums
-    // the phases of each output in phase order.
-    constexpr int TP = TH * TW;
-    __syncthreads();  // every wavefront is done with its weights
-    float *red = lds;
-#pragma unroll
-    for (int y = 0; y < TH; ++y)
-#pragma unroll
-        for (int x = 0; x < TW; ++x) red[(wave * TP + y * TW + x) * kRPad + lane] = acc[y][x][0];
-    __syncthreads();
-    const int Wo = a.Wo;
-    const int oyb = band * a.rg * TH;             // first output row of the workgroup
-    const int rows = min(a.rg * TH, a.Ho - oyb);  // its output rows
-    const int npos = rows * Wo;                   // <= kWaves * kMaxTile = 512
-    const int ostep = (kWaves * kLanes) / npos;
-    const int k0 = tid / npos;
-    const int pos = tid - k0 * npos;
-    if (k0 >= ostep) return;
-    const int oyl = pos / Wo;
-    const int ox = pos - oyl * Wo;
-    const int g = oyl / TH;
-    const size_t plane_out = static_cast<size_t>(a.Ho) * Wo;
-    const float *src = red + ((g * cs) * TP + (oyl - g * TH) * TW + ox) * kRPad;
-    float *dst = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oyb) * Wo + pos;
-    // phase p's partial at src + p * TP * kRPad; phases past cs read the last
-    // one again (in bounds, no branches) and are not added
-    int poff[kWaves];
-#pragma unroll
-    for (int p = 0; p < kWaves; ++p) poff[p] = min(p, cs - 1) * TP * kRPad;
-    for (int k = k0; k < a.K; k += ostep) {
-        float part[kWaves];
-#pragma unroll
-        for (int p = 0; p < kWaves; ++p) part[p] = src[poff[p] + k];
-        float sum = part[0];
-#pragma unroll
-        for (int p = 1; p < kWaves; ++p) sum += p < cs ? part[p] : 0.0f;
-        dst[static_cast<size_t>(k) * plane_out] = sum;
-    }
-}
-
-struct FusedPlan {
-    int th, tw, cs;
-    size_t lds;
-};
 
 int fused_tw(int Wo) { return Wo <= 8 ? 8 : (Wo <= 16 ? 16 : 28); }
 
@@ -249,57 +54,24 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     return found;
 }
 
-template <int RS_, int TH, int TW>
-hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
-    if constexpr (TH * TW > kMaxTile) {
-        return hipErrorInvalidValue;
-    } else {
-        auto kern = sparse_conv_fused_kernel<RS_, TH, TW>;
-        if (lds > 64 * 1024) {
-            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-            if (e != hipSuccess) return e;
-        }
-        kern<<<a.N * a.bands, kWaves * kLanes, lds, s>>>(a);
-        return hipGetLastError();
-    }
-}
-
-template <int RS_, int TW>
-hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s) {
-    switch (th) {
-    case 8: return launch_fused_t<RS_, 8, TW>(a, lds, s);
-    case 4: return launch_fused_t<RS_, 4, TW>(a, lds, s);
-    case 2: return launch_fused_t<RS_, 2, TW>(a, lds, s);
-    default: return launch_fused_t<RS_, 1, TW>(a, lds, s);
-    }
-}
-
-template <int RS_>
-hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
-    switch (p.tw) {
-    case 8: return launch_fused_th<RS_, 8>(a, p.th, p.lds, s);
-    case 16: return launch_fused_th<RS_, 16>(a, p.th, p.lds, s);
-    default: return launch_fused_th<RS_, 28>(a, p.th, p.lds, s);
-    }
-}
-
 }  // namespace
+}  // namespace fused
 
 bool sparse_fused_applies(const SparseShape &sh) {
-    FusedPlan p;
-    return fused_plan(sh, &p) || sparse_fring_applies(sh);
+    fused::FusedPlan p;
+    return fused::fused_plan(sh, &p) || sparse_fring_applies(sh);
 }
 
 int sparse_fused_kernel(const SparseShape &sh) {
-    FusedPlan p;
-    return fused_plan(sh, &p) ? 1 : (sparse_fring_applies(sh) ? 5 : 0);
+    fused::FusedPlan p;
+    return fused::fused_plan(sh, &p) ? 1 : (sparse_fring_applies(sh) ? 5 : 0);
 }
 
 // The filter-resident kernel when the filter fits in LDS, else the
 // filter-ring kernel.
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s) {
+    using namespace fused;
     FusedPlan p;
     if (!fused_plan(sh, &p)) return launch_sparse_fring(sh, x, wt, y, dec, s);
     FusedArgs a{};
@@ -312,9 +84,9 @@ hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const floa
     a.bands = (sh.Ho + a.rg * p.th - 1) / (a.rg * p.th);
     a.dec = dec;
     switch (sh.R) {
-    case 1: return launch_fused_rs<1>(a, p, s);
-    case 3: return launch_fused_rs<3>(a, p, s);
-    default: return launch_fused_rs<5>(a, p, s);
+    case 1: return launch_r1(a, p, s);
+    case 3: return launch_r3(a, p, s);
+    default: return launch_r5(a, p, s);
     }
 }
 
