@@ -18,6 +18,9 @@ What each function follows (Shi & Chu, arXiv 1704.07724):
                                Sec. "Sparse Convolution", border-exact)
   im2col                       the unrolled input matrix M_I of the
                                matrix-multiplication formulation (Fig. 3)
+  relu_conv2d_f64              Eq. 1 followed by the rectifier of Eq. 2
+                               (Sec. "Sparsity of ReLUs"), with the nonzero
+                               count of the rectified output
 
 Pins (tests/test_oracle_pins.py) tie each function to something other than
 itself: brute-force loops, closed forms, numpy / torch library routines,
@@ -65,6 +68,8 @@ def load_library(path: str):
     lib.oracle_nz_macs.restype = i64
     lib.oracle_im2col.argtypes = [vp] + [i32] * 8 + [i64, vp]
     lib.oracle_im2col.restype = None
+    lib.oracle_rectify_f64.argtypes = [vp, i64]
+    lib.oracle_rectify_f64.restype = i64
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = i32
     lib.oracle_set_threads.argtypes = [i32]
@@ -145,6 +150,14 @@ def conv2d_f64_at(x, w, stride: int, pad: int, flat_idx) -> np.ndarray:
         _load().oracle_conv2d_f64_at(_ptr(x), _ptr(w), N, C, H, W, K, R, S,
                                      stride, pad, _ptr(idx), idx.size, _ptr(out))
     return out
+
+
+def relu_conv2d_f64(x, w, stride: int = 1, pad: int = 0):
+    """Eq. 1 then the rectifier max(0, v) of Eq. 2, fp64; returns (y, nnz),
+    nnz the number of nonzero entries of y (the next layer's nonzero count)."""
+    y = conv2d_f64(x, w, stride, pad)
+    nnz = int(_load().oracle_rectify_f64(_ptr(y), y.size)) if y.size else 0
+    return y, nnz
 
 
 def compact(x):

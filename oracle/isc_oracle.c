@@ -231,3 +231,19 @@ void oracle_im2col(const float *x, int N, int C, int H, int W, int R, int S,
                         }
             }
 }
+
+/* The rectifier of Eq. 2 (Sec. "Sparsity of ReLUs"), f(v) = max(0, v),
+ * applied in place to n entries of an fp64 convolution output; returns how
+ * many entries are nonzero afterwards -- the nonzero count of the next
+ * layer's input, from which its sparsity 1 - rho follows. */
+int64_t oracle_rectify_f64(double *y, int64_t n)
+{
+    int64_t nnz = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (y[i] > 0.0)
+            ++nnz;
+        else
+            y[i] = 0.0;
+    }
+    return nnz;
+}

@@ -35,6 +35,8 @@ MUTANTS = {
     "row_ptr_after_row": ("            row_ptr[p * (H + 1) + y] = cnt;\n            for (long xx",
                           "            for (long xx"),
     "macs_bound_inclusive": ("if (num / t < out) ++cnt;", "if (num / t <= out) ++cnt;"),
+    "relu_keeps_negatives": ("        if (y[i] > 0.0)\n            ++nnz;", "        if (y[i] < 0.0)\n            ++nnz;"),
+    "relu_counts_zeros": ("        if (y[i] > 0.0)\n            ++nnz;", "        if (y[i] >= 0.0)\n            ++nnz;"),
     "im2col_rs_swapped": ("long y = i * T + r - P, xx = j * T + s - P;",
                           "long y = i * T + s - P, xx = j * T + r - P;"),
 }

@@ -12,7 +12,10 @@
 - compaction against numpy's flatnonzero; the nonzero-MAC count against a
   brute-force enumeration and against the dense count for all-nonzero input;
 - im2col against a numpy sliding-window construction and the GEMM identity
-  of Fig. 3 (M_K x M_I = M_O).
+  of Fig. 3 (M_K x M_I = M_O);
+- the rectifier of Eq. 2 against torch.relu, the exact split
+  relu(o) - relu(-o) = o, and the identity / all-zero closed forms; its
+  nonzero count against numpy's count of positive outputs.
 """
 import itertools
 
@@ -321,3 +324,50 @@ def test_integer_inputs_are_exact_in_fp32_order_free():
     assert np.array_equal(out, np.round(out))
     assert np.max(np.abs(out)) < 2 ** 24
     assert np.array_equal(out.astype(np.float32).astype(np.float64), out)
+
+
+# ------------------------------------------- rectifier (Eq. 2) and counts ---
+
+def test_relu_conv_against_torch_float64():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(4100)
+    for T, P in [(1, 0), (1, 1), (2, 2)]:
+        x, w = rand_case(rng, 2, 5, 11, 9, 6, 3, 3, sparsity=0.6)
+        y, nnz = oracle.relu_conv2d_f64(x, w, T, P)
+        want = torch.relu(torch.nn.functional.conv2d(torch.from_numpy(x).double(),
+                                                     torch.from_numpy(w).double(),
+                                                     stride=T, padding=P)).numpy()
+        np.testing.assert_allclose(y, want, rtol=1e-12, atol=1e-12)
+        assert nnz == int(np.count_nonzero(want))
+
+
+def test_relu_splits_the_convolution_exactly():
+    # conv(-x) = -conv(x) exactly in fp64, so relu(o) - relu(-o) = o: the
+    # rectifier keeps the positive part and nothing else; the rectified
+    # output is non-negative, equals o or 0 everywhere, and its count is the
+    # number of positive outputs
+    rng = np.random.default_rng(4101)
+    x, w = rand_case(rng, 2, 4, 9, 8, 5, 3, 3, sparsity=0.5)
+    x[:, :, :3, :] = 0.0  # exact zero outputs along the top rows
+    o = oracle.conv2d_f64(x, w, 1, 1)
+    pos, n_pos = oracle.relu_conv2d_f64(x, w, 1, 1)
+    neg, n_neg = oracle.relu_conv2d_f64(-x, w, 1, 1)
+    assert np.array_equal(pos - neg, o)
+    assert np.all(pos >= 0.0) and np.all((pos == o) | (pos == 0.0))
+    assert np.any(o == 0.0)
+    assert n_pos == int(np.count_nonzero(o > 0.0)) == int(np.count_nonzero(pos))
+    assert n_neg == int(np.count_nonzero(o < 0.0))
+    assert n_pos + n_neg + int(np.count_nonzero(o == 0.0)) == o.size
+
+
+def test_relu_closed_forms():
+    # non-negative input and filter: the rectifier is the identity; a
+    # non-positive filter: every output is rectified to zero
+    rng = np.random.default_rng(4102)
+    x, w = rand_case(rng, 1, 3, 7, 7, 4, 3, 3, sparsity=0.3)
+    w = np.abs(w)
+    y, nnz = oracle.relu_conv2d_f64(x, w, 1, 1)
+    assert np.array_equal(y, oracle.conv2d_f64(x, w, 1, 1))
+    assert nnz == int(np.count_nonzero(y))
+    y2, nnz2 = oracle.relu_conv2d_f64(x, -w, 1, 1)
+    assert nnz2 == 0 and np.all(y2 == 0.0)

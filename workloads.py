@@ -19,6 +19,14 @@ Recipe (numpy PCG64 via default_rng):
            box-blurred N(0,1) field per (n, c) plane thresholded so that
            exactly ceil(sparsity * numel) entries are zero
   values   |N(0,1)|; a draw that rounds to 0 in fp32 is redrawn
+
+Layer chain (conv3 -> ReLU -> conv4 -> ReLU -> conv5 of AlexNet, no pooling
+between them): only the first layer's input is drawn; each later layer's
+input is the rectified output of the one before.  Eq. 1 has no bias, so the
+sparsity of a rectified output is set by the filters' mean instead: weights
+~ N(mean, 0.01) with mean = -0.208, -0.187, -0.189 times sigma for conv3,
+conv4, conv5, which leaves about 0.95 of each rectified output zero on the
+drawn input (the sparsity the paper reports for those layers, Tab. 2).
 """
 from __future__ import annotations
 
@@ -46,6 +54,7 @@ class Layer:
     sparsity: float
     sigma: float
     clustered: bool = False
+    w_mean: float = 0.0      # mean of the weights (0 except in the layer chain)
     config: int = 0
     layer: int = 0
     sweep_index: int = 0
@@ -97,6 +106,15 @@ WORKLOADS = {
         Layer("alexnet_conv4", 128, 384, 13, 13, 384, 3, 3, 1, 1, 0.95, 0.01, config=4, layer=1),
         Layer("alexnet_conv5", 128, 384, 13, 13, 256, 3, 3, 1, 1, 0.95, 0.01, config=4, layer=2),
     )),
+    # conv3 -> ReLU -> conv4 -> ReLU -> conv5: only conv3's input is drawn
+    "alexnet_chain345": Workload("alexnet_chain345", (
+        Layer("chain_conv3", 128, 256, 13, 13, 384, 3, 3, 1, 1, 0.95, 0.01, w_mean=-0.208 * 0.01,
+              config=6, layer=0),
+        Layer("chain_conv4", 128, 384, 13, 13, 384, 3, 3, 1, 1, 0.95, 0.01, w_mean=-0.187 * 0.01,
+              config=6, layer=1),
+        Layer("chain_conv5", 128, 384, 13, 13, 256, 3, 3, 1, 1, 0.95, 0.01, w_mean=-0.189 * 0.01,
+              config=6, layer=2),
+    )),
     # GoogLeNet inception-shaped, 28x28: 3x3 branch and 5x5 branch, clustered zeros
     "inception_28": Workload("inception_28", (
         Layer("inception_3x3", 128, 96, 28, 28, 128, 3, 3, 1, 1, 0.9, 0.01, True, config=5, layer=0),
@@ -142,7 +160,7 @@ def _clustered_mask(rng, shape, sparsity) -> np.ndarray:
 def make_inputs(layer: Layer, seed: int | None = None):
     """(x, w) as float32 numpy arrays for one layer, from its own seed."""
     rng = np.random.default_rng(layer.seed if seed is None else seed)
-    w = rng.normal(0.0, layer.sigma, size=layer.w_shape).astype(np.float32)
+    w = rng.normal(layer.w_mean, layer.sigma, size=layer.w_shape).astype(np.float32)
     if layer.clustered:
         mask = _clustered_mask(rng, layer.x_shape, layer.sparsity)
     else:
@@ -175,3 +193,17 @@ def integer_case(N, C, H, W, K, R, S, seed, sparsity=0.8, xmax=7, wmax=4):
     vals = rng.integers(1, xmax + 1, size=(N, C, H, W)).astype(np.float32)
     x = np.where(mask, np.float32(0.0), vals).astype(np.float32)
     return x, w
+
+
+def make_chain(workload: Workload, N: int | None = None):
+    """(x0, [w per layer]) of a layer chain: the first layer's input and
+    every layer's weights, each layer's weights from its own seed (the first
+    layer's input follows its weights, as in make_inputs).  N overrides the
+    batch of the drawn input."""
+    first = workload.layers[0] if N is None else workload.layers[0].with_(N=N)
+    x0, w0 = make_inputs(first)
+    ws = [w0]
+    for layer in workload.layers[1:]:
+        rng = np.random.default_rng(layer.seed)
+        ws.append(rng.normal(layer.w_mean, layer.sigma, size=layer.w_shape).astype(np.float32))
+    return x0, ws
