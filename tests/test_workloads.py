@@ -49,7 +49,7 @@ def test_clustered_exact_zero_count():
 def test_workload_shapes():
     names = set(workloads.WORKLOADS)
     assert names == {"lenet_conv2_tiny", "lenet_conv2_batch", "alexnet_conv2",
-                     "alexnet_conv345", "inception_28"}
+                     "alexnet_conv345", "inception_28", "alexnet_chain345"}
     sweep = workloads.WORKLOADS["lenet_conv2_batch"].layers
     assert [l.sparsity for l in sweep] == [0.5, 0.7, 0.9, 0.95, 0.99]
     assert len({l.seed for l in sweep}) == 5
@@ -59,3 +59,20 @@ def test_integer_case_bounds():
     x, w = workloads.integer_case(2, 3, 5, 5, 2, 3, 3, seed=4)
     assert set(np.unique(x)).issubset(set(range(0, 8)))
     assert set(np.unique(w)).issubset(set(range(-4, 5)))
+
+
+def test_chain_weights_and_input():
+    chain = workloads.WORKLOADS["alexnet_chain345"]
+    x0, ws = workloads.make_chain(chain, N=2)
+    assert x0.shape == (2, 256, 13, 13)
+    assert [w.shape for w in ws] == [l.w_shape for l in chain.layers]
+    # each layer's input channels are the previous layer's output maps
+    for a, b in zip(chain.layers, chain.layers[1:]):
+        assert b.C == a.K and (b.H, b.W) == (a.H, a.W)
+    for w, l in zip(ws, chain.layers):
+        assert abs(float(w.mean()) - l.w_mean) < 0.1 * l.sigma
+        assert abs(float(w.std()) - l.sigma) < 0.05 * l.sigma
+    assert abs((x0 == 0).mean() - 0.95) < 0.01
+    # weights drawn again from the same seeds are the same
+    _, ws2 = workloads.make_chain(chain, N=1)
+    assert all(np.array_equal(a, b) for a, b in zip(ws, ws2))
