@@ -127,6 +127,58 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
 int isc_decision(const isc_conv_desc *d, const void *ws, size_t ws_bytes,
                  uint64_t *nnz_total, int32_t *path_taken, void *stream);
 
+/* ---- Layer chains: the rectifier of Eq. 2 in the convolution's epilogue ----
+ *
+ * In a network the input of a convolution is the rectified output of the
+ * layer before (Eq. 2, Sec. "Sparsity of ReLUs"), and its sparsity is what
+ * the dispatcher needs.  isc_conv2d_relu applies the rectifier where y is
+ * written and counts the nonzeros of the rectified y in the same pass, into
+ * a census: one count per workgroup of the kernel that wrote y, behind a
+ * header that names the entries they cover (layout private to the library;
+ * no counter to clear, no atomics).  Given to the next layer as x_census,
+ * it replaces that layer's count of its input, so a chain of layers reads
+ * every activation once and writes it once, with no separate ReLU pass. */
+
+/* Bytes of the census of the output of a convolution with descriptor d
+ * (the layer that writes it).  Host-only.  Errors: NULL, SHAPE, LIMIT. */
+int isc_census_size(const isc_conv_desc *d, size_t *bytes);
+
+/* y = max(0, conv(x, w)): the convolution of isc_conv2d, then the rectifier
+ * of Eq. 2 on every entry (v > 0 ? v : +0, so -0 and NaN give +0), with the
+ * nonzero count of y written to y_census.
+ *   x, w, y, ws, ws_bytes, path, threshold, stream: as for isc_conv2d (the
+ *     workspace size is isc_workspace_size's).
+ *   x_census, x_census_bytes: the census an isc_conv2d_relu call wrote for
+ *     x (16-byte aligned), or NULL.  AUTO then decides from it instead of
+ *     counting x.  A census that does not cover exactly N*C*H*W entries
+ *     (never written, or written for another shape) leaves the count
+ *     unknown and AUTO runs the dense path: y is right either way.  Shapes
+ *     whose sparse path runs over compacted lists (isc_sparse_kernel not
+ *     FUSED or FUSED_RING) count x while listing it and ignore x_census.
+ *   wt: the repacked filter of isc_repack_filter for K, C, R, S of d
+ *     (16-byte aligned), or NULL to repack w into the workspace on every
+ *     call.  Used by the on-the-fly sparse kernels.
+ *   y_census, y_census_bytes: at least isc_census_size(d) bytes, 16-byte
+ *     aligned, or NULL for no census.
+ * The filter-resident, filter-ring and GEMM kernels rectify and count as
+ * they store y; after a kernel over compacted lists, one more launch
+ * rectifies y in place and counts it.  y must not overlap x, w, wt, ws or a
+ * census; y_census must not overlap any other argument.
+ * Errors: as isc_conv2d; WORKSPACE also for a census smaller than needed;
+ * ALIGN for a misaligned census or wt. */
+int isc_conv2d_relu(const isc_conv_desc *d, const float *x, const void *x_census,
+                    size_t x_census_bytes, const float *w, const float *wt, float *y,
+                    void *y_census, size_t y_census_bytes, void *ws, size_t ws_bytes,
+                    int32_t path, float threshold, void *stream);
+
+/* After the call that wrote `census` has completed on `stream` (this call
+ * synchronises the stream): the number of entries the census covers and how
+ * many of them are nonzero.  bytes: the census buffer's size.  Errors:
+ * NULL, WORKSPACE (bytes below the header), ARG (the buffer holds no
+ * census), DEVICE, HIP. */
+int isc_census_read(const void *census, size_t bytes, uint64_t *elems, uint64_t *nnz,
+                    void *stream);
+
 /* ISC step 1 (Sec. "Sparse Convolution"): list the nonzero inputs of every
  * (n, c) plane with their row and column, in row-major order.
  *   row_ptr: device int32[N*C*(H+1)]; row_ptr[p*(H+1) + y] = nonzeros of

@@ -7,7 +7,10 @@ library (there is no fallback of any kind).
 
 The functions carry the C names:
     isc_out_shape, isc_workspace_size, isc_conv2d, isc_decision,
-    isc_compact, isc_im2col, isc_gemm_f32, isc_status_str, isc_version
+    isc_census_size, isc_conv2d_relu, isc_census_read,
+    isc_compact, isc_repacked_filter_size, isc_repack_filter,
+    isc_sparse_conv, isc_sparse_conv_fused, isc_sparse_kernel,
+    isc_im2col, isc_gemm_f32, isc_status_str, isc_version
 """
 from __future__ import annotations
 
@@ -29,6 +32,7 @@ STATUS = {
 EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
            "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
+           "isc_census_size", "isc_conv2d_relu", "isc_census_read",
            "isc_status_str", "isc_version")
 
 
@@ -73,7 +77,10 @@ def lib():
     L.isc_gemm_f32.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
     L.isc_sparse_conv_fused.argtypes = [dp, vp, vp, vp, vp]
     L.isc_sparse_kernel.argtypes = [dp, ctypes.POINTER(i32)]
-    for name in EXPORTS[:12]:
+    L.isc_census_size.argtypes = [dp, ctypes.POINTER(sz)]
+    L.isc_conv2d_relu.argtypes = [dp, vp, vp, sz, vp, vp, vp, vp, sz, vp, sz, i32, ctypes.c_float, vp]
+    L.isc_census_read.argtypes = [vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64), vp]
+    for name in EXPORTS[:-2]:
         getattr(L, name).restype = ctypes.c_int
     L.isc_status_str.argtypes = [ctypes.c_int]
     L.isc_status_str.restype = ctypes.c_char_p
@@ -193,6 +200,61 @@ def isc_decision(desc: ConvDesc, ws, stream=None):
                               ctypes.byref(nnz), ctypes.byref(path), _stream(stream)),
            "isc_decision")
     return nnz.value, PATH_NAMES.get(path.value, path.value)
+
+
+def isc_census_size(desc: ConvDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().isc_census_size(ctypes.byref(desc), ctypes.byref(n)), "isc_census_size")
+    return n.value
+
+
+def census(desc: ConvDesc, device=None):
+    """A device buffer for the census of the output of the layer `desc`
+    (isc_census_size bytes; torch's allocations are 256-byte aligned)."""
+    torch = _torch()
+    return torch.empty(isc_census_size(desc), dtype=torch.uint8, device=device or "cuda")
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def isc_conv2d_relu(x, w, stride=1, pad=0, path="auto", threshold=0.9, x_census=None, wt=None,
+                    y_census=None, out=None, ws=None, stream=None):
+    """y = max(0, conv(x, w)) (Eq. 1, then the rectifier of Eq. 2) with the
+    nonzero count of y written to ``y_census`` (a buffer from ``census``)
+    when given.  ``x_census``: the census of x from the call that wrote x
+    (AUTO then decides from it instead of counting x).  ``wt``: a
+    RepackedFilter of w (else w is repacked in the workspace).  Returns y."""
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    w = _dev_f32(w, "w")
+    desc = _desc_of(x.shape, w.shape, stride, pad)
+    ho, wo = isc_out_shape(desc)
+    if out is None:
+        out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
+    elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
+        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+    if ws is None:
+        ws = workspace(desc, path, x.device)
+    if wt is not None and (wt.K, wt.C, wt.R, wt.S) != tuple(int(v) for v in w.shape):
+        raise ValueError("repacked filter does not match w")
+    _check(lib().isc_conv2d_relu(
+        ctypes.byref(desc), x.data_ptr(),
+        None if x_census is None else x_census.data_ptr(), 0 if x_census is None else _nbytes(x_census),
+        w.data_ptr(), None if wt is None else wt.data.data_ptr(), out.data_ptr(),
+        None if y_census is None else y_census.data_ptr(), 0 if y_census is None else _nbytes(y_census),
+        ws.data_ptr(), _nbytes(ws), _path(path), float(threshold), _stream(stream)), "isc_conv2d_relu")
+    return out
+
+
+def isc_census_read(census_buf, stream=None):
+    """(entries covered, nonzero count) of a census; synchronises the stream."""
+    elems = ctypes.c_uint64()
+    nnz = ctypes.c_uint64()
+    _check(lib().isc_census_read(census_buf.data_ptr(), _nbytes(census_buf), ctypes.byref(elems),
+                                 ctypes.byref(nnz), _stream(stream)), "isc_census_read")
+    return elems.value, nnz.value
 
 
 NZ_TAIL = 256  # spare entries isc_sparse_conv may read past the last plane

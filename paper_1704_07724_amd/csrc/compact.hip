@@ -219,6 +219,25 @@ void count_parts_kernel(const float *__restrict__ x, int64_t total, uint32_t *__
     }
 }
 
+// The output epilogue as a pass of its own, for the kernels over compacted
+// lists (which store y without one): y rectified in place and its nonzeros
+// counted into the census; workgroup b takes one contiguous chunk.
+__global__ __launch_bounds__(kWaves * 64)
+void rectify_kernel(float *__restrict__ y, int64_t n, Epilogue epi, Decision dec) {
+    if (!decision_gate(dec, 1u)) return;
+    __shared__ uint32_t sums[kWaves];
+    const int64_t chunk = (n + gridDim.x - 1) / gridDim.x;
+    const int64_t beg = static_cast<int64_t>(blockIdx.x) * chunk;
+    const int64_t end = min(n, beg + chunk);
+    uint32_t cnt = 0;
+    for (int64_t e = beg + threadIdx.x; e < end; e += kWaves * 64) {
+        const float v = epilogue_value(y[e], epi.relu);
+        cnt += nonzero_bit(v);
+        y[e] = v;
+    }
+    if (epi.census) census_commit(epi, cnt, sums);
+}
+
 int compact_groups(int planes) {
     // one wavefront per plane, enough workgroups to cover 256 CUs many times
     return std::max(1, std::min((planes + kWaves - 1) / kWaves, 8192));
@@ -258,6 +277,14 @@ hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, in
     count_parts_kernel<<<groups + tiles, kWaves * 64, 0, s>>>(x, total, parts, groups, np, w, K, Kp, CRS, qtiles,
                                                               wt);
     *nparts = np;
+    return hipGetLastError();
+}
+
+hipError_t launch_rectify(float *y, int64_t n, const Epilogue &epi, const Decision &dec, hipStream_t s) {
+    const int64_t per = static_cast<int64_t>(kWaves) * 64 * 16;  // elements per workgroup, at least
+    const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kRectifyGroups, (n + per - 1) / per)));
+    if (epi.census && census_slots_for(groups) > epi.cap) return hipErrorInvalidValue;
+    rectify_kernel<<<groups, kWaves * 64, 0, s>>>(y, n, epi, dec);
     return hipGetLastError();
 }
 

@@ -80,6 +80,7 @@ struct GemmArgs {
     int64_t ldc;
     int conv_hw;  // > 0: scatter column n to NCHW with Ho*Wo = conv_hw
     Decision dec;
+    Epilogue epi;  // rectifier and census of c
     // implicit im2col: B[k][j] is gathered from the input x instead of read
     // from b (k = (c, r, s), j = (n, oy, ox))
     const float *x;
@@ -274,6 +275,7 @@ void gemm_f32_kernel(GemmArgs g) {
 
     // epilogue: accumulator register v of lane l holds row
     // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32 x 32 block
+    uint32_t cnt = 0;  // nonzero values stored (the census count)
 #pragma unroll
     for (int j = 0; j < WN; ++j) {
         const int nn = n0 + (wn * WN + j) * 32 + lrow;
@@ -294,9 +296,17 @@ void gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int m = m0 + (wm * WM + i) * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
-                if (m < M) g.c[col_off + static_cast<size_t>(m) * row_stride] = acc[i][j][v];
+                if (m < M) {
+                    const float o = epilogue_value(acc[i][j][v], g.epi.relu);
+                    cnt += nonzero_bit(o);
+                    g.c[col_off + static_cast<size_t>(m) * row_stride] = o;
+                }
             }
         }
+    }
+    if (g.epi.census) {
+        __shared__ uint32_t sums[4];
+        census_commit(g.epi, cnt, sums);
     }
 }
 
@@ -305,6 +315,8 @@ hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, bool impl
     constexpr int BM = WAVES_M * WM * 32;
     constexpr int BN = (4 / WAVES_M) * WN * 32;
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
+    if (g.epi.census && census_slots_for(static_cast<int64_t>(grid.x) * grid.y) > g.epi.cap)
+        return hipErrorInvalidValue;
     if (implicit) {
         if (a_vec) gemm_f32_kernel<WAVES_M, WM, WN, true, false, true, BK><<<grid, 256, 0, s>>>(g);
         else gemm_f32_kernel<WAVES_M, WM, WN, false, false, true, BK><<<grid, 256, 0, s>>>(g);
@@ -350,20 +362,29 @@ hipError_t launch_im2col(const float *x, int N, int C, int H, int W, int R, int 
 
 hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda, const float *b,
                            int64_t ldb, float *c, int64_t ldc, int conv_hw, bool b_padded,
-                           const Decision &dec, hipStream_t s) {
+                           const Decision &dec, hipStream_t s, const Epilogue &epi) {
     GemmArgs g{};
     g.M = M; g.N = Ncols; g.Kd = Kd; g.a = a; g.lda = lda; g.b = b; g.ldb = ldb; g.c = c; g.ldc = ldc;
-    g.conv_hw = conv_hw; g.dec = dec;
+    g.conv_hw = conv_hw; g.dec = dec; g.epi = epi;
     const bool a_vec = (lda % 4 == 0) && (reinterpret_cast<uintptr_t>(a) % 16 == 0);
     const bool b_vec = b_padded && (ldb % 4 == 0) && (reinterpret_cast<uintptr_t>(b) % 16 == 0);
     return launch_gemm_any(g, a_vec, b_vec, false, s);
 }
 
+int64_t gemm_max_groups(int64_t M, int64_t Ncols) {
+    // the smallest tiles launch_gemm_any picks are 32 rows x 128 columns
+    // (M <= 32) and 64 x 64 (M <= 64); the widest grid of any tile is at most
+    // ceil(M / 32) * ceil(Ncols / 64)
+    return (M + 31) / 32 * ((Ncols + 63) / 64);
+}
+
 bool conv_gemm_implicit_ok(int C, int R, int S) { return static_cast<int64_t>(C) * R * S < (1 << 16); }
 
 hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
-                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s) {
+                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s,
+                            const Epilogue &epi) {
     GemmArgs g{};
+    g.epi = epi;
     g.M = K;
     g.N = N * Ho * Wo;
     g.Kd = C * R * S;

@@ -7,7 +7,9 @@
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <algorithm>
 #include <limits>
+#include <vector>
 
 namespace isc {
 bool sparse_conv_feasible(const SparseShape &sh);
@@ -151,6 +153,149 @@ unsigned long long nnz_limit_for(int64_t total, float threshold) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? ISC_OK : ISC_ERR_HIP; }
 
+// What isc_conv2d_relu adds to isc_conv2d: the epilogue (rectifier and
+// census of y), the census of x, and a caller's repacked filter.
+struct Chain {
+    const isc::CensusHeader *x_census = nullptr;
+    uint32_t x_cap = 0;
+    size_t x_census_bytes = 0;
+    size_t y_census_bytes = 0;
+    const float *wt = nullptr;
+    isc::Epilogue epi{};
+};
+
+uint32_t census_cap(size_t bytes) {
+    const size_t n = (bytes - sizeof(isc::CensusHeader)) / sizeof(uint32_t);
+    return static_cast<uint32_t>(std::min<size_t>(n, std::numeric_limits<uint32_t>::max()) / 4 * 4);
+}
+
+// A census has room for the workgroups of every kernel that may write the
+// output: the on-the-fly sparse kernels, the stand-alone epilogue pass
+// after the list kernels, and the GEMM.
+size_t census_bytes(const Shape &s) {
+    const int64_t groups = std::max<int64_t>({isc::sparse_fused_max_groups(sparse_shape(s)),
+                                              static_cast<int64_t>(isc::kRectifyGroups),
+                                              isc::gemm_max_groups(s.K, s.ncols())});
+    return sizeof(isc::CensusHeader) + sizeof(uint32_t) * isc::census_slots_for(groups);
+}
+
+int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws, size_t ws_bytes,
+              int32_t path, float threshold, void *stream, const Chain *ch) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !w || !y || !ws) return ISC_ERR_NULL;
+    if (!valid_path(path)) return ISC_ERR_PATH;
+    if (!(threshold >= 0.0f && threshold <= 1.0f)) return ISC_ERR_ARG;
+    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
+    const Layout L = layout_for(s, path);
+    if (ws_bytes < L.total) return ISC_ERR_WORKSPACE;
+    const size_t xbytes = sizeof(float) * static_cast<size_t>(s.in_elems());
+    const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
+    const size_t wbytes = sizeof(float) * static_cast<size_t>(s.filt_elems());
+    if (overlap(y, ybytes, x, xbytes) || overlap(y, ybytes, w, wbytes) || overlap(y, ybytes, ws, L.total))
+        return ISC_ERR_ALIAS;
+    const isc::Epilogue epi = ch ? ch->epi : isc::Epilogue{};
+    if (ch) {
+        const size_t tbytes = sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
+                                                                         static_cast<int>(s.R), static_cast<int>(s.S));
+        const void *yc = epi.census;
+        const size_t ycb = ch->y_census_bytes;
+        if (ch->wt && (overlap(y, ybytes, ch->wt, tbytes) || overlap(ch->wt, tbytes, ws, L.total)))
+            return ISC_ERR_ALIAS;
+        if (ch->x_census && overlap(y, ybytes, ch->x_census, ch->x_census_bytes)) return ISC_ERR_ALIAS;
+        if (yc && (overlap(yc, ycb, x, xbytes) || overlap(yc, ycb, y, ybytes) || overlap(yc, ycb, w, wbytes) ||
+                   overlap(yc, ycb, ws, L.total) || (ch->wt && overlap(yc, ycb, ch->wt, tbytes)) ||
+                   (ch->x_census && overlap(yc, ycb, ch->x_census, ch->x_census_bytes))))
+            return ISC_ERR_ALIAS;
+    }
+
+    const isc::SparseShape sh = sparse_shape(s);
+    const bool sparse_fits = L.fused || isc::sparse_conv_feasible(sh);
+    if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
+    if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
+
+    st = check_device();
+    if (st) return st;
+
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    char *base = static_cast<char *>(ws);
+    Ctrl *ctrl = reinterpret_cast<Ctrl *>(base);
+    hipError_t e = hipSuccess;
+    uint32_t *parts = L.sparse ? reinterpret_cast<uint32_t *>(base + L.parts) : nullptr;
+    int nparts = 0;
+    const unsigned long long limit = nnz_limit_for(s.in_elems(), threshold);
+    const int gate_sparse = path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways;
+
+    if (path != ISC_PATH_DENSE) {
+        // steps 2-3 are gated by the device-side decision in AUTO and record
+        // the count and the path taken
+        float *wt_ws = reinterpret_cast<float *>(base + L.wt);
+        if (L.fused) {
+            const float *wt = ch && ch->wt ? ch->wt : wt_ws;
+            isc::Decision dec{parts, 0, limit, gate_sparse, ctrl};
+            if (ch && ch->x_census) {
+                // the count comes from the census of x: no pass over x
+                if (!ch->wt && (e = isc::launch_repack_filter(w, sh.K, sh.C, sh.R, sh.S, wt_ws, hs)) != hipSuccess)
+                    return hip_status(e);
+                dec.parts = nullptr;
+                dec.census = ch->x_census;
+                dec.census_cap = ch->x_cap;
+                dec.census_elems = static_cast<unsigned long long>(s.in_elems());
+            } else {
+                // the count for the decision and the filter repack to
+                // K-contiguous in one launch, then steps 1-3 in one launch
+                const bool repack = !(ch && ch->wt);
+                if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs, repack ? w : nullptr, sh.K,
+                                                 sh.C, sh.R, sh.S, repack ? wt_ws : nullptr)) != hipSuccess)
+                    return hip_status(e);
+                dec.nparts = nparts;
+            }
+            if ((e = isc::launch_sparse_fused(sh, x, wt, y, dec, hs, epi)) != hipSuccess) return hip_status(e);
+        } else {
+            int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
+            NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
+            // step 1 and the filter repack to K-contiguous, one launch
+            if ((e = isc::launch_prep(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz, parts, &nparts, w,
+                                      sh.K, sh.C, sh.R, sh.S, wt_ws, hs)) != hipSuccess)
+                return hip_status(e);
+            isc::Decision dec{parts, nparts, limit, gate_sparse, ctrl};
+            if ((e = isc::launch_sparse_conv(sh, row_ptr, nz, wt_ws, y, dec, hs)) != hipSuccess)
+                return hip_status(e);
+            if (epi.relu || epi.census) {
+                // the list kernels store y without the epilogue: a pass of its
+                // own, run iff the sparse path was taken
+                isc::Decision after{nullptr, 0, limit, isc::kGateIfSparse, nullptr, ctrl};
+                if ((e = isc::launch_rectify(y, s.out_elems(), epi, after, hs)) != hipSuccess)
+                    return hip_status(e);
+            }
+        }
+    }
+    if (path != ISC_PATH_SPARSE) {
+        // AUTO: run iff the sparse kernel, launched before on this stream,
+        // recorded the dense path; DENSE alone: no count, recorded as such
+        isc::Decision dec{nullptr, 0, limit, path == ISC_PATH_AUTO ? isc::kGateIfDense : isc::kGateAlways,
+                          path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
+        if (L.implicit) {
+            // one launch: the GEMM gathers the im2col matrix from x
+            if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
+                                           sh.Wo, dec, hs, epi)) != hipSuccess)
+                return hip_status(e);
+        } else {
+            float *col = reinterpret_cast<float *>(base + L.col);
+            if ((e = isc::launch_im2col(x, sh.N, sh.C, sh.H, sh.W, sh.R, sh.S, sh.T, sh.P, sh.Ho, sh.Wo, col,
+                                        s.ldcol(), dec, hs)) != hipSuccess)
+                return hip_status(e);
+            dec.record = nullptr;
+            if ((e = isc::launch_gemm_f32(sh.K, static_cast<int>(s.ncols()), static_cast<int>(s.crs()), w,
+                                          s.crs(), col, s.ldcol(), y, 0, sh.Ho * sh.Wo, true, dec, hs, epi)) !=
+                hipSuccess)
+                return hip_status(e);
+        }
+    }
+    return ISC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -198,85 +343,68 @@ int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes) {
 
 int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
                size_t ws_bytes, int32_t path, float threshold, void *stream) {
+    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, nullptr);
+}
+
+int isc_census_size(const isc_conv_desc *d, size_t *bytes) {
+    if (!bytes) return ISC_ERR_NULL;
     Shape s;
-    int st = check_desc(d, &s);
+    const int st = check_desc(d, &s);
     if (st) return st;
-    if (!x || !w || !y || !ws) return ISC_ERR_NULL;
-    if (!valid_path(path)) return ISC_ERR_PATH;
-    if (!(threshold >= 0.0f && threshold <= 1.0f)) return ISC_ERR_ARG;
-    if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
-    const Layout L = layout_for(s, path);
-    if (ws_bytes < L.total) return ISC_ERR_WORKSPACE;
-    const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
-    if (overlap(y, ybytes, x, sizeof(float) * static_cast<size_t>(s.in_elems())) ||
-        overlap(y, ybytes, w, sizeof(float) * static_cast<size_t>(s.filt_elems())) ||
-        overlap(y, ybytes, ws, L.total))
-        return ISC_ERR_ALIAS;
+    *bytes = census_bytes(s);
+    return ISC_OK;
+}
 
-    const isc::SparseShape sh = sparse_shape(s);
-    const bool sparse_fits = L.fused || isc::sparse_conv_feasible(sh);
-    if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
-    if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
-
-    st = check_device();
+int isc_conv2d_relu(const isc_conv_desc *d, const float *x, const void *x_census, size_t x_census_bytes,
+                    const float *w, const float *wt, float *y, void *y_census, size_t y_census_bytes, void *ws,
+                    size_t ws_bytes, int32_t path, float threshold, void *stream) {
+    Shape s;
+    const int st = check_desc(d, &s);
     if (st) return st;
+    Chain ch;
+    ch.wt = wt;
+    ch.epi.relu = 1;
+    ch.epi.elems = static_cast<unsigned long long>(s.out_elems());
+    if (x_census) {
+        if (!aligned(x_census, 16)) return ISC_ERR_ALIGN;
+        if (x_census_bytes < sizeof(isc::CensusHeader)) return ISC_ERR_WORKSPACE;
+        ch.x_census = static_cast<const isc::CensusHeader *>(x_census);
+        ch.x_cap = census_cap(x_census_bytes);
+        ch.x_census_bytes = x_census_bytes;
+    }
+    if (y_census) {
+        if (!aligned(y_census, 16)) return ISC_ERR_ALIGN;
+        if (y_census_bytes < census_bytes(s)) return ISC_ERR_WORKSPACE;
+        ch.epi.census = static_cast<isc::CensusHeader *>(y_census);
+        ch.epi.cap = census_cap(y_census_bytes);
+        ch.y_census_bytes = y_census_bytes;
+    }
+    if (wt && !aligned(wt, 16)) return ISC_ERR_ALIGN;
+    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, &ch);
+}
 
+int isc_census_read(const void *census, size_t bytes, uint64_t *elems, uint64_t *nnz, void *stream) {
+    if (!census || !elems || !nnz) return ISC_ERR_NULL;
+    if (bytes < sizeof(isc::CensusHeader)) return ISC_ERR_WORKSPACE;
+    const int st = check_device();
+    if (st) return st;
     hipStream_t hs = static_cast<hipStream_t>(stream);
-    char *base = static_cast<char *>(ws);
-    Ctrl *ctrl = reinterpret_cast<Ctrl *>(base);
-    hipError_t e = hipSuccess;
-    uint32_t *parts = L.sparse ? reinterpret_cast<uint32_t *>(base + L.parts) : nullptr;
-    int nparts = 0;
-    const unsigned long long limit = nnz_limit_for(s.in_elems(), threshold);
-
-    if (path != ISC_PATH_DENSE) {
-        // steps 2-3 are gated by the device-side decision in AUTO and record
-        // the count and the path taken
-        float *wt = reinterpret_cast<float *>(base + L.wt);
-        if (L.fused) {
-            // the count for the decision and the filter repack to
-            // K-contiguous in one launch, then steps 1-3 in one launch
-            if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs, w, sh.K, sh.C, sh.R, sh.S,
-                                             wt)) != hipSuccess)
-                return hip_status(e);
-            isc::Decision dec{parts, nparts, limit, path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways,
-                              ctrl};
-            if ((e = isc::launch_sparse_fused(sh, x, wt, y, dec, hs)) != hipSuccess) return hip_status(e);
-        } else {
-            int32_t *row_ptr = reinterpret_cast<int32_t *>(base + L.row_ptr);
-            NzEntry *nz = reinterpret_cast<NzEntry *>(base + L.nz);
-            // step 1 and the filter repack to K-contiguous, one launch
-            if ((e = isc::launch_prep(x, static_cast<int>(s.N * s.C), sh.H, sh.W, row_ptr, nz, parts, &nparts, w,
-                                      sh.K, sh.C, sh.R, sh.S, wt, hs)) != hipSuccess)
-                return hip_status(e);
-            isc::Decision dec{parts, nparts, limit, path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways,
-                              ctrl};
-            if ((e = isc::launch_sparse_conv(sh, row_ptr, nz, wt, y, dec, hs)) != hipSuccess)
-                return hip_status(e);
-        }
+    isc::CensusHeader h;
+    hipError_t e = hipMemcpyAsync(&h, census, sizeof(h), hipMemcpyDeviceToHost, hs);
+    if (e == hipSuccess) e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return ISC_ERR_HIP;
+    if (h.nslots % 4 != 0 || h.nslots > census_cap(bytes)) return ISC_ERR_ARG;  // not a census
+    std::vector<uint32_t> slots(h.nslots);
+    if (h.nslots) {
+        e = hipMemcpyAsync(slots.data(), static_cast<const isc::CensusHeader *>(census) + 1,
+                           sizeof(uint32_t) * h.nslots, hipMemcpyDeviceToHost, hs);
+        if (e == hipSuccess) e = hipStreamSynchronize(hs);
+        if (e != hipSuccess) return ISC_ERR_HIP;
     }
-    if (path != ISC_PATH_SPARSE) {
-        // AUTO: run iff the sparse kernel, launched before on this stream,
-        // recorded the dense path; DENSE alone: no count, recorded as such
-        isc::Decision dec{nullptr, 0, limit, path == ISC_PATH_AUTO ? isc::kGateIfDense : isc::kGateAlways,
-                          path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
-        if (L.implicit) {
-            // one launch: the GEMM gathers the im2col matrix from x
-            if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
-                                           sh.Wo, dec, hs)) != hipSuccess)
-                return hip_status(e);
-        } else {
-            float *col = reinterpret_cast<float *>(base + L.col);
-            if ((e = isc::launch_im2col(x, sh.N, sh.C, sh.H, sh.W, sh.R, sh.S, sh.T, sh.P, sh.Ho, sh.Wo, col,
-                                        s.ldcol(), dec, hs)) != hipSuccess)
-                return hip_status(e);
-            dec.record = nullptr;
-            if ((e = isc::launch_gemm_f32(sh.K, static_cast<int>(s.ncols()), static_cast<int>(s.crs()), w,
-                                          s.crs(), col, s.ldcol(), y, 0, sh.Ho * sh.Wo, true, dec, hs)) !=
-                hipSuccess)
-                return hip_status(e);
-        }
-    }
+    uint64_t total = 0;
+    for (uint32_t v : slots) total += v;
+    *elems = h.elems;
+    *nnz = total;
     return ISC_OK;
 }
 

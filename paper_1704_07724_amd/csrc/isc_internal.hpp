@@ -29,9 +29,29 @@ enum Gate : int { kGateAlways = 0, kGateIfSparse = 1, kGateIfDense = 2 };
 // (a multiple of 4; unused entries are zero).
 constexpr int kMaxParts = 1024;
 
+// Census of a layer's output: its nonzero count, kept as one count per
+// workgroup of the kernel that wrote the output (so no counter needs
+// clearing and no atomics are involved).  The next layer's decision sums the
+// counts instead of reading its input again.  Header, then the counts.
+struct alignas(16) CensusHeader {
+    unsigned long long elems;  // entries of the output the counts cover
+    uint32_t nslots;           // counts in use, a multiple of 4 (zero tail)
+    uint32_t reserved;
+};
+
+// Output epilogue of the kernels that write y: the rectifier of Eq. 2 and
+// the census of the rectified output.
+struct Epilogue {
+    int relu;                  // store max(0, v) (v > 0 ? v : +0, NaN -> +0)
+    CensusHeader *census;      // nullptr: no census
+    uint32_t cap;              // counts the census has room for
+    unsigned long long elems;  // entries of y
+};
+
 // Device-side decision: sparse iff the input's nonzero count, the sum of the
-// compaction's per-workgroup counts, is <= nnz_limit.  A kernel launched
-// after the one that recorded the decision reads the recorded path instead.
+// compaction's per-workgroup counts (or of a census of the input), is <=
+// nnz_limit.  A kernel launched after the one that recorded the decision
+// reads the recorded path instead.
 struct Decision {
     const uint32_t *parts;         // per-workgroup counts (nullptr: no compaction ran)
     int nparts;                    // entries of parts, a multiple of 4
@@ -39,14 +59,20 @@ struct Decision {
     int gate;
     Ctrl *record;                  // where block 0 records count and path (may be nullptr)
     const Ctrl *recorded = nullptr;  // decision recorded by an earlier kernel on the stream
+    // census of the input (used when parts is nullptr): counts must cover
+    // census_elems entries and fit in census_cap, else the count is unknown
+    // (all ones: the dense path)
+    const CensusHeader *census = nullptr;
+    uint32_t census_cap = 0;
+    unsigned long long census_elems = 0;
 };
 
-// Sum of the per-workgroup counts, by the calling wavefront (every lane gets
-// the total).
-__device__ __forceinline__ unsigned long long decision_total(const Decision &d) {
+// Sum of n counts (n a multiple of 4), by the calling wavefront (every lane
+// gets the total).
+__device__ __forceinline__ unsigned long long sum_counts(const uint32_t *counts, int n) {
     unsigned long long s = 0;
-    const uint4 *p = reinterpret_cast<const uint4 *>(d.parts);
-    for (int i = threadIdx.x & 63; i < d.nparts / 4; i += 64) {
+    const uint4 *p = reinterpret_cast<const uint4 *>(counts);
+    for (int i = threadIdx.x & 63; i < n / 4; i += 64) {
         const uint4 v = p[i];
         s += static_cast<unsigned long long>(v.x) + v.y + v.z + v.w;
     }
@@ -55,13 +81,25 @@ __device__ __forceinline__ unsigned long long decision_total(const Decision &d) 
     return s;
 }
 
+// The input's nonzero count for the decision, by the calling wavefront;
+// all ones when neither a compaction nor a usable census gives it.
+__device__ __forceinline__ unsigned long long decision_total(const Decision &d) {
+    if (d.parts) return sum_counts(d.parts, d.nparts);
+    if (d.census) {
+        const CensusHeader h = *d.census;
+        if (h.elems == d.census_elems && h.nslots <= d.census_cap && h.nslots % 4 == 0)
+            return sum_counts(reinterpret_cast<const uint32_t *>(d.census + 1), static_cast<int>(h.nslots));
+    }
+    return ~0ull;
+}
+
 // Gate of a kernel on path `mine` (1 sparse, 2 dense): whether it runs.
-// Block 0 records the count (all ones when no compaction ran) and the path
+// Block 0 records the count (all ones when no count is known) and the path
 // taken when asked.  Called by whole wavefronts.
 __device__ __forceinline__ bool decision_gate(const Decision &d, uint32_t mine) {
     if (d.recorded) return d.recorded->path_taken == mine;
-    const unsigned long long total = d.parts ? decision_total(d) : ~0ull;
-    const bool sparse = d.parts != nullptr && total <= d.nnz_limit;
+    const unsigned long long total = decision_total(d);
+    const bool sparse = total != ~0ull && total <= d.nnz_limit;
     const bool run = d.gate == kGateAlways || (d.gate == kGateIfSparse ? sparse : !sparse);
     if (d.record && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
         d.record->nnz_total = total;
@@ -69,6 +107,46 @@ __device__ __forceinline__ bool decision_gate(const Decision &d, uint32_t mine) 
     }
     return run;
 }
+
+// The stored value under the epilogue: the rectifier when asked.
+__device__ __forceinline__ float epilogue_value(float v, int relu) { return relu && !(v > 0.0f) ? 0.0f : v; }
+
+// 1 if the stored value is nonzero (the compaction's zero test: +0 and -0
+// are zero).
+__device__ __forceinline__ uint32_t nonzero_bit(float v) { return (__float_as_uint(v) & 0x7fffffffu) != 0u; }
+
+// The workgroup's census count: the sum of every thread's `cnt` into the
+// workgroup's slot; block 0 also writes the header and clears the tail
+// slots up to a multiple of 4.  Called by every thread of the workgroup
+// (uniformly: it synchronises); `sums` is LDS with one word per wavefront
+// that nothing else uses until the call returns.
+__device__ __forceinline__ void census_commit(const Epilogue &e, uint32_t cnt, uint32_t *sums) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) sums[wave] = cnt;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t t = 0;
+        for (int i = 0; i < static_cast<int>(blockDim.x >> 6); ++i) t += sums[i];
+        const uint32_t nblocks = gridDim.x * gridDim.y * gridDim.z;
+        const uint32_t b = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+        uint32_t *slots = reinterpret_cast<uint32_t *>(e.census + 1);
+        slots[b] = t;
+        if (b == 0) {
+            const uint32_t n4 = (nblocks + 3u) & ~3u;
+            for (uint32_t i = nblocks; i < n4; ++i) slots[i] = 0u;
+            CensusHeader h;
+            h.elems = e.elems;
+            h.nslots = n4;
+            h.reserved = 0u;
+            *e.census = h;
+        }
+    }
+}
+
+// Census slots a launch of `blocks` workgroups needs.
+inline uint32_t census_slots_for(int64_t blocks) { return static_cast<uint32_t>((blocks + 3) / 4 * 4); }
 
 // --- launchers (each returns hipGetLastError() of its launches) ------------
 
@@ -107,12 +185,15 @@ struct SparseShape {
 // filter-ring kernel (sparse_fring.hip) streams larger ones through LDS.
 bool sparse_fused_applies(const SparseShape &sh);
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
-                               hipStream_t s);
+                               hipStream_t s, const Epilogue &epi = Epilogue{});
 bool sparse_fring_applies(const SparseShape &sh);
 // 1 (filter-resident), 5 (filter-ring) or 0 (neither): isc_sparse_kernel's ids.
 int sparse_fused_kernel(const SparseShape &sh);
 hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
-                               hipStream_t s);
+                               hipStream_t s, const Epilogue &epi = Epilogue{});
+// Upper bound of the workgroups of the on-the-fly kernels' launch for a
+// shape (the census slots their epilogue may write).
+int64_t sparse_fused_max_groups(const SparseShape &sh);
 
 // Which kernel runs over compacted lists for a shape (the values are those
 // of isc_sparse_kernel in the C ABI).
@@ -136,13 +217,22 @@ hipError_t launch_im2col(const float *x, int N, int C, int H, int W, int R, int 
 hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda,
                            const float *b, int64_t ldb, float *c, int64_t ldc,
                            int conv_hw, bool b_padded, const Decision &dec,
-                           hipStream_t s);
+                           hipStream_t s, const Epilogue &epi = Epilogue{});
 
 // The dense baseline as one implicit GEMM: the fp32 MFMA GEMM of Fig. 3 with
 // the im2col matrix gathered from x while loading (C*R*S < 2^16), output
 // scattered to NCHW.
 bool conv_gemm_implicit_ok(int C, int R, int S);
 hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
-                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s);
+                            int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s,
+                            const Epilogue &epi = Epilogue{});
+// Upper bound of the GEMM's workgroups for an M x Ncols product (the census
+// slots its epilogue may write).
+int64_t gemm_max_groups(int64_t M, int64_t Ncols);
+
+// The epilogue as a pass of its own over y[0 .. n) (in place), for the
+// kernels that have none: at most kRectifyGroups workgroups.
+constexpr int kRectifyGroups = 1024;
+hipError_t launch_rectify(float *y, int64_t n, const Epilogue &epi, const Decision &dec, hipStream_t s);
 
 }  // namespace isc

@@ -14,14 +14,19 @@ int fring_tw(int Wo) { return Wo <= 16 ? 16 : 28; }
 
 // Among the tiles that fit the register budget, the one that wastes least
 // work -- lanes past K in the last map group times rows past Ho in the last
-// band -- then the larger K-contiguous block (longer straight-line blocks);
-// ISC_FRING_KPL / ISC_FRING_TH restrict the choice (for measurements).
+// band.  Ties go to 4 maps per lane (256 maps per workgroup), then to two
+// rows per wavefront (each weight read from LDS serves twice the outputs,
+// which counts at high sparsity, where a channel's weight reads cost more
+// than the few multiply-adds they feed), then to more maps per lane.  Tie
+// order measured on AlexNet conv2-5 and the inception 3x3 branch; ISC_FRING_KPL /
+// ISC_FRING_TH restrict the choice (for measurements).
 bool fring_choose(const SparseShape &sh, int tw, TileChoice *tc) {
     int kpl_fix = 0, th_fix = 0;
     if (const char *env = std::getenv("ISC_FRING_KPL")) kpl_fix = std::atoi(env);
     if (const char *env = std::getenv("ISC_FRING_TH")) th_fix = std::atoi(env);
     bool found = false;
     double best = 0.0;
+    int best_rank = 0;
     for (int kpl : {6, 4, 2, 1}) {
         if (kpl_fix && kpl != kpl_fix) continue;
         for (int th : {2, 1}) {
@@ -31,9 +36,11 @@ bool fring_choose(const SparseShape &sh, int tw, TileChoice *tc) {
             const double lanes = static_cast<double>((sh.K + kw - 1) / kw * kw) / sh.K;
             const double rws = static_cast<double>((sh.Ho + rows - 1) / rows * rows) / sh.Ho;
             const double waste = lanes * rws;
-            if (!found || waste < best * (1.0 - 1e-9)) {
+            const int rank = (kpl == 4 ? 100 : 0) + th * 10 + kpl;  // tie order
+            if (!found || waste < best * (1.0 - 1e-9) || (waste <= best * (1.0 + 1e-9) && rank > best_rank)) {
                 *tc = TileChoice{kpl, th};
                 best = waste;
+                best_rank = rank;
                 found = true;
             }
         }
@@ -51,7 +58,7 @@ bool sparse_fring_applies(const SparseShape &sh) {
 }
 
 hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
-                               hipStream_t s) {
+                               hipStream_t s, const Epilogue &epi) {
     using namespace fring;
     const int tw = fring_tw(sh.Wo);
     TileChoice tc;
@@ -68,6 +75,7 @@ hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const floa
     a.bands = (sh.Ho + kWaves * tc.th - 1) / (kWaves * tc.th);
     a.kgroups = (sh.K + kLanes * tc.kpl - 1) / (kLanes * tc.kpl);
     a.dec = dec;
+    a.epi = epi;
     switch (sh.R) {
     case 1: return launch_r1(a, tw, tc, s);
     case 3: return launch_r3(a, tw, tc, s);

@@ -11,11 +11,12 @@
 // rows of one image), TW columns and 64*KPL output maps in registers (tile
 // machinery in sparse_tile.hpp).  Input channels go in order through a ring
 // of NBUF stages: stage c holds channel c's R*S*64*KPL weights (from the
-// K-contiguous repacked filter, by direct global->LDS loads, no registers)
-// and, in each wavefront's registers, the channel's input window of that
-// wavefront -- (TH+R-1) rows x (TW+S-1) columns in leaf-key order, padding
-// read as zero.  Stages are issued NBUF-1 channels ahead; one barrier per
-// channel, after a wait for exactly the stage consumed.  Per channel a
+// K-contiguous repacked filter) and each wavefront's input window of the
+// channel -- (TH+R-1) rows x (TW+S-1) columns in leaf-key order, padding
+// read as zero -- all brought in by direct global->LDS loads.  No register
+// is the target of a load in flight, so the only waits are the kernel's own:
+// stages are issued NBUF-1 channels ahead and each channel waits for exactly
+// the stage it consumes, then one barrier.  Per channel a
 // wavefront reads the weights into registers, takes a ballot of the zero test
 // over its window and scans the window statically (walk_scan): every set
 // position runs the straight-line block of its (row, column).  Each lane
@@ -32,6 +33,7 @@ namespace fring {
 using tile::kLanes;
 constexpr int kWaves = 4;
 constexpr size_t kLdsMax = 160 * 1024;
+constexpr size_t kLdsPair = kLdsMax / 2;  // two workgroups per CU
 
 struct FringArgs {
     const float *x;   // N x C x H x W
@@ -43,6 +45,7 @@ struct FringArgs {
     int bands;        // groups of kWaves * TH output rows
     int kgroups;      // groups of 64 * KPL output maps
     Decision dec;
+    Epilogue epi;     // rectifier and census of y
 };
 
 // Register tiles instantiated: (KPL, TH) per filter size and tile width,
@@ -78,10 +81,18 @@ struct FringShape {
     static constexpr int CHF = RS2 * T::KW;                  // floats of one channel's weights
     static constexpr int NDW = (CHF + 255) / 256;            // 1 KB direct-to-LDS blocks
     static constexpr int SLOT4 = NDW * kLanes;               // float4 per ring slot
-    static constexpr int NBUF = SLOT4 * 16 <= 16384 ? 4 : (SLOT4 * 16 <= 32768 ? 3 : 2);
+    static constexpr size_t SLOTB = sizeof(float4) * SLOT4;  // bytes of one stage's weights
+    static constexpr int WIN4 = kWaves * T::EPL * kLanes / 4;             // float4 of its windows
+    static constexpr size_t WINB = sizeof(float4) * WIN4;
+    // stages: up to 4 for slots of <= 16 KB, 3 for <= 32 KB, else 2, and no
+    // more than leave room for two workgroups per CU
+    static constexpr int NPREF = SLOTB <= 16384 ? 4 : (SLOTB <= 32768 ? 3 : 2);
+    static constexpr int NBUF = NPREF >= 4 && 4 * (SLOTB + WINB) <= kLdsPair   ? 4
+                                : NPREF >= 3 && 3 * (SLOTB + WINB) <= kLdsPair ? 3
+                                                                               : 2;
     static constexpr int DPW = (NDW + kWaves - 1) / kWaves;  // weight blocks per wavefront per stage
     static constexpr int VPS = DPW + T::EPL;                 // vector-memory operations per stage
-    static constexpr size_t lds = sizeof(float4) * NBUF * SLOT4;
+    static constexpr size_t lds = NBUF * (SLOTB + WINB);
 };
 
 template <int RS_, int KPL, int TH, int TW>
@@ -92,9 +103,12 @@ void sparse_conv_fring_kernel(FringArgs a) {
     constexpr int KW = T::KW, NDW = SH::NDW, NBUF = SH::NBUF, DPW = SH::DPW, EPL = T::EPL;
 
     // ring of NBUF slots, each one channel's weights [R*S][KW] (k = kbase +
-    // lane*KPL + j) padded to whole 1 KB blocks; static, so that the compiler
-    // can tell the slot being read from the slots being filled
-    __shared__ float4 wring[NBUF][SH::SLOT4];
+    // lane*KPL + j) padded to whole 1 KB blocks, then the wavefronts' input
+    // windows [wavefront][q][lane].  Static, so that the compiler can tell
+    // the slot being read from the slots being filled, and the kernel's only
+    // LDS variable: with a second one the compiler makes every read of the
+    // ring wait for all loads into LDS in flight, prefetched stages included.
+    __shared__ float4 wring[NBUF][SH::SLOT4 + SH::WIN4];
 
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
@@ -129,9 +143,6 @@ void sparse_conv_fring_kernel(FringArgs a) {
         xoff[q] = inwin[q] ? y * W + xx : 0;
     }
 
-    // input windows, one register ring slot per weight slot
-    float xw[NBUF][EPL];
-
     // stage c -> slot SLOT: weights by direct global->LDS loads (every
     // wavefront issues exactly DPW blocks and EPL window loads, so the number
     // of vector-memory operations per stage is the same everywhere)
@@ -150,7 +161,8 @@ void sparse_conv_fring_kernel(FringArgs a) {
         }
         const float *plane = x_n + static_cast<size_t>(c) * HW;
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) xw[SLOT][q] = plane[xoff[q]];
+        for (int q = 0; q < EPL; ++q)
+            tile::load_lds4(plane + xoff[q], reinterpret_cast<float *>(&wring[SLOT][SH::SLOT4]) + (wave * EPL + q) * kLanes);
     };
 
     // prologue: stages 0 .. NBUF-2 in flight before the decision is read
@@ -172,9 +184,9 @@ void sparse_conv_fring_kernel(FringArgs a) {
             for (int j = 0; j < KPL; ++j) acc[y][x][j] = 0.0f;
 
     // per channel: wait for its stage and the barrier, issue the stage NBUF-1
-    // channels ahead, then read the channel's weights (LDS -> registers) and
-    // copy its window into one set of registers, so that the scan (most of
-    // the code) is inlined once
+    // channels ahead, then read the channel's weights and window (LDS ->
+    // registers) into one set of registers, so that the scan (most of the
+    // code) is inlined once
     float cur[EPL];
     tile::Wts<T> w;
 #pragma unroll 1
@@ -187,8 +199,9 @@ void sparse_conv_fring_kernel(FringArgs a) {
                 tile::wait_vm_and_barrier<(NBUF - 2) * SH::VPS>();
                 issue(std::integral_constant<int, (B + NBUF - 1) % NBUF>{}, min(c + NBUF - 1, C - 1));
                 tile::load_weights<T>(reinterpret_cast<const float *>(&wring[B][0]), lane, w);
+                const float *win = reinterpret_cast<const float *>(&wring[B][SH::SLOT4]) + wave * EPL * kLanes + lane;
 #pragma unroll
-                for (int q = 0; q < EPL; ++q) cur[q] = xw[B][q];
+                for (int q = 0; q < EPL; ++q) cur[q] = win[q * kLanes];
                 tile::wait_lgkm0();
             }
         });
@@ -200,10 +213,15 @@ void sparse_conv_fring_kernel(FringArgs a) {
     __builtin_amdgcn_s_waitcnt(0);  // no load into LDS may outlive the workgroup
 
     // step 3: each lane stores its accumulators to NCHW
+    uint32_t cnt = 0;
     if (rows_ok) {
         const size_t plane_out = static_cast<size_t>(a.Ho) * a.Wo;
         float *yrow = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oy0) * a.Wo + ox0;
-        tile::store_tile<T>(acc, yrow, plane_out, a.Wo, kbase, lane, a.K, a.Ho - oy0, tw);
+        cnt = tile::store_tile<T>(acc, yrow, plane_out, a.Wo, kbase, lane, a.K, a.Ho - oy0, tw, a.epi.relu);
+    }
+    if (a.epi.census) {
+        __syncthreads();  // every wavefront is done with the ring
+        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(&wring[0][0]));
     }
 }
 
@@ -214,8 +232,9 @@ hipError_t launch_fring_t(const FringArgs &a, hipStream_t s) {
     } else {
         using SH = FringShape<RS_, KPL, TH, TW>;
         static_assert(SH::lds <= kLdsMax, "weight ring exceeds LDS");
-        const int grid = a.N * a.bands * a.ctiles * a.kgroups;
-        sparse_conv_fring_kernel<RS_, KPL, TH, TW><<<grid, kWaves * kLanes, 0, s>>>(a);
+        const int64_t grid = static_cast<int64_t>(a.N) * a.bands * a.ctiles * a.kgroups;
+        if (a.epi.census && census_slots_for(grid) > a.epi.cap) return hipErrorInvalidValue;
+        sparse_conv_fring_kernel<RS_, KPL, TH, TW><<<static_cast<unsigned>(grid), kWaves * kLanes, 0, s>>>(a);
         return hipGetLastError();
     }
 }

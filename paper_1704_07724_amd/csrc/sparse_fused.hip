@@ -57,6 +57,14 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
 }  // namespace
 }  // namespace fused
 
+// The filter-resident kernel launches N * bands <= N * Ho workgroups; the
+// filter-ring kernel N * bands * column tiles * map groups, with bands <=
+// ceil(Ho / 4), column tiles <= ceil(Wo / 16) and map groups <= ceil(K / 64).
+int64_t sparse_fused_max_groups(const SparseShape &sh) {
+    const int64_t ring = static_cast<int64_t>((sh.Ho + 3) / 4) * ((sh.Wo + 15) / 16) * ((sh.K + 63) / 64);
+    return static_cast<int64_t>(sh.N) * std::max<int64_t>(sh.Ho, ring);
+}
+
 bool sparse_fused_applies(const SparseShape &sh) {
     fused::FusedPlan p;
     return fused::fused_plan(sh, &p) || sparse_fring_applies(sh);
@@ -70,10 +78,10 @@ int sparse_fused_kernel(const SparseShape &sh) {
 // The filter-resident kernel when the filter fits in LDS, else the
 // filter-ring kernel.
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
-                               hipStream_t s) {
+                               hipStream_t s, const Epilogue &epi) {
     using namespace fused;
     FusedPlan p;
-    if (!fused_plan(sh, &p)) return launch_sparse_fring(sh, x, wt, y, dec, s);
+    if (!fused_plan(sh, &p)) return launch_sparse_fring(sh, x, wt, y, dec, s, epi);
     FusedArgs a{};
     a.x = x;
     a.wt = wt;
@@ -83,6 +91,7 @@ hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const floa
     a.rg = kWaves / p.cs;
     a.bands = (sh.Ho + a.rg * p.th - 1) / (a.rg * p.th);
     a.dec = dec;
+    a.epi = epi;
     switch (sh.R) {
     case 1: return launch_r1(a, p, s);
     case 3: return launch_r3(a, p, s);

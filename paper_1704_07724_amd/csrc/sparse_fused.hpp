@@ -50,6 +50,7 @@ struct FusedArgs {
     int rg;           // row groups per workgroup (kWaves / cs)
     int bands;        // groups of rg * TH output rows
     Decision dec;
+    Epilogue epi;     // rectifier and census of y
 };
 
 struct FusedPlan {
@@ -197,7 +198,6 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     const int ostep = (kWaves * kLanes) / npos;
     const int k0 = tid / npos;
     const int pos = tid - k0 * npos;
-    if (k0 >= ostep) return;
     const int oyl = pos / Wo;
     const int ox = pos - oyl * Wo;
     const int g = oyl / TH;
@@ -209,14 +209,23 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     int poff[kWaves];
 #pragma unroll
     for (int p = 0; p < kWaves; ++p) poff[p] = min(p, cs - 1) * TP * kRPad;
-    for (int k = k0; k < a.K; k += ostep) {
+    const int relu = a.epi.relu;
+    uint32_t cnt = 0;
+    // threads past ostep map groups have no output (k0 >= ostep)
+    for (int k = k0 < ostep ? k0 : a.K; k < a.K; k += ostep) {
         float part[kWaves];
 #pragma unroll
         for (int p = 0; p < kWaves; ++p) part[p] = src[poff[p] + k];
         float sum = part[0];
 #pragma unroll
         for (int p = 1; p < kWaves; ++p) sum += p < cs ? part[p] : 0.0f;
+        sum = epilogue_value(sum, relu);
+        cnt += nonzero_bit(sum);
         dst[static_cast<size_t>(k) * plane_out] = sum;
+    }
+    if (a.epi.census) {
+        __syncthreads();  // every thread is done reading the phase tiles
+        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(lds));
     }
 }
 
@@ -231,7 +240,9 @@ hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
             if (e != hipSuccess) return e;
         }
-        kern<<<a.N * a.bands, kWaves * kLanes, lds, s>>>(a);
+        const int64_t grid = static_cast<int64_t>(a.N) * a.bands;
+        if (a.epi.census && census_slots_for(grid) > a.epi.cap) return hipErrorInvalidValue;
+        kern<<<static_cast<unsigned>(grid), kWaves * kLanes, lds, s>>>(a);
         return hipGetLastError();
     }
 }

@@ -233,10 +233,12 @@ __device__ __forceinline__ void wait_vm_and_barrier() {
 }
 
 // Store the tile rows/columns inside the output (rows < rows_ok, columns <
-// cols_ok) and maps < K to NCHW; yrow points at y[n][0][oy0][ox0].
+// cols_ok) and maps < K to NCHW, rectified when relu is set; yrow points at
+// y[n][0][oy0][ox0].  Returns how many of the stored values are nonzero.
 template <typename SH>
-__device__ __forceinline__ void store_tile(const Acc<SH> &acc, float *yrow, size_t plane_out, int Wo, int kbase,
-                                           int lane, int K, int rows_ok, int cols_ok) {
+__device__ __forceinline__ uint32_t store_tile(const Acc<SH> &acc, float *yrow, size_t plane_out, int Wo, int kbase,
+                                               int lane, int K, int rows_ok, int cols_ok, int relu = 0) {
+    uint32_t cnt = 0;
 #pragma unroll
     for (int j = 0; j < SH::KPL; ++j) {
         const int k = kbase + lane * SH::KPL + j;
@@ -247,9 +249,14 @@ __device__ __forceinline__ void store_tile(const Acc<SH> &acc, float *yrow, size
             if (oy >= rows_ok) break;
 #pragma unroll
             for (int ox = 0; ox < SH::TW; ++ox)
-                if (ox < cols_ok) dst[oy * Wo + ox] = acc[oy][ox][j];
+                if (ox < cols_ok) {
+                    const float v = epilogue_value(acc[oy][ox][j], relu);
+                    cnt += nonzero_bit(v);
+                    dst[oy * Wo + ox] = v;
+                }
         }
     }
+    return cnt;
 }
 
 }  // namespace tile

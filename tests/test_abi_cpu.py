@@ -164,3 +164,56 @@ def test_fused_entry_validation():
     assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, x + 4, None) == 5   # y overlaps x
     assert L.isc_sparse_conv_fused(ctypes.byref(ok), x + 2, w, y, None) == 9   # misaligned
     assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, y, None) == 7       # no gfx950 here
+
+
+def test_census_size():
+    # room for the workgroups of every kernel that may write the output: at
+    # least the GEMM's ceil(K/32) * ceil(N*Ho*Wo/64) and the 1024 of the
+    # stand-alone epilogue pass, after a 16-byte header; multiple of 16 bytes
+    d = isc.make_desc(128, 256, 13, 13, 384, 3, 3, 1, 1)
+    n = isc.isc_census_size(d)
+    assert n % 16 == 0
+    assert n >= 16 + 4 * (384 // 32) * ((128 * 169 + 63) // 64)
+    small = isc.isc_census_size(isc.make_desc(1, 1, 3, 3, 1, 3, 3, 1, 0))
+    assert small >= 16 + 4 * 1024
+    with pytest.raises(isc.IscError) as e:
+        isc.isc_census_size(isc.make_desc(0, 1, 3, 3, 1, 3, 3, 1, 0))
+    assert e.value.status == 2
+
+
+def _relu(desc, x=0x1000, xc=None, xcb=0, w=0x200000, wt=None, y=0x400000, yc=None, ycb=0,
+          ws=0x800000, ws_bytes=1 << 30, path=0, th=0.9):
+    return isc.lib().isc_conv2d_relu(ctypes.byref(desc), x, xc, xcb, w, wt, y, yc, ycb, ws, ws_bytes,
+                                     path, ctypes.c_float(th), None)
+
+
+def test_conv2d_relu_validation():
+    good = isc.make_desc(2, 3, 8, 8, 4, 3, 3, 1, 1)
+    cb = isc.isc_census_size(good)
+    yc = 0x10000000
+    assert _relu(good, x=0) == 1
+    assert _relu(good, yc=yc, ycb=cb - 16) == 4                  # census too small
+    assert _relu(good, yc=yc + 8, ycb=cb) == 9                   # census misaligned
+    assert _relu(good, xc=0x20000008, xcb=4096) == 9             # input census misaligned
+    assert _relu(good, xc=0x20000000, xcb=8) == 4                # input census below its header
+    assert _relu(good, wt=0x30000004) == 9                       # repacked filter misaligned
+    assert _relu(good, yc=0x400000, ycb=cb) == 5                 # census overlaps y
+    assert _relu(good, yc=0x1000, ycb=cb) == 5                   # census overlaps x
+    assert _relu(good, yc=yc, ycb=cb, xc=yc, xcb=cb) == 5        # input and output census overlap
+    assert _relu(good, wt=0x400000) == 5                         # wt overlaps y
+    assert _relu(good, y=0x1000) == 5
+    assert _relu(good, path=9) == 6
+    try:
+        import torch
+        if torch.cuda.is_available():
+            return
+    except Exception:
+        pass
+    assert _relu(good, yc=yc, ycb=cb, xc=0x20000000, xcb=cb) == 7  # valid; no gfx950 here
+
+
+def test_census_read_validation():
+    L = isc.lib()
+    e, n = ctypes.c_uint64(), ctypes.c_uint64()
+    assert L.isc_census_read(None, 4096, ctypes.byref(e), ctypes.byref(n), None) == 1
+    assert L.isc_census_read(0x1000, 8, ctypes.byref(e), ctypes.byref(n), None) == 4
