@@ -193,6 +193,98 @@ class LayerRun:
         return out
 
 
+class ChainRun:
+    """conv3 -> ReLU -> conv4 -> ReLU -> conv5 (the layer-chain workload):
+    the rectifier fused into each layer's epilogue, each layer deciding from
+    the census its predecessor wrote, filters repacked once (as an inference
+    engine holds them); against the same chain with separate launches
+    (isc_conv2d, which counts its input and repacks its filter, then a ReLU
+    pass) and against the dense path with the fused rectifier."""
+
+    def __init__(self, torch, isc, workload):
+        self.torch, self.isc, self.workload = torch, isc, workload
+        x0, ws = workloads.make_chain(workload)
+        self.x0 = torch.from_numpy(x0).cuda()
+        self.w = [torch.from_numpy(w).cuda() for w in ws]
+        self.wt = [isc.isc_repack_filter(w) for w in self.w]
+        self.layers = workload.layers
+        self.descs, self.ys, self.census, self.ws = [], [], [], []
+        x_shape = x0.shape
+        for L in self.layers:
+            d = isc.make_desc(*x_shape, L.K, L.R, L.S, L.T, L.P)
+            ho, wo = isc.isc_out_shape(d)
+            self.descs.append(d)
+            self.ys.append(torch.empty((x_shape[0], L.K, ho, wo), device="cuda"))
+            self.census.append(isc.census(d))
+            self.ws.append({p: isc.workspace(d, p) for p in ("auto", "dense")})
+            x_shape = (x_shape[0], L.K, ho, wo)
+        torch.cuda.synchronize()
+
+    def fused(self):
+        isc, L = self.isc, self.layers
+
+        def run():
+            x, xc = self.x0, None
+            for i in range(len(L)):
+                isc.isc_conv2d_relu(x, self.w[i], L[i].T, L[i].P, x_census=xc, wt=self.wt[i],
+                                    y_census=self.census[i], out=self.ys[i], ws=self.ws[i]["auto"])
+                x, xc = self.ys[i], self.census[i]
+        return run
+
+    def separate(self):
+        isc, L, torch = self.isc, self.layers, self.torch
+
+        def run():
+            x = self.x0
+            for i in range(len(L)):
+                isc.isc_conv2d(x, self.w[i], L[i].T, L[i].P, out=self.ys[i], ws=self.ws[i]["auto"])
+                torch.relu_(self.ys[i])
+                x = self.ys[i]
+        return run
+
+    def dense(self):
+        isc, L = self.isc, self.layers
+
+        def run():
+            x = self.x0
+            for i in range(len(L)):
+                isc.isc_conv2d_relu(x, self.w[i], L[i].T, L[i].P, path="dense", out=self.ys[i],
+                                    ws=self.ws[i]["dense"])
+                x = self.ys[i]
+        return run
+
+    def measure(self, steps, warmup, graphs=True):
+        torch = self.torch
+        res = {}
+        for name in ("fused", "separate", "dense"):
+            fn = getattr(self, name)()
+            if graphs:
+                fn = graph_of(torch, fn).replay
+            res["t_chain_%s_ms" % name] = event_time_ms(torch, fn, steps, warmup)
+        # the activations of the fused run (the last one timed wrote the
+        # dense run's outputs, equal up to rounding): run it once more
+        self.fused()()
+        torch.cuda.synchronize()
+        xs = [self.x0] + self.ys[:-1]
+        res["input_sparsity"] = [round(1.0 - int(torch.count_nonzero(x).item()) / x.numel(), 6) for x in xs]
+        res["paths"] = []
+        for i, d in enumerate(self.descs):
+            _, path = self.isc.isc_decision(d, self.ws[i]["auto"])
+            res["paths"].append(path)
+        flops = 0.0
+        x_shape = tuple(self.x0.shape)
+        for L in self.layers:
+            d = self.isc.make_desc(*x_shape, L.K, L.R, L.S, L.T, L.P)
+            ho, wo = self.isc.isc_out_shape(d)
+            flops += dense_flops(L.with_(N=x_shape[0]), ho, wo)
+            x_shape = (x_shape[0], L.K, ho, wo)
+        res["dense_gflop"] = round(flops / 1e9, 4)
+        res["tflops_chain_fused"] = round(flops / (res["t_chain_fused_ms"] * 1e-3) / 1e12, 3)
+        res["speedup_fused_vs_separate"] = round(res["t_chain_separate_ms"] / res["t_chain_fused_ms"], 3)
+        res["speedup_fused_vs_dense"] = round(res["t_chain_dense_ms"] / res["t_chain_fused_ms"], 3)
+        return res
+
+
 def cpu_baseline(layer, budget_s=10.0):
     """The oracle (fp64 direct convolution) on the headline workload, timed on
     this host: with all its threads, repeated over the whole batch (or the
@@ -237,7 +329,7 @@ def cpu_baseline(layer, budget_s=10.0):
 
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "lenet_conv2_s0.9_hbm_counters.md")
 SPARSE_SOURCES = [os.path.join(ROOT, "paper_1704_07724_amd", "csrc", f)
-                  for f in ("sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp")]
+                  for f in ("sparse_fused.hpp", "sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp")]
 
 
 def sparse_source_hash() -> str:
@@ -440,6 +532,19 @@ def main():
     if args.all:
         rows = []
         for wl in workloads.WORKLOADS.values():
+            if wl.name == "alexnet_chain345":
+                chain = ChainRun(torch, isc, wl)
+                r = chain.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph)
+                r["workload"] = wl.name
+                rows.append(r)
+                print("# %s: fused %.4f ms separate %.4f dense %.4f (fused vs separate %.2fx, vs dense %.2fx) "
+                      "input sparsity %s paths %s" % (
+                          wl.name, r["t_chain_fused_ms"], r["t_chain_separate_ms"], r["t_chain_dense_ms"],
+                          r["speedup_fused_vs_separate"], r["speedup_fused_vs_dense"], r["input_sparsity"],
+                          r["paths"]), file=sys.stderr, flush=True)
+                del chain
+                torch.cuda.empty_cache()
+                continue
             for layer in wl.layers:
                 if wl.name == "lenet_conv2_batch":
                     continue
