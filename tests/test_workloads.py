@@ -49,7 +49,7 @@ def test_clustered_exact_zero_count():
 def test_workload_shapes():
     names = set(workloads.WORKLOADS)
     assert names == {"lenet_conv2_tiny", "lenet_conv2_batch", "alexnet_conv2",
-                     "alexnet_conv345", "inception_28", "alexnet_chain345"}
+                     "alexnet_conv345", "inception_28", "alexnet_chain345", "paper_tab2", "paper_tab2_n1"}
     sweep = workloads.WORKLOADS["lenet_conv2_batch"].layers
     assert [l.sparsity for l in sweep] == [0.5, 0.7, 0.9, 0.95, 0.99]
     assert len({l.seed for l in sweep}) == 5
@@ -76,3 +76,20 @@ def test_chain_weights_and_input():
     # weights drawn again from the same seeds are the same
     _, ws2 = workloads.make_chain(chain, N=1)
     assert all(np.array_equal(a, b) for a, b in zip(ws, ws2))
+
+
+def test_tab2_layers():
+    """The ten layers of the paper's Tab. 2 (C, H_in, K, R x S, P, T,
+    sparsity as printed), at batch 128 and batch 1, each with its own seed."""
+    for name, n in (("paper_tab2", 128), ("paper_tab2_n1", 1)):
+        layers = workloads.WORKLOADS[name].layers
+        assert len(layers) == 10 and all(l.N == n for l in layers)
+        assert len({l.seed for l in layers}) == 10
+        first = layers[0]
+        assert (first.C, first.H, first.W, first.K, first.R, first.S, first.P, first.T, first.sparsity) == \
+            (20, 11, 11, 64, 5, 5, 1, 2, 0.95)
+        last = layers[-1]
+        assert (last.C, last.H, last.K, last.R, last.P, last.T, last.sparsity) == (48, 7, 128, 5, 2, 1, 0.95)
+        assert sorted({l.sparsity for l in layers}) == [0.9, 0.95]
+    x, _ = workloads.make_inputs(workloads.WORKLOADS["paper_tab2_n1"].layers[6])
+    assert x.shape == (1, 832, 7, 7) and abs((x == 0).mean() - 0.95) < 0.01

@@ -91,6 +91,28 @@ def _lenet(name, N, config, sparsity, sweep_index=0):
                  config=config, sweep_index=sweep_index)
 
 
+# Tab. 2 of the paper: name, C, H_in (= W_in), K, R (= S), P, T, sparsity
+TAB2 = (
+    ("lenet_conv2", 20, 11, 64, 5, 1, 2, 0.95),
+    ("alexnetc_conv3", 32, 6, 64, 5, 2, 1, 0.9),
+    ("alexneti_conv4", 384, 5, 384, 3, 1, 1, 0.9),
+    ("inception4a_1", 480, 14, 192, 1, 0, 1, 0.9),
+    ("inception4a_2", 192, 14, 96, 1, 0, 1, 0.9),
+    ("inception4e_3", 160, 14, 320, 3, 1, 1, 0.9),
+    ("inception5a_1", 832, 7, 256, 1, 0, 1, 0.95),
+    ("inception5a_2", 256, 7, 160, 1, 0, 1, 0.9),
+    ("inception5b_3", 192, 7, 384, 3, 1, 1, 0.95),
+    ("inception5b_5", 48, 7, 128, 5, 2, 1, 0.95),
+)
+
+
+def _tab2(N, config):
+    suffix = "" if N == 128 else "_n%d" % N
+    return [Layer("tab2_%s%s" % (name, suffix), N, C, H, H, K, R, R, T, P, sp, 0.1 if name == "lenet_conv2" else 0.01,
+                  config=config, layer=i)
+            for i, (name, C, H, K, R, P, T, sp) in enumerate(TAB2)]
+
+
 WORKLOADS = {
     # LeNet conv2, 20->50 maps at 12x12, 5x5, no pad: tiny batch
     "lenet_conv2_tiny": Workload("lenet_conv2_tiny", (_lenet("lenet_conv2", 8, 1, 0.9),)),
@@ -115,6 +137,10 @@ WORKLOADS = {
         Layer("chain_conv5", 128, 384, 13, 13, 256, 3, 3, 1, 1, 0.95, 0.01, w_mean=-0.189 * 0.01,
               config=6, layer=2),
     )),
+    # the layers of the paper's Tab. 2 at their listed sparsity, batch 128 and
+    # batch 1 (the paper's runs are one image at a time)
+    "paper_tab2": Workload("paper_tab2", tuple(_tab2(128, 7))),
+    "paper_tab2_n1": Workload("paper_tab2_n1", tuple(_tab2(1, 8))),
     # GoogLeNet inception-shaped, 28x28: 3x3 branch and 5x5 branch, clustered zeros
     "inception_28": Workload("inception_28", (
         Layer("inception_3x3", 128, 96, 28, 28, 128, 3, 3, 1, 1, 0.9, 0.01, True, config=5, layer=0),
