@@ -21,6 +21,9 @@ What each function follows (Shi & Chu, arXiv 1704.07724):
   relu_conv2d_f64              Eq. 1 followed by the rectifier of Eq. 2
                                (Sec. "Sparsity of ReLUs"), with the nonzero
                                count of the rectified output
+  conv2d_dw_f64                the weight gradient of Eq. 1 (training, whose
+                               rectified inputs the paper measures in Sec.
+                               "Sparsity of ReLUs")
 
 Pins (tests/test_oracle_pins.py) tie each function to something other than
 itself: brute-force loops, closed forms, numpy / torch library routines,
@@ -68,6 +71,8 @@ def load_library(path: str):
     lib.oracle_nz_macs.restype = i64
     lib.oracle_im2col.argtypes = [vp] + [i32] * 8 + [i64, vp]
     lib.oracle_im2col.restype = None
+    lib.oracle_conv2d_dw_f64.argtypes = [vp, vp] + [i32] * 9 + [vp]
+    lib.oracle_conv2d_dw_f64.restype = None
     lib.oracle_rectify_f64.argtypes = [vp, i64]
     lib.oracle_rectify_f64.restype = i64
     lib.oracle_threads.argtypes = []
@@ -158,6 +163,21 @@ def relu_conv2d_f64(x, w, stride: int = 1, pad: int = 0):
     y = conv2d_f64(x, w, stride, pad)
     nnz = int(_load().oracle_rectify_f64(_ptr(y), y.size)) if y.size else 0
     return y, nnz
+
+
+def conv2d_dw_f64(x, dy, R: int, S: int, stride: int = 1, pad: int = 0) -> np.ndarray:
+    """Weight gradient of Eq. 1: dw[k,c,r,s] = sum over n, i, j of
+    dy[n,k,i,j] * X^[n, c, i*T + r - P, j*T + s - P], fp64 (K x C x R x S)."""
+    x, dy = _f32(x), _f32(dy)
+    N, C, H, W = x.shape
+    Ho, Wo = out_size(H, R, pad, stride), out_size(W, S, pad, stride)
+    if dy.shape[0] != N or dy.shape[2:] != (Ho, Wo):
+        raise ValueError("dy must be N x K x Ho x Wo")
+    K = dy.shape[1]
+    dw = np.zeros((K, C, R, S), dtype=np.float64)
+    if dw.size and Ho > 0 and Wo > 0:
+        _load().oracle_conv2d_dw_f64(_ptr(x), _ptr(dy), N, C, H, W, K, R, S, stride, pad, _ptr(dw))
+    return dw
 
 
 def compact(x):

@@ -247,3 +247,30 @@ int64_t oracle_rectify_f64(double *y, int64_t n)
     }
     return nnz;
 }
+
+/* Weight gradient of Eq. 1 for training (the paper measures the sparsity of
+ * the rectified inputs during training, Sec. "Sparsity of ReLUs"): with
+ * dy = dLoss/dO of shape N x K x Ho x Wo,
+ *   dw[k,c,r,s] = sum_{n,i,j} dy[n,k,i,j] * X^[n, c, i*T + r - P, j*T + s - P]
+ * (X^ = x inside the map, 0 outside), fp64 accumulation in (n, i, j) order.
+ * dw is K x C x R x S. */
+void oracle_conv2d_dw_f64(const float *x, const float *dy, int N, int C, int H, int W,
+                          int K, int R, int S, int T, int P, double *dw)
+{
+    const long Ho = oracle_out_size(H, R, P, T);
+    const long Wo = oracle_out_size(W, S, P, T);
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (long k = 0; k < K; ++k)
+        for (long c = 0; c < C; ++c)
+            for (long r = 0; r < R; ++r)
+                for (long s = 0; s < S; ++s) {
+                    double acc = 0.0;
+                    for (long n = 0; n < N; ++n)
+                        for (long i = 0; i < Ho; ++i)
+                            for (long j = 0; j < Wo; ++j) {
+                                double xv = oracle_xhat(x, n, c, i * T + r - P, j * T + s - P, C, H, W);
+                                acc += (double)dy[((n * K + k) * Ho + i) * Wo + j] * xv;
+                            }
+                    dw[((k * C + c) * R + r) * S + s] = acc;
+                }
+}

@@ -37,6 +37,9 @@ MUTANTS = {
     "macs_bound_inclusive": ("if (num / t < out) ++cnt;", "if (num / t <= out) ++cnt;"),
     "relu_keeps_negatives": ("        if (y[i] > 0.0)\n            ++nnz;", "        if (y[i] < 0.0)\n            ++nnz;"),
     "relu_counts_zeros": ("        if (y[i] > 0.0)\n            ++nnz;", "        if (y[i] >= 0.0)\n            ++nnz;"),
+    "dw_tap_sign": ("double xv = oracle_xhat(x, n, c, i * T + r - P, j * T + s - P, C, H, W);",
+                    "double xv = oracle_xhat(x, n, c, i * T - r + P, j * T + s - P, C, H, W);"),
+    "dw_map_transposed": ("dw[((k * C + c) * R + r) * S + s] = acc;", "dw[((c * K + k) * R + r) * S + s] = acc;"),
     "im2col_rs_swapped": ("long y = i * T + r - P, xx = j * T + s - P;",
                           "long y = i * T + s - P, xx = j * T + r - P;"),
 }

@@ -15,7 +15,11 @@
   of Fig. 3 (M_K x M_I = M_O);
 - the rectifier of Eq. 2 against torch.relu, the exact split
   relu(o) - relu(-o) = o, and the identity / all-zero closed forms; its
-  nonzero count against numpy's count of positive outputs.
+  nonzero count against numpy's count of positive outputs;
+- the weight gradient against its zero-skipping scatter form in plain Python,
+  torch's conv2d_weight in float64, the adjoint identity
+  <conv(x, w), dy> = <w, dw(x, dy)> (exact on dyadic values, which ties it to
+  the pinned forward oracle) and the 1x1 matrix product.
 """
 import itertools
 
@@ -371,3 +375,86 @@ def test_relu_closed_forms():
     assert nnz == int(np.count_nonzero(y))
     y2, nnz2 = oracle.relu_conv2d_f64(x, -w, 1, 1)
     assert nnz2 == 0 and np.all(y2 == 0.0)
+
+
+# ------------------------------------------- weight gradient (training) ---
+
+def scatter_dw_py(x, dy, R, S, T, P):
+    """Zero-skipping form: every nonzero input adds x * dy at each output it
+    reaches to the gradient of the tap that connects them."""
+    N, C, H, W = x.shape
+    K, Ho, Wo = dy.shape[1], dy.shape[2], dy.shape[3]
+    dw = [[[[0.0] * S for _ in range(R)] for _ in range(C)] for _ in range(K)]
+    for n in range(N):
+        for c in range(C):
+            for y in range(H):
+                for xx in range(W):
+                    v = float(x[n, c, y, xx])
+                    if v == 0.0:
+                        continue
+                    for r in range(R):
+                        ty = y + P - r
+                        if ty < 0 or ty % T or ty // T >= Ho:
+                            continue
+                        for s in range(S):
+                            tx = xx + P - s
+                            if tx < 0 or tx % T or tx // T >= Wo:
+                                continue
+                            for k in range(K):
+                                dw[k][c][r][s] += v * float(dy[n, k, ty // T, tx // T])
+    return np.array(dw, dtype=np.float64)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dw_equals_scatter_form_bruteforce(seed):
+    rng = np.random.default_rng(5000 + seed)
+    N = int(rng.integers(1, 3)); C = int(rng.integers(1, 4)); K = int(rng.integers(1, 4))
+    R = int(rng.choice([1, 2, 3])); S = int(rng.choice([1, 3]))
+    T = int(rng.integers(1, 4)); P = int(rng.integers(0, 3))
+    H = int(rng.integers(max(1, R - 2 * P), 8)); W = int(rng.integers(max(1, S - 2 * P), 8))
+    x, _ = rand_case(rng, N, C, H, W, K, R, S)
+    Ho, Wo = oracle.out_size(H, R, P, T), oracle.out_size(W, S, P, T)
+    dy = rng.standard_normal((N, K, Ho, Wo)).astype(np.float32)
+    np.testing.assert_allclose(oracle.conv2d_dw_f64(x, dy, R, S, T, P), scatter_dw_py(x, dy, R, S, T, P),
+                               rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_dw_against_torch_float64(seed):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(5100 + seed)
+    N = int(rng.integers(1, 4)); C = int(rng.integers(1, 7)); K = int(rng.integers(1, 7))
+    R = int(rng.choice([1, 3, 5])); S = R
+    T = int(rng.integers(1, 3)); P = int(rng.integers(0, 3))
+    H = int(rng.integers(max(1, R - 2 * P), 14)); W = int(rng.integers(max(1, S - 2 * P), 14))
+    x, _ = rand_case(rng, N, C, H, W, K, R, S, sparsity=0.8)
+    Ho, Wo = oracle.out_size(H, R, P, T), oracle.out_size(W, S, P, T)
+    dy = rng.standard_normal((N, K, Ho, Wo)).astype(np.float32)
+    want = torch.nn.grad.conv2d_weight(torch.from_numpy(x).double(), (K, C, R, S), torch.from_numpy(dy).double(),
+                                       stride=T, padding=P).numpy()
+    np.testing.assert_allclose(oracle.conv2d_dw_f64(x, dy, R, S, T, P), want, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("T,P", [(1, 0), (1, 2), (2, 1)])
+def test_dw_adjoint_of_the_convolution(T, P):
+    # <conv(x, w), dy> = <w, dw(x, dy)> for every w: the gradient is the
+    # adjoint of Eq. 1 in w.  Dyadic values keep both sides exact in fp64.
+    rng = np.random.default_rng(5200 + T + P)
+    N, C, H, W, K, R, S = 2, 3, 8, 7, 4, 3, 3
+    x = (rng.integers(0, 8, (N, C, H, W)) / 4).astype(np.float32)
+    x[rng.random(x.shape) < 0.6] = 0.0
+    w = (rng.integers(-8, 9, (K, C, R, S)) / 8).astype(np.float32)
+    o = oracle.conv2d_f64(x, w, T, P)
+    dy = (rng.integers(-8, 9, o.shape) / 2).astype(np.float32)
+    lhs = float(np.sum(o * dy.astype(np.float64)))
+    rhs = float(np.sum(w.astype(np.float64) * oracle.conv2d_dw_f64(x, dy, R, S, T, P)))
+    assert lhs == rhs
+
+
+def test_dw_one_by_one_is_matmul_and_zero_input():
+    rng = np.random.default_rng(5300)
+    x, _ = rand_case(rng, 3, 5, 6, 4, 2, 1, 1)
+    dy = rng.standard_normal((3, 7, 6, 4)).astype(np.float32)
+    want = sum(dy[n].reshape(7, -1).astype(np.float64) @ x[n].reshape(5, -1).T.astype(np.float64) for n in range(3))
+    np.testing.assert_allclose(oracle.conv2d_dw_f64(x, dy, 1, 1)[:, :, 0, 0], want, rtol=1e-13, atol=1e-13)
+    assert np.all(oracle.conv2d_dw_f64(np.zeros_like(x), dy, 1, 1) == 0.0)
