@@ -264,6 +264,34 @@ enum isc_kernel {
 };
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel);
 
+/* ---- Training: the weight gradient with zero skipping ----
+ *
+ * The paper measures the sparsity of the rectified inputs during training
+ * (Sec. "Sparsity of ReLUs").  The gradient of Eq. 1 with respect to the
+ * filter multiplies every input by output gradients, so a zero input adds
+ * nothing: isc_conv2d_dw visits the nonzero inputs only, each meeting the
+ * K-contiguous vector of output gradients it reaches (ISC step 2 with the
+ * roles of filter and output exchanged). */
+
+/* Bytes of device workspace isc_conv2d_dw needs (per-range partial sums).
+ * Host-only.  Errors: NULL, SHAPE, LIMIT (not stride 1 with a square 1x1,
+ * 3x3 or 5x5 filter). */
+int isc_conv2d_dw_workspace_size(const isc_conv_desc *d, size_t *bytes);
+
+/*   dw[k,c,r,s] = sum_{n,i,j} dy[n,k,i,j] * x[n, c, i*T + r - P, j*T + s - P]
+ * (x taken as 0 outside the map), stride T = 1.
+ *   x: device input N x C x H x W; dy: device output gradient N x K x Ho x Wo
+ *     (read only).
+ *   dw: device K x C x R x S, fully written; must not overlap x, dy or ws.
+ *   ws, ws_bytes: workspace of isc_conv2d_dw_workspace_size bytes, 256-byte
+ *     aligned; contents on entry are ignored.
+ * Two launches: one wavefront per 64 or 128 output maps, a few input channels
+ * and a range of output rows sums in registers over the nonzero inputs of
+ * its range; the ranges' sums are then added in order.  fp32, deterministic.
+ * Errors: NULL, SHAPE, LIMIT, WORKSPACE, ALIAS, ALIGN, DEVICE, HIP. */
+int isc_conv2d_dw(const isc_conv_desc *d, const float *x, const float *dy, float *dw,
+                  void *ws, size_t ws_bytes, void *stream);
+
 /* The unrolled input matrix M_I of the matrix-multiplication formulation
  * (Sec. "Sparse Convolution", Fig. 3), with the batch as extra columns:
  *   col[(c*R + r)*S + s][(n*Ho + i)*Wo + j] = x[n, c, i*T + r - P, j*T + s - P]

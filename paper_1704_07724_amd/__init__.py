@@ -8,6 +8,7 @@ library (there is no fallback of any kind).
 The functions carry the C names:
     isc_out_shape, isc_workspace_size, isc_conv2d, isc_decision,
     isc_census_size, isc_conv2d_relu, isc_census_read,
+    isc_conv2d_dw_workspace_size, isc_conv2d_dw,
     isc_compact, isc_repacked_filter_size, isc_repack_filter,
     isc_sparse_conv, isc_sparse_conv_fused, isc_sparse_kernel,
     isc_im2col, isc_gemm_f32, isc_status_str, isc_version
@@ -33,6 +34,7 @@ EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
            "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
            "isc_census_size", "isc_conv2d_relu", "isc_census_read",
+           "isc_conv2d_dw_workspace_size", "isc_conv2d_dw",
            "isc_status_str", "isc_version")
 
 
@@ -80,6 +82,8 @@ def lib():
     L.isc_census_size.argtypes = [dp, ctypes.POINTER(sz)]
     L.isc_conv2d_relu.argtypes = [dp, vp, vp, sz, vp, vp, vp, vp, sz, vp, sz, i32, ctypes.c_float, vp]
     L.isc_census_read.argtypes = [vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64), vp]
+    L.isc_conv2d_dw_workspace_size.argtypes = [dp, ctypes.POINTER(sz)]
+    L.isc_conv2d_dw.argtypes = [dp, vp, vp, vp, vp, sz, vp]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = ctypes.c_int
     L.isc_status_str.argtypes = [ctypes.c_int]
@@ -255,6 +259,35 @@ def isc_census_read(census_buf, stream=None):
     _check(lib().isc_census_read(census_buf.data_ptr(), _nbytes(census_buf), ctypes.byref(elems),
                                  ctypes.byref(nnz), _stream(stream)), "isc_census_read")
     return elems.value, nnz.value
+
+
+def isc_conv2d_dw_workspace_size(desc: ConvDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().isc_conv2d_dw_workspace_size(ctypes.byref(desc), ctypes.byref(n)), "isc_conv2d_dw_workspace_size")
+    return n.value
+
+
+def isc_conv2d_dw(x, dy, R, S, stride=1, pad=0, out=None, ws=None, stream=None):
+    """The weight gradient dw [K, C, R, S] of Eq. 1 from x [N, C, H, W] and
+    the output gradient dy [N, K, Ho, Wo], over the nonzero inputs only."""
+    torch = _torch()
+    x = _dev_f32(x, "x")
+    dy = _dev_f32(dy, "dy")
+    N, C, H, W = (int(v) for v in x.shape)
+    K = int(dy.shape[1])
+    desc = make_desc(N, C, H, W, K, int(R), int(S), int(stride), int(pad))
+    ho, wo = isc_out_shape(desc)
+    if tuple(dy.shape) != (N, K, ho, wo):
+        raise ValueError("dy must be [N, K, Ho, Wo] = %r" % ((N, K, ho, wo),))
+    if out is None:
+        out = torch.empty((K, C, int(R), int(S)), dtype=torch.float32, device=x.device)
+    elif not out.is_contiguous() or tuple(out.shape) != (K, C, int(R), int(S)):
+        raise ValueError("out must be a contiguous [K, C, R, S] tensor")
+    if ws is None:
+        ws = torch.empty(max(isc_conv2d_dw_workspace_size(desc), 1), dtype=torch.uint8, device=x.device)
+    _check(lib().isc_conv2d_dw(ctypes.byref(desc), x.data_ptr(), dy.data_ptr(), out.data_ptr(), ws.data_ptr(),
+                               _nbytes(ws), _stream(stream)), "isc_conv2d_dw")
+    return out
 
 
 NZ_TAIL = 256  # spare entries isc_sparse_conv may read past the last plane

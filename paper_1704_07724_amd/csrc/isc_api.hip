@@ -426,6 +426,39 @@ int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w
     return hip_status(isc::launch_sparse_fused(sh, x, wt, y, dec, static_cast<hipStream_t>(stream)));
 }
 
+int isc_conv2d_dw_workspace_size(const isc_conv_desc *d, size_t *bytes) {
+    if (!bytes) return ISC_ERR_NULL;
+    Shape s;
+    const int st = check_desc(d, &s);
+    if (st) return st;
+    const isc::SparseShape sh = sparse_shape(s);
+    if (!isc::sparse_dw_applies(sh)) return ISC_ERR_LIMIT;
+    *bytes = align_up(sizeof(float) * isc::sparse_dw_workspace_floats(sh), kAlign);
+    return ISC_OK;
+}
+
+int isc_conv2d_dw(const isc_conv_desc *d, const float *x, const float *dy, float *dw, void *ws, size_t ws_bytes,
+                  void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !dy || !dw || !ws) return ISC_ERR_NULL;
+    if (!aligned(x, 4) || !aligned(dy, 4) || !aligned(dw, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
+    const isc::SparseShape sh = sparse_shape(s);
+    if (!isc::sparse_dw_applies(sh)) return ISC_ERR_LIMIT;
+    const size_t need = sizeof(float) * isc::sparse_dw_workspace_floats(sh);
+    if (ws_bytes < need) return ISC_ERR_WORKSPACE;
+    const size_t xb = sizeof(float) * static_cast<size_t>(s.in_elems());
+    const size_t yb = sizeof(float) * static_cast<size_t>(s.out_elems());
+    const size_t wb = sizeof(float) * static_cast<size_t>(s.filt_elems());
+    if (overlap(dw, wb, x, xb) || overlap(dw, wb, dy, yb) || overlap(dw, wb, ws, need) || overlap(ws, need, x, xb) ||
+        overlap(ws, need, dy, yb))
+        return ISC_ERR_ALIAS;
+    st = check_device();
+    if (st) return st;
+    return hip_status(isc::launch_sparse_dw(sh, x, dy, dw, static_cast<float *>(ws), static_cast<hipStream_t>(stream)));
+}
+
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {
     if (!kernel) return ISC_ERR_NULL;
     Shape s;

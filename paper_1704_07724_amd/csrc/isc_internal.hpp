@@ -195,6 +195,14 @@ hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const floa
 // shape (the census slots their epilogue may write).
 int64_t sparse_fused_max_groups(const SparseShape &sh);
 
+// Weight gradient of Eq. 1 from the nonzero inputs (stride 1, square 1x1,
+// 3x3 or 5x5 filters): per-range sums into part (sparse_dw_workspace_floats
+// floats), then their ordered sum into dw (K x C x R x S).
+bool sparse_dw_applies(const SparseShape &sh);
+size_t sparse_dw_workspace_floats(const SparseShape &sh);
+hipError_t launch_sparse_dw(const SparseShape &sh, const float *x, const float *dy, float *dw, float *part,
+                            hipStream_t s);
+
 // Which kernel runs over compacted lists for a shape (the values are those
 // of isc_sparse_kernel in the C ABI).
 enum ListKernel : int { kListNone = 0, kListResident = 2, kListRing = 3, kListGeneric = 4 };

@@ -188,6 +188,47 @@ __device__ __forceinline__ void walk_scan(const unsigned long long (&mask)[SH::E
     static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group<SH, decltype(gc)::value * 16, 16>(mask, xv, acc, w); });
 }
 
+// The same static scan with the block of a set position supplied by the
+// caller: blk(integral_constant<WY>, integral_constant<XP>, v) for a nonzero v
+// at window row WY, shifted column XP (the weight-gradient kernel's leaves).
+template <typename SH, int Q, typename Blk>
+__device__ __forceinline__ void scan_one_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                           Blk &blk) {
+    constexpr int E = Q / kLanes, L = Q % kLanes;
+    if (__builtin_expect((mask[E] & (1ull << L)) != 0ull, 0)) {
+        const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xv[E]), L));
+        blk(std::integral_constant<int, Q / SH::WCOLS>{}, std::integral_constant<int, Q % SH::WCOLS>{}, v);
+    }
+}
+
+template <typename SH, int Q0, int G, typename Blk>
+__device__ __forceinline__ void scan_group_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                             Blk &blk) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+    if constexpr (Q0 < NQ) {
+        if constexpr (G == 1) {
+            scan_one_f<SH, Q0>(mask, xv, blk);
+        } else {
+            constexpr int E = Q0 / kLanes, L = Q0 % kLanes;
+            constexpr int N = (NQ - Q0) < G ? (NQ - Q0) : G;
+            constexpr unsigned long long gm = (N == 64 ? ~0ull : ((1ull << N) - 1)) << L;
+            if (__builtin_expect((mask[E] & gm) != 0ull, 0)) {
+                constexpr int G2 = G == 16 ? 4 : 1;
+                static_for<0, G / G2>([&](auto ic) {
+                    scan_group_f<SH, Q0 + decltype(ic)::value * G2, G2>(mask, xv, blk);
+                });
+            }
+        }
+    }
+}
+
+template <typename SH, typename Blk>
+__device__ __forceinline__ void walk_scan_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+                                            Blk &blk) {
+    constexpr int NQ = SH::WROWS * SH::WCOLS;
+    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group_f<SH, decltype(gc)::value * 16, 16>(mask, xv, blk); });
+}
+
 // Load one channel's weights for this lane: w[r][s][j] = wc[(r*S+s)*ld + lane*KPL + j]
 // (ld = KW for the ring's layout, padded for the transposed one).
 template <typename SH>
