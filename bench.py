@@ -172,6 +172,32 @@ class LayerRun:
         res["t_sparse_kernel_ms"] = kernel_time_ms(torch, self.sparse_kernel(), reps, graphs)
         return res
 
+    def measure_dw(self, steps, warmup, graphs=True):
+        """The weight gradient (training) on this layer's input with a random
+        output gradient: the zero-skipping kernel (isc_conv2d_dw, graph
+        replayed) against torch's GPU weight gradient of the same
+        convolution (the vendor library, eager), when the kernel takes the
+        shape."""
+        torch, isc, L = self.torch, self.isc, self.layer
+        try:
+            nbytes = isc.isc_conv2d_dw_workspace_size(self.desc)
+        except isc.IscError:
+            return {}
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(self.layer.seed)
+        dy = torch.randn((L.N, L.K, self.Ho, self.Wo), device="cuda", generator=gen)
+        ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
+        dw = torch.empty((L.K, L.C, L.R, L.S), device="cuda")
+        fn = lambda: isc.isc_conv2d_dw(self.x, dy, L.R, L.S, L.T, L.P, out=dw, ws=ws)
+        res = {"t_dw_sparse_ms": kernel_time_ms(torch, fn, max(20, steps), graphs, inner=5)}
+        ref = lambda: torch.nn.grad.conv2d_weight(self.x, (L.K, L.C, L.R, L.S), dy, stride=L.T, padding=L.P)
+        res["t_dw_library_ms"] = event_time_ms(torch, ref, max(20, steps), warmup)
+        res["speedup_dw_vs_library"] = round(res["t_dw_library_ms"] / res["t_dw_sparse_ms"], 3)
+        res["dw_tflops_nonzero"] = round(2 * self.nz_macs / (res["t_dw_sparse_ms"] * 1e-3) / 1e12, 3)
+        res["dw_tflops_dense_equiv"] = round(self.flops / (res["t_dw_sparse_ms"] * 1e-3) / 1e12, 3)
+        del dy, ws, dw
+        return res
+
     def summary(self, res):
         f, nzm = self.flops, self.nz_macs
         L = self.layer
@@ -550,10 +576,14 @@ def main():
                     continue
                 run = LayerRun(torch, isc, layer)
                 s = run.summary(run.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph))
+                s.update(run.measure_dw(max(20, args.steps // 4), 5, graphs=not args.no_graph))
                 rows.append(s)
-                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx" % (
+                dws = (" | dw sparse %.4f ms library %.4f (%.2fx)" % (
+                    s["t_dw_sparse_ms"], s["t_dw_library_ms"], s["speedup_dw_vs_library"])
+                       if "t_dw_sparse_ms" in s else "")
+                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx%s" % (
                     layer.name, s["t_auto_ms"], s["t_sparse_ms"], s["t_dense_ms"],
-                    s["speedup_sparse_vs_dense"]), file=sys.stderr, flush=True)
+                    s["speedup_sparse_vs_dense"], dws), file=sys.stderr, flush=True)
                 del run
                 torch.cuda.empty_cache()
         if args.out:

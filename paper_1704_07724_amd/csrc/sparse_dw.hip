@@ -19,9 +19,11 @@
 // scans it statically (tile::walk_scan_f): every set position runs a
 // straight-line block of multiply-adds whose register indices are constants.
 // The four wavefronts of a workgroup share maps and tile range and differ in
-// channels, so they load the same output gradients at about the same time
-// (cache hits after the first).  Each wavefront finally stores its sums for
-// its range; a second launch adds the ranges in order (deterministic, no
+// channels: per tile they load the output gradients of their maps once,
+// together, with consecutive lanes on consecutive columns of a map (whole
+// cache lines), and transpose them through LDS so that each lane then reads
+// its maps' values for every column.  Each wavefront finally stores its sums
+// for its range; a second launch adds the ranges in order (deterministic, no
 // atomics).
 #include "sparse_tile.hpp"
 
@@ -73,63 +75,106 @@ void sparse_dw_kernel(DwArgs a) {
 #pragma unroll
                 for (int j = 0; j < KPL; ++j) acc[ch][r][s][j] = 0.0f;
 
-    // this lane's maps (clamped: maps past K read map K-1 and get zero)
-    int krow[KPL];
+    // this lane's maps
     bool kok[KPL];
 #pragma unroll
-    for (int j = 0; j < KPL; ++j) {
-        const int k = kbase + lane * KPL + j;
-        kok[j] = k < K;
-        krow[j] = min(k, K - 1);
-    }
+    for (int j = 0; j < KPL; ++j) kok[j] = kbase + lane * KPL + j < K;
 
-    const int t0 = split * a.per;
-    const int t1 = min(a.ntiles, t0 + a.per);
-#pragma unroll 1
-    for (int t = t0; t < t1; ++t) {
+    // the tile's output gradients, [column][map] (pitch KW + 1); the
+    // cooperative load: lane l of a load covers column l % COLS of map
+    // l / COLS of a group of 64 / COLS maps
+    constexpr int KW = T::KW;
+    constexpr int COLS = TW <= 16 ? 16 : 32;
+    constexpr int MPI = kLanes / COLS;                 // maps per load
+    constexpr int NLD = KW / (MPI * kDwWaves);         // loads per wavefront per tile
+    static_assert(KW % (MPI * kDwWaves) == 0, "cooperative load");
+    static_assert(NLD <= 32, "validity bits");
+    __shared__ float gs[2][TW][KW + 1];
+    const int lcol = lane % COLS;
+    const int lmap = lane / COLS;
+
+    // the loads of one tile, issued a tile ahead: its output gradients for
+    // the cooperative load (vg: gs[ox][m] = dy[n, kbase + m, oy0, ox0 + ox],
+    // zero past the map's columns and past K) and this wavefront's channel
+    // windows (vx, element e = q*64 + lane at window row wy = e / WCOLS,
+    // input row oy0 - P + wy, shifted column xp, input column ox0 - P + xp;
+    // inw: the element lies in the map and its column reaches the tile)
+    float vg[NLD];
+    uint32_t vok = 0;  // bit i: vg[i] is a gradient of the tile (else stored as zero)
+    float vx[CH][EPL];
+    bool inw[EPL];
+    auto load_tile = [&](int t) {
         const int ct = t % a.ctiles;
         const int rest = t / a.ctiles;
         const int oy0 = rest % Ho;
         const int n = rest / Ho;
         const int ox0 = ct * a.TWr;
         const int tw = min(a.TWr, Wo - ox0);
-
-        // output gradients of the tile: g[0][ox][j] = dy[n, k_j, oy0, ox0 + ox]
-        // (zero for columns past the map and maps past K)
-        tile::Acc<T> g;
+        // every load in bounds (clamped), the validity kept aside: a select
+        // on the loaded value would let the compiler turn each load into a
+        // branch with its own wait
+        vok = 0;
 #pragma unroll
-        for (int j = 0; j < KPL; ++j) {
-            const float *row = a.dy + ((static_cast<size_t>(n) * K + krow[j]) * Ho + oy0) * Wo + ox0;
-#pragma unroll
-            for (int ox = 0; ox < TW; ++ox) {
-                const float v = row[min(ox, tw - 1)];
-                g[0][ox][j] = (kok[j] && ox < tw) ? v : 0.0f;
-            }
+        for (int i = 0; i < NLD; ++i) {
+            const int m = (wave * NLD + i) * MPI + lmap;
+            const int k = kbase + m;
+            const float *row = a.dy + ((static_cast<size_t>(n) * K + min(k, K - 1)) * Ho + oy0) * Wo + ox0;
+            vg[i] = row[min(lcol, tw - 1)];
+            vok |= (k < K && lcol < tw) ? (1u << i) : 0u;
         }
-
-        // the input window that reaches the tile: element e = q*64 + lane is
-        // window row wy = e / WCOLS (input row oy0 - P + wy), shifted column
-        // xp (input column ox0 - P + xp); only columns that reach an output
-        // of the tile, inside the map, take part
         int xoff[EPL];
-        bool inwin[EPL];
 #pragma unroll
         for (int q = 0; q < EPL; ++q) {
             const int e = q * kLanes + lane;
             const int wy = e / T::WCOLS;
             const int xp = e - wy * T::WCOLS;
             const int y = oy0 - P + wy, xx = ox0 - P + xp;
-            inwin[q] = e < T::WROWS * T::WCOLS && xp < tw + RS_ - 1 && y >= 0 && y < H && xx >= 0 && xx < W;
-            xoff[q] = inwin[q] ? y * W + xx : 0;
+            inw[q] = e < T::WROWS * T::WCOLS && xp < tw + RS_ - 1 && y >= 0 && y < H && xx >= 0 && xx < W;
+            xoff[q] = inw[q] ? y * W + xx : 0;
         }
-        float cur[CH][EPL];
         tile::static_for<0, CH>([&](auto chc) {
             constexpr int ch = decltype(chc)::value;
             const int c = min(cbase + ch, C - 1);
             const float *plane = a.x + (static_cast<size_t>(n) * C + c) * HW;
 #pragma unroll
-            for (int q = 0; q < EPL; ++q) cur[ch][q] = plane[xoff[q]];
+            for (int q = 0; q < EPL; ++q) vx[ch][q] = plane[xoff[q]];
         });
+    };
+
+    const int t0 = split * a.per;
+    const int t1 = min(a.ntiles, t0 + a.per);
+    if (t0 < t1) load_tile(t0);
+#pragma unroll 1
+    for (int t = t0; t < t1; ++t) {
+        // the tile loaded last into LDS (one buffer of two: the other one is
+        // still being read by wavefronts behind) and its windows into the
+        // working registers, then the next tile's loads go out and land
+        // while this one is scanned
+        const int buf = (t - t0) & 1;
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+            const int m = (wave * NLD + i) * MPI + lmap;
+            if (lcol < TW) gs[buf][lcol][m] = ((vok >> i) & 1u) ? vg[i] : 0.0f;
+        }
+        // the windows move to working registers by explicit moves, which the
+        // compiler cannot forward: the loaded registers are free again before
+        // the next tile's loads, so none has to be copied (after a wait for
+        // every load in flight) at the loop's back edge
+        float cur[CH][EPL];
+        bool inwin[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) inwin[q] = inw[q];
+#pragma unroll
+        for (int ch = 0; ch < CH; ++ch)
+#pragma unroll
+            for (int q = 0; q < EPL; ++q) asm volatile("v_mov_b32 %0, %1" : "=v"(cur[ch][q]) : "v"(vx[ch][q]));
+        __syncthreads();
+        if (t + 1 < t1) load_tile(t + 1);
+        tile::Acc<T> g;
+#pragma unroll
+        for (int ox = 0; ox < TW; ++ox)
+#pragma unroll
+            for (int j = 0; j < KPL; ++j) g[0][ox][j] = gs[buf][ox][lane * KPL + j];
 
         // per channel: ballot of the zero test, static scan of the window
         tile::static_for<0, CH>([&](auto chc) {
