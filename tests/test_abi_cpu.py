@@ -217,3 +217,28 @@ def test_census_read_validation():
     e, n = ctypes.c_uint64(), ctypes.c_uint64()
     assert L.isc_census_read(None, 4096, ctypes.byref(e), ctypes.byref(n), None) == 1
     assert L.isc_census_read(0x1000, 8, ctypes.byref(e), ctypes.byref(n), None) == 4
+
+
+def test_dw_entry_validation():
+    L = isc.lib()
+    d = isc.make_desc(2, 3, 9, 9, 8, 3, 3, 1, 1)
+    n = isc.isc_conv2d_dw_workspace_size(d)
+    assert n > 0 and n % 256 == 0
+    with pytest.raises(isc.IscError) as e:                      # stride 2: not taken
+        isc.isc_conv2d_dw_workspace_size(isc.make_desc(2, 3, 9, 9, 8, 3, 3, 2, 1))
+    assert e.value.status == 3
+    with pytest.raises(isc.IscError) as e:                      # 7x7 filter: not taken
+        isc.isc_conv2d_dw_workspace_size(isc.make_desc(2, 3, 9, 9, 8, 7, 7, 1, 3))
+    assert e.value.status == 3
+    x, dy, dw, ws = 0x1000, 0x100000, 0x200000, 0x300000
+    assert L.isc_conv2d_dw(ctypes.byref(d), None, dy, dw, ws, n, None) == 1
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n - 1, None) == 4    # workspace too small
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, x, ws, n, None) == 5        # dw overlaps x
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws + 16, n, None) == 9  # workspace misaligned
+    try:
+        import torch
+        if torch.cuda.is_available():
+            return
+    except Exception:
+        pass
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n, None) == 7       # no gfx950 here
