@@ -446,7 +446,7 @@ int isc_conv2d_dw(const isc_conv_desc *d, const float *x, const float *dy, float
     if (!aligned(x, 4) || !aligned(dy, 4) || !aligned(dw, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
     const isc::SparseShape sh = sparse_shape(s);
     if (!isc::sparse_dw_applies(sh)) return ISC_ERR_LIMIT;
-    const size_t need = sizeof(float) * isc::sparse_dw_workspace_floats(sh);
+    const size_t need = align_up(sizeof(float) * isc::sparse_dw_workspace_floats(sh), kAlign);
     if (ws_bytes < need) return ISC_ERR_WORKSPACE;
     const size_t xb = sizeof(float) * static_cast<size_t>(s.in_elems());
     const size_t yb = sizeof(float) * static_cast<size_t>(s.out_elems());
