@@ -19,30 +19,44 @@ void dw_reduce_kernel(const float *__restrict__ part, int splits, int64_t n, flo
     dw[e] = s;
 }
 
-// Maps per lane: two -- measured fastest or within a few percent of it on
-// every workload layer, K <= 64 included: each scanned nonzero feeds twice
-// the multiply-adds, which outweighs lanes past K.  ISC_DW_KPL = 1, 2 or 4
-// fixes it (for measurements; four only with 16-column tiles).
-int dw_kpl(const SparseShape &sh) {
+// Tile rows and maps per lane (measured on every workload layer):
+//  - 3x3 filters: one-row tiles, two maps per lane;
+//  - 5x5 and 1x1 filters: two-row tiles (each scanned nonzero feeds two
+//    output rows), two maps per lane -- one when K > 64 with 5x5 filters,
+//    which keeps three channels per wavefront instead of one.
+// ISC_DW_KPL (1, 2, 4) and ISC_DW_TH (1, 2) override the choice, for
+// measurements (four maps per lane only with one-row 16-column tiles, two
+// rows only with one or two maps per lane).
+int dw_th(const SparseShape &sh) {
+    if (const char *env = std::getenv("ISC_DW_TH")) {
+        const int t = std::atoi(env);
+        if (t == 1 || t == 2) return t;
+    }
+    return sh.R == 3 ? 1 : 2;
+}
+
+int dw_kpl(const SparseShape &sh, int th) {
     if (const char *env = std::getenv("ISC_DW_KPL")) {
         const int k = std::atoi(env);
-        if (k == 1 || k == 2 || (k == 4 && sh.Wo <= 16)) return k;
+        if ((k == 1 || k == 2) || (k == 4 && th == 1 && sh.Wo <= 16)) return k;
     }
-    return 2;
+    return sh.R == 5 && sh.K > kLanes ? 1 : 2;
 }
 int dw_tw(int Wo) { return Wo <= 16 ? 16 : 28; }
 
 bool dw_plan(const SparseShape &sh, DwPlan *p) {
     if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
-    p->kpl = dw_kpl(sh);
-    p->ch = dw_ch_for(sh.R, p->kpl);
-    p->tw = dw_tw(sh.Wo);
+    p->th = dw_th(sh);
+    p->kpl = dw_kpl(sh, p->th);
+    p->ch = dw_ch_for(sh.R, p->kpl, p->th);
+    p->tw = p->th == 2 ? 16 : dw_tw(sh.Wo);
     p->TWr = std::min(p->tw, sh.Wo);
     p->ctiles = (sh.Wo + p->TWr - 1) / p->TWr;
+    p->bands = (sh.Ho + p->th - 1) / p->th;
     p->kgroups = (sh.K + kLanes * p->kpl - 1) / (kLanes * p->kpl);
     const int cgroups = (sh.C + p->ch - 1) / p->ch;
     p->cquads = (cgroups + kDwWaves - 1) / kDwWaves;
-    const int64_t ntiles = static_cast<int64_t>(sh.N) * sh.Ho * p->ctiles;
+    const int64_t ntiles = static_cast<int64_t>(sh.N) * p->bands * p->ctiles;
     if (ntiles > (1ll << 30)) return false;
     p->ntiles = static_cast<int>(ntiles);
     const int64_t base = static_cast<int64_t>(p->kgroups) * p->cquads;
@@ -78,6 +92,7 @@ hipError_t launch_sparse_dw(const SparseShape &sh, const float *x, const float *
     a.N = sh.N; a.C = sh.C; a.H = sh.H; a.W = sh.W; a.K = sh.K; a.P = sh.P; a.Ho = sh.Ho; a.Wo = sh.Wo;
     a.TWr = p.TWr;
     a.ctiles = p.ctiles;
+    a.bands = p.bands;
     a.cquads = p.cquads;
     a.splits = p.splits;
     a.per = p.per;

@@ -15,10 +15,10 @@
 // the K-contiguous gradient vector dw[:, c, r, s].
 //
 // A wavefront owns 64*KPL output maps (lanes over maps, as in the forward
-// kernels), CH input channels and a contiguous range of output tiles (one
-// output row, TW columns, one image each).  It keeps the CH*R*S*KPL
+// kernels), CH input channels and a contiguous range of output tiles (TH
+// output rows, TW columns, one image each).  It keeps the CH*R*S*KPL
 // gradient sums in registers for the whole range; per tile it loads the
-// tile's output gradients for its maps (TW*KPL registers) and, per channel,
+// tile's output gradients for its maps (TH*TW*KPL registers) and, per channel,
 // the input window that reaches the tile, takes a ballot of the zero test and
 // scans it statically (tile::walk_scan_f): every set position runs a
 // straight-line block of multiply-adds whose register indices are constants.
@@ -47,19 +47,24 @@ struct DwArgs {
     float *part;       // [splits][K][C*R*S]: sums of each tile range
     int N, C, H, W, K, P, Ho, Wo;
     int TWr, ctiles;   // output columns per tile in use, column tiles per row
+    int bands;         // groups of TH output rows
     int cquads;        // groups of kDwWaves * CH channels
     int splits, per;   // tile ranges, tiles per range
-    int ntiles;        // N * Ho * ctiles
+    int ntiles;        // N * bands * ctiles
 };
 
 struct DwPlan {
-    int kpl, ch, tw, TWr, ctiles, kgroups, cquads, splits, per, ntiles;
+    int kpl, th, ch, tw, TWr, ctiles, bands, kgroups, cquads, splits, per, ntiles;
 };
 
 // Channels per wavefront for a filter size and maps per lane: as many as
 // kDwMaxRegs gradient sums allow, at most 16.
-constexpr int dw_ch_for(int RS, int KPL) {
-    return kDwMaxRegs / (RS * RS * KPL) < 16 ? kDwMaxRegs / (RS * RS * KPL) : 16;
+// Two-row tiles hold twice the output gradients: the channels are cut so
+// that gradient sums and gradients together stay within the same budget.
+constexpr int dw_ch_for(int RS, int KPL, int TH = 1) {
+    const int room = kDwMaxRegs - (TH - 1) * 16 * KPL * 3 / 4;
+    const int ch = room / (RS * RS * KPL);
+    return ch < 1 ? 1 : (ch < 16 ? ch : 16);
 }
 
 // Launchers of the kernels of one filter size (sparse_dw_r{1,3,5}.hip).
@@ -75,10 +80,10 @@ namespace isc {
 namespace dwk {
 namespace {
 
-template <int RS_, int KPL, int TW, int CH>
+template <int RS_, int KPL, int TH, int TW, int CH>
 __global__ __launch_bounds__(kDwWaves * kLanes)
 void sparse_dw_kernel(DwArgs a) {
-    using T = tile::Shape<RS_, RS_, KPL, 1, TW>;
+    using T = tile::Shape<RS_, RS_, KPL, TH, TW>;
     constexpr int EPL = T::EPL, RS2 = RS_ * RS_;
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
@@ -107,22 +112,23 @@ void sparse_dw_kernel(DwArgs a) {
 #pragma unroll
     for (int j = 0; j < KPL; ++j) kok[j] = kbase + lane * KPL + j < K;
 
-    // the tile's output gradients, [column][map] (pitch KW + 1); the
-    // cooperative load: lane l of a load covers column l % COLS of map
-    // l / COLS of a group of 64 / COLS maps
+    // the tile's output gradients, [row * TW + column][map] (pitch KW + 1);
+    // the cooperative load: load i of the workgroup covers one row of 64 /
+    // COLS maps, lane l column l % COLS of map l / COLS
     constexpr int KW = T::KW;
     constexpr int COLS = TW <= 16 ? 16 : 32;
     constexpr int MPI = kLanes / COLS;                 // maps per load
-    constexpr int NLD = KW / (MPI * kDwWaves);         // loads per wavefront per tile
-    static_assert(KW % (MPI * kDwWaves) == 0, "cooperative load");
+    constexpr int GPR = KW / MPI;                      // loads per tile row
+    constexpr int NLD = TH * GPR / kDwWaves;           // loads per wavefront per tile
+    static_assert((TH * GPR) % kDwWaves == 0, "cooperative load");
     static_assert(NLD <= 32, "validity bits");
-    __shared__ float gs[2][TW][KW + 1];
+    __shared__ float gs[2][TH * TW][KW + 1];
     const int lcol = lane % COLS;
     const int lmap = lane / COLS;
 
     // the loads of one tile, issued a tile ahead: its output gradients for
-    // the cooperative load (vg: gs[ox][m] = dy[n, kbase + m, oy0, ox0 + ox],
-    // zero past the map's columns and past K) and this wavefront's channel
+    // the cooperative load (vg: gs[hr * TW + ox][m] = dy[n, kbase + m,
+    // oy0 + hr, ox0 + ox], zero past the map and past K) and this wavefront's channel
     // windows (vx, element e = q*64 + lane at window row wy = e / WCOLS,
     // input row oy0 - P + wy, shifted column xp, input column ox0 - P + xp;
     // inw: the element lies in the map and its column reaches the tile)
@@ -133,8 +139,8 @@ void sparse_dw_kernel(DwArgs a) {
     auto load_tile = [&](int t) {
         const int ct = t % a.ctiles;
         const int rest = t / a.ctiles;
-        const int oy0 = rest % Ho;
-        const int n = rest / Ho;
+        const int oy0 = (rest % a.bands) * TH;
+        const int n = rest / a.bands;
         const int ox0 = ct * a.TWr;
         const int tw = min(a.TWr, Wo - ox0);
         // every load in bounds (clamped), the validity kept aside: a select
@@ -143,11 +149,15 @@ void sparse_dw_kernel(DwArgs a) {
         vok = 0;
 #pragma unroll
         for (int i = 0; i < NLD; ++i) {
-            const int m = (wave * NLD + i) * MPI + lmap;
+            const int li = wave * NLD + i;
+            const int hr = li / GPR;
+            const int m = (li - hr * GPR) * MPI + lmap;
             const int k = kbase + m;
-            const float *row = a.dy + ((static_cast<size_t>(n) * K + min(k, K - 1)) * Ho + oy0) * Wo + ox0;
+            const int oy = oy0 + hr;
+            const float *row =
+                a.dy + ((static_cast<size_t>(n) * K + min(k, K - 1)) * Ho + min(oy, Ho - 1)) * Wo + ox0;
             vg[i] = row[min(lcol, tw - 1)];
-            vok |= (k < K && lcol < tw) ? (1u << i) : 0u;
+            vok |= (k < K && lcol < tw && oy < Ho) ? (1u << i) : 0u;
         }
         int xoff[EPL];
 #pragma unroll
@@ -180,8 +190,10 @@ void sparse_dw_kernel(DwArgs a) {
         const int buf = (t - t0) & 1;
 #pragma unroll
         for (int i = 0; i < NLD; ++i) {
-            const int m = (wave * NLD + i) * MPI + lmap;
-            if (lcol < TW) gs[buf][lcol][m] = ((vok >> i) & 1u) ? vg[i] : 0.0f;
+            const int li = wave * NLD + i;
+            const int hr = li / GPR;
+            const int m = (li - hr * GPR) * MPI + lmap;
+            if (lcol < TW) gs[buf][hr * TW + lcol][m] = ((vok >> i) & 1u) ? vg[i] : 0.0f;
         }
         // the windows move to working registers by explicit moves, which the
         // compiler cannot forward: the loaded registers are free again before
@@ -199,9 +211,11 @@ void sparse_dw_kernel(DwArgs a) {
         if (t + 1 < t1) load_tile(t + 1);
         tile::Acc<T> g;
 #pragma unroll
-        for (int ox = 0; ox < TW; ++ox)
+        for (int oy = 0; oy < TH; ++oy)
 #pragma unroll
-            for (int j = 0; j < KPL; ++j) g[0][ox][j] = gs[buf][ox][lane * KPL + j];
+            for (int ox = 0; ox < TW; ++ox)
+#pragma unroll
+                for (int j = 0; j < KPL; ++j) g[oy][ox][j] = gs[buf][oy * TW + ox][lane * KPL + j];
 
         // per channel: ballot of the zero test, static scan of the window
         tile::static_for<0, CH>([&](auto chc) {
@@ -211,16 +225,21 @@ void sparse_dw_kernel(DwArgs a) {
 #pragma unroll
                 for (int q = 0; q < EPL; ++q)
                     mask[q] = __ballot(inwin[q] && (__float_as_uint(cur[ch][q]) & 0x7fffffffu) != 0u);
-                // one output row: the tap row is r = WY; the tap column s
-                // reaches output column XP - s when it lies in the tile
+                // tap (r, s) reaches output (WY - r, XP - s) when it lies in
+                // the tile
                 auto blk = [&](auto wy_c, auto xp_c, float v) {
                     constexpr int WY = decltype(wy_c)::value, XP = decltype(xp_c)::value;
-                    tile::static_for<0, RS_>([&](auto sc) {
-                        constexpr int sx = decltype(sc)::value, ox = XP - sx;
-                        if constexpr (ox >= 0 && ox < TW) {
+                    tile::static_for<0, RS_>([&](auto rc) {
+                        constexpr int r = decltype(rc)::value, oy = WY - r;
+                        if constexpr (oy >= 0 && oy < TH) {
+                            tile::static_for<0, RS_>([&](auto sc) {
+                                constexpr int sx = decltype(sc)::value, ox = XP - sx;
+                                if constexpr (ox >= 0 && ox < TW) {
 #pragma unroll
-                            for (int j = 0; j < KPL; ++j)
-                                acc[ch][WY][sx][j] = __builtin_fmaf(v, g[0][ox][j], acc[ch][WY][sx][j]);
+                                    for (int j = 0; j < KPL; ++j)
+                                        acc[ch][r][sx][j] = __builtin_fmaf(v, g[oy][ox][j], acc[ch][r][sx][j]);
+                                }
+                            });
                         }
                     });
                 };
@@ -249,22 +268,29 @@ void sparse_dw_kernel(DwArgs a) {
     });
 }
 
-template <int RS_, int KPL, int TW>
-hipError_t launch_dw_t(const DwArgs &a, int kgroups, hipStream_t s) {
-    constexpr int CH = dw_ch_for(RS_, KPL);
+template <int RS_, int KPL, int TH, int TW>
+hipError_t launch_dw_t(const DwArgs &a, const DwPlan &p, hipStream_t s) {
+    constexpr int CH = dw_ch_for(RS_, KPL, TH);
     static_assert(CH >= 1 && CH * RS_ * RS_ * KPL <= kDwMaxRegs, "gradient sums");
-    const int64_t grid = static_cast<int64_t>(kgroups) * a.splits * a.cquads;
-    sparse_dw_kernel<RS_, KPL, TW, CH><<<static_cast<unsigned>(grid), kDwWaves * kLanes, 0, s>>>(a);
+    if (p.ch != CH) return hipErrorInvalidValue;
+    const int64_t grid = static_cast<int64_t>(p.kgroups) * a.splits * a.cquads;
+    sparse_dw_kernel<RS_, KPL, TH, TW, CH><<<static_cast<unsigned>(grid), kDwWaves * kLanes, 0, s>>>(a);
     return hipGetLastError();
 }
 
-// 16- or 28-column tiles; four maps per lane only with 16-column tiles.
+// One-row tiles of 16 or 28 columns with 1, 2 or 4 maps per lane (four
+// only with 16 columns); two-row tiles of 16 columns with 1 or 2.
 template <int RS_>
 hipError_t launch_dw_rs(const DwArgs &a, const DwPlan &p, hipStream_t s) {
+    if (p.th == 2) {
+        if (p.tw != 16) return hipErrorInvalidValue;
+        return p.kpl == 1 ? launch_dw_t<RS_, 1, 2, 16>(a, p, s)
+                          : (p.kpl == 2 ? launch_dw_t<RS_, 2, 2, 16>(a, p, s) : hipErrorInvalidValue);
+    }
     switch (p.kpl) {
-    case 1: return p.tw == 16 ? launch_dw_t<RS_, 1, 16>(a, p.kgroups, s) : launch_dw_t<RS_, 1, 28>(a, p.kgroups, s);
-    case 2: return p.tw == 16 ? launch_dw_t<RS_, 2, 16>(a, p.kgroups, s) : launch_dw_t<RS_, 2, 28>(a, p.kgroups, s);
-    default: return p.tw == 16 ? launch_dw_t<RS_, 4, 16>(a, p.kgroups, s) : hipErrorInvalidValue;
+    case 1: return p.tw == 16 ? launch_dw_t<RS_, 1, 1, 16>(a, p, s) : launch_dw_t<RS_, 1, 1, 28>(a, p, s);
+    case 2: return p.tw == 16 ? launch_dw_t<RS_, 2, 1, 16>(a, p, s) : launch_dw_t<RS_, 2, 1, 28>(a, p, s);
+    default: return p.tw == 16 ? launch_dw_t<RS_, 4, 1, 16>(a, p, s) : hipErrorInvalidValue;
     }
 }
 

@@ -127,3 +127,22 @@ def test_dw_full_size_sampled(torch, isc):
     want = oracle.conv2d_dw_f64(np.ascontiguousarray(x[:, cs]), np.ascontiguousarray(dy[:, ks]), layer.R, layer.S, 1,
                                 layer.P)
     assert_close(got[np.ix_(ks, cs)], want, "dw full size")
+
+
+@pytest.mark.parametrize("R,W", [(1, 13), (3, 13), (3, 30), (5, 11), (5, 27)])
+def test_dw_every_tile_variant(torch, isc, monkeypatch, R, W):
+    """Every compiled tile (rows per tile, maps per lane, 16- or 28-column
+    tiles), forced through the measurement overrides, against the oracle on
+    ragged maps and channels."""
+    N, C, H, K, P = 2, 9, 10, 70, R // 2
+    x, _ = workloads.make_case(N, C, H, W, K, R, R, 1, P, 0.8, seed=61 + R + W)
+    Ho, Wo = oracle.out_size(H, R, P, 1), oracle.out_size(W, R, P, 1)
+    dy = _dy((N, K, Ho, Wo), 62 + R + W)
+    want = oracle.conv2d_dw_f64(x, dy, R, R, 1, P)
+    variants = [(1, 1), (2, 1), (1, 2), (2, 2)] + ([(4, 1)] if Wo <= 16 else [])
+    for kpl, th in variants:
+        note("dw variant", R, W, "kpl", kpl, "th", th)
+        monkeypatch.setenv("ISC_DW_KPL", str(kpl))
+        monkeypatch.setenv("ISC_DW_TH", str(th))
+        got = isc.isc_conv2d_dw(to_dev(torch, x), to_dev(torch, dy), R, R, 1, P).cpu().numpy()
+        assert_close(got, want, "dw R%d W%d kpl%d th%d" % (R, W, kpl, th))
