@@ -241,8 +241,9 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
  *   y: device output N x K x Ho x Wo, fully written, must not overlap x or
  *     wt.
  * Deterministic (fixed summation order per output).  Errors: NULL, SHAPE,
- * LIMIT (shape not eligible: stride 1 and a square 1x1, 3x3 or 5x5 filter
- * are required), ALIAS, ALIGN, DEVICE, HIP. */
+ * LIMIT (shape not eligible: a square 1x1, 3x3 or 5x5 filter at stride 1,
+ * or a 3x3 or 5x5 filter at stride 2 with K <= 64, a filter that fits in LDS
+ * and at most 8 output columns), ALIAS, ALIGN, DEVICE, HIP. */
 int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y,
                           void *stream);
 

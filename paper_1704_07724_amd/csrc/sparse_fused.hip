@@ -15,14 +15,16 @@ size_t fused_lds(int crs, int th, int tw) {
     return std::max(sizeof(float) * crs * kWPitch, sizeof(float) * kWaves * th * tw * kRPad);
 }
 
-// The filter must fit in LDS.  Tile height and channel phases: the tallest
+// The filter must fit in LDS; stride 1, or stride 2 with 3x3 or 5x5 filters
+// and at most 8 output columns.  Tile height and channel phases: the tallest
 // tile (up to kMaxTile accumulators per lane), then the fewest phases that
 // leave no row group of a workgroup idle (rg <= ceil(Ho / TH)), preferring
 // plans with at least kMinGroups workgroups; else the plan with most
 // workgroups.  ISC_FUSED_TH caps the tile height and ISC_FUSED_CS fixes the
 // phases (for measurements).
 bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
-    if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
+    if (sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
+    if (!(sh.T == 1 || (sh.T == 2 && sh.R > 1 && sh.Wo <= 8))) return false;
     if (sh.Wo > 28 || sh.K > kLanes) return false;
     const int crs = sh.C * sh.R * sh.S;
     if (static_cast<size_t>(crs) * kWPitch * sizeof(float) > kLdsMax) return false;
@@ -43,7 +45,7 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
             const size_t lds = fused_lds(crs, th, tw);
             if (lds > kLdsMax) continue;
             if (!found || groups > best_groups) {
-                *plan = FusedPlan{th, tw, cs, lds};
+                *plan = FusedPlan{th, tw, cs, lds, sh.T};
                 best_groups = groups;
                 found = true;
             }

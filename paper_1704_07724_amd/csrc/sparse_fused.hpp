@@ -56,6 +56,7 @@ struct FusedArgs {
 struct FusedPlan {
     int th, tw, cs;
     size_t lds;
+    int st;  // stride (1, or 2 with 8-column tiles)
 };
 
 // Launchers of the kernels of one filter size (sparse_fused_r{1,3,5}.hip).
@@ -71,10 +72,10 @@ namespace isc {
 namespace fused {
 namespace {
 
-template <int RS_, int TH, int TW>
+template <int RS_, int TH, int TW, int ST>
 __global__ __launch_bounds__(kWaves * kLanes)
 void sparse_conv_fused_kernel(FusedArgs a) {
-    using T = tile::Shape<RS_, RS_, 1, TH, TW>;
+    using T = tile::Shape<RS_, RS_, 1, TH, TW, ST>;
     constexpr int RS2 = RS_ * RS_, EPL = T::EPL;
     constexpr int NS = 4;  // input-window register ring
 
@@ -99,7 +100,7 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     const int ncw = phase < C ? (C - 1 - phase) / cs + 1 : 0;
 
     // lane l of register q holds window element e = q*64 + l in leaf-key
-    // order, e = wy * WCOLS + xp: input row oy0 - P + wy, column xp - P.
+    // order, e = wy * WCOLS + xp: input row oy0*ST - P + wy, column xp - P.
     // Elements outside the map (padding) or past the window read the plane's
     // first element and never count as nonzero.
     int xoff[EPL];
@@ -108,7 +109,7 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     for (int q = 0; q < EPL; ++q) {
         const int e = q * kLanes + lane;
         const int wy = e / T::WCOLS;
-        const int y = oy0 - P + wy, xx = e - wy * T::WCOLS - P;
+        const int y = oy0 * ST - P + wy, xx = e - wy * T::WCOLS - P;
         inwin[q] = rows_ok && e < T::WROWS * T::WCOLS && y >= 0 && y < H && xx >= 0 && xx < W;
         xoff[q] = inwin[q] ? y * W + xx : 0;
     }
@@ -229,12 +230,12 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     }
 }
 
-template <int RS_, int TH, int TW>
+template <int RS_, int TH, int TW, int ST>
 hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
     if constexpr (TH * TW > kMaxTile) {
         return hipErrorInvalidValue;
     } else {
-        auto kern = sparse_conv_fused_kernel<RS_, TH, TW>;
+        auto kern = sparse_conv_fused_kernel<RS_, TH, TW, ST>;
         if (lds > 64 * 1024) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
@@ -247,22 +248,31 @@ hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
     }
 }
 
-template <int RS_, int TW>
+template <int RS_, int TW, int ST>
 hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s) {
     switch (th) {
-    case 8: return launch_fused_t<RS_, 8, TW>(a, lds, s);
-    case 4: return launch_fused_t<RS_, 4, TW>(a, lds, s);
-    case 2: return launch_fused_t<RS_, 2, TW>(a, lds, s);
-    default: return launch_fused_t<RS_, 1, TW>(a, lds, s);
+    case 8: return launch_fused_t<RS_, 8, TW, ST>(a, lds, s);
+    case 4: return launch_fused_t<RS_, 4, TW, ST>(a, lds, s);
+    case 2: return launch_fused_t<RS_, 2, TW, ST>(a, lds, s);
+    default: return launch_fused_t<RS_, 1, TW, ST>(a, lds, s);
     }
 }
 
+// Stride 1 with 8-, 16- or 28-column tiles; stride 2 with 8-column tiles
+// (3x3 and 5x5 filters).
 template <int RS_>
 hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
+    if (p.st == 2) {
+        if constexpr (RS_ == 1) {
+            return hipErrorInvalidValue;
+        } else {
+            return p.tw == 8 ? launch_fused_th<RS_, 8, 2>(a, p.th, p.lds, s) : hipErrorInvalidValue;
+        }
+    }
     switch (p.tw) {
-    case 8: return launch_fused_th<RS_, 8>(a, p.th, p.lds, s);
-    case 16: return launch_fused_th<RS_, 16>(a, p.th, p.lds, s);
-    default: return launch_fused_th<RS_, 28>(a, p.th, p.lds, s);
+    case 8: return launch_fused_th<RS_, 8, 1>(a, p.th, p.lds, s);
+    case 16: return launch_fused_th<RS_, 16, 1>(a, p.th, p.lds, s);
+    default: return launch_fused_th<RS_, 28, 1>(a, p.th, p.lds, s);
     }
 }
 

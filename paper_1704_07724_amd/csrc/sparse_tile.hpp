@@ -24,12 +24,13 @@ namespace tile {
 
 constexpr int kLanes = 64;
 
-template <int R_, int S_, int KPL_, int TH_, int TW_>
+// T_: the convolution's stride (output row oy reads input rows oy*T + r).
+template <int R_, int S_, int KPL_, int TH_, int TW_, int T_ = 1>
 struct Shape {
-    static constexpr int R = R_, S = S_, KPL = KPL_, TH = TH_, TW = TW_;
-    static constexpr int KW = kLanes * KPL;     // output maps per wavefront
-    static constexpr int WROWS = TH + R - 1;    // input rows the tile sees
-    static constexpr int WCOLS = TW + S - 1;    // shifted input columns it sees
+    static constexpr int R = R_, S = S_, KPL = KPL_, TH = TH_, TW = TW_, T = T_;
+    static constexpr int KW = kLanes * KPL;           // output maps per wavefront
+    static constexpr int WROWS = (TH - 1) * T + R;    // input rows the tile sees
+    static constexpr int WCOLS = (TW - 1) * T + S;    // shifted input columns it sees
     // list entries of the tile's window, staged kLanes per register
     static constexpr int EPL = (WROWS * WCOLS + kLanes - 1) / kLanes;
 };
@@ -47,17 +48,20 @@ using Acc = float[SH::TH][SH::TW][SH::KPL];
 template <typename SH>
 using Wts = float[SH::R][SH::S][SH::KPL];
 
-// Straight-line block for a nonzero at window row WY, shifted column XP.
+// Straight-line block for a nonzero at window row WY, shifted column XP:
+// tap (r, s) reaches output ((WY - r) / T, (XP - s) / T) when both divide.
 template <typename SH, int WY, int XP>
 __device__ __forceinline__ void leaf(Acc<SH> &acc, const Wts<SH> &w, float v) {
 #pragma unroll
     for (int r = 0; r < SH::R; ++r) {
-        const int oy = WY - r;
-        if (oy < 0 || oy >= SH::TH) continue;
+        const int dy = WY - r;
+        if (dy < 0 || dy % SH::T != 0 || dy / SH::T >= SH::TH) continue;
+        const int oy = dy / SH::T;
 #pragma unroll
         for (int s = 0; s < SH::S; ++s) {
-            const int ox = XP - s;
-            if (ox < 0 || ox >= SH::TW) continue;
+            const int dx = XP - s;
+            if (dx < 0 || dx % SH::T != 0 || dx / SH::T >= SH::TW) continue;
+            const int ox = dx / SH::T;
 #pragma unroll
             for (int j = 0; j < SH::KPL; ++j) acc[oy][ox][j] = __builtin_fmaf(v, w[r][s][j], acc[oy][ox][j]);
         }

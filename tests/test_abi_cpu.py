@@ -146,7 +146,10 @@ def test_sparse_kernel_choice(monkeypatch):
     assert isc.isc_sparse_kernel(d(128, 384, 13, 13, 256, 3, 3, 1, 1)) == "fused_ring"  # AlexNet conv5
     assert isc.isc_sparse_kernel(d(128, 96, 28, 28, 128, 3, 3, 1, 1)) == "fused_ring"  # inception 3x3
     assert isc.isc_sparse_kernel(d(1, 3, 20, 200, 66, 3, 3, 1, 1)) == "fused_ring"     # column tiles
-    assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 64, 5, 5, 2, 1)) == "generic"     # stride 2
+    assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 64, 5, 5, 2, 1)) == "fused"       # stride 2, 5 x 5 output
+    assert isc.isc_sparse_kernel(d(128, 20, 11, 11, 64, 5, 5, 2, 1)) == "fused"    # LeNet conv2 of Tab. 2
+    assert isc.isc_sparse_kernel(d(2, 4, 21, 21, 64, 5, 5, 2, 1)) == "generic"     # stride 2, 10 columns
+    assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 65, 5, 5, 2, 1)) == "generic"     # stride 2, K > 64
     assert isc.isc_sparse_kernel(d(1, 3, 10, 9, 9, 2, 3, 1, 1)) == "generic"       # 2 x 3 filter
     assert isc.isc_sparse_kernel(d(1, 3, 9, 9, 9, 7, 7, 1, 3)) == "generic"        # 7 x 7 filter
 
@@ -155,7 +158,7 @@ def test_fused_entry_validation():
     L = isc.lib()
     ok = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 1, 0)
     big_k = isc.make_desc(1, 2, 12, 12, 65, 7, 7, 1, 0)       # 7 x 7 filter: not taken
-    strided = isc.make_desc(1, 2, 12, 12, 8, 5, 5, 2, 0)      # stride 2: not taken
+    strided = isc.make_desc(1, 2, 24, 24, 8, 5, 5, 2, 0)      # stride 2 with 10 output columns: not taken
     x, w, y = 0x1000, 0x200000, 0x400000
     assert L.isc_sparse_conv_fused(None, x, w, y, None) == 1
     assert L.isc_sparse_conv_fused(ctypes.byref(ok), None, w, y, None) == 1

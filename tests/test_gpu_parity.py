@@ -413,6 +413,11 @@ FUSED_CASES = [c for c in CONV_CASES if c[7] == 1 and c[5] == c[6] and c[5] in (
     (1, 4, 9, 70, 96, 5, 5, 1, 2, 0.8),       # column tiles, ragged last tile
     (3, 3, 6, 6, 130, 1, 1, 1, 0, 0.7),       # 1x1
     (1, 300, 5, 5, 20, 5, 5, 1, 2, 0.9),      # filter of 64 maps larger than LDS
+    # stride 2 (filter resident, at most 8 output columns)
+    (3, 20, 11, 11, 64, 5, 5, 2, 1, 0.95),    # LeNet conv2 of Tab. 2
+    (2, 7, 16, 15, 33, 5, 5, 2, 2, 0.8),      # 8 x 8 output, ragged columns
+    (2, 9, 12, 9, 40, 3, 3, 2, 1, 0.9),       # 3 x 3, 6 x 5 output
+    (1, 3, 4, 4, 5, 3, 3, 2, 0, 0.5),         # 1 x 1 output
 ]
 
 

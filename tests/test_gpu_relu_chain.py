@@ -76,7 +76,8 @@ RELU_CASES = [
     (2, 11, 13, 13, 384, 3, 3, 1, 1, 0.95, "fused_ring"),   # conv3/4-like, filter streamed
     (1, 7, 13, 13, 200, 3, 3, 1, 1, 0.9, "fused_ring"),     # ragged last map group
     (1, 4, 9, 70, 96, 5, 5, 1, 2, 0.8, "fused_ring"),       # column tiles, ragged last tile
-    (2, 4, 11, 11, 64, 5, 5, 2, 1, 0.8, "generic"),         # stride 2: lists, then the epilogue pass
+    (2, 4, 11, 11, 64, 5, 5, 2, 1, 0.8, "fused"),           # stride 2, filter resident
+    (2, 4, 21, 21, 64, 5, 5, 2, 1, 0.8, "generic"),         # stride 2, 10 columns: lists, then the epilogue pass
     (1, 3, 10, 9, 9, 2, 3, 1, 1, 0.7, "generic"),           # 2 x 3 filter
 ]
 
