@@ -145,7 +145,7 @@ class LayerRun:
         on-the-fly compaction (isc_sparse_conv_fused) or the kernel over
         compacted lists (isc_sparse_conv)."""
         L = self.layer
-        if self.kernel in ("fused", "fused_ring"):
+        if self.kernel in ("fused", "fused_ring", "fused_reg"):
             return lambda: self.isc.isc_sparse_conv_fused(self.x, self.wt, L.T, L.P, out=self.y)
         return lambda: self.isc.isc_sparse_conv(self.x.shape, self.lists, self.wt, L.T, L.P,
                                                 out=self.y)
@@ -402,7 +402,7 @@ def algorithmic_bytes(run) -> dict:
     w_bytes = L.K * L.C * L.R * L.S * 4
     kp = (L.K + 63) // 64 * 64
     wt_bytes = L.C * L.R * L.S * kp * 4
-    if run.kernel in ("fused", "fused_ring"):   # reads x and the repacked filter once, writes y
+    if run.kernel in ("fused", "fused_reg", "fused_ring"):   # reads x and the repacked filter once, writes y
         sparse = x_bytes + wt_bytes + y_bytes
         prep = x_bytes + w_bytes + wt_bytes
     else:                                        # lists, row offsets, repacked filter; writes y

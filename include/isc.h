@@ -248,8 +248,11 @@ int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w
                           void *stream);
 
 /* Which kernel isc_conv2d's sparse path runs for this descriptor, reported in
- * *kernel: ISC_KERNEL_FUSED or ISC_KERNEL_FUSED_RING (compaction on the fly,
- * isc_sparse_conv_fused; filter resident in or streamed through LDS), else
+ * *kernel: ISC_KERNEL_FUSED, ISC_KERNEL_FUSED_REG or ISC_KERNEL_FUSED_RING
+ * (compaction on the fly, isc_sparse_conv_fused; filter resident in LDS,
+ * each wavefront's own channels' weights streamed to registers -- for plans
+ * whose wavefronts share no input channel, at stride 1 and at most 8 output
+ * columns -- or filter streamed through LDS), else
  * the kernel over compacted lists that isc_sparse_conv also runs:
  * ISC_KERNEL_RESIDENT (filter resident in LDS), ISC_KERNEL_RING (filter
  * streamed through LDS) or ISC_KERNEL_GENERIC (any filter and stride);
@@ -261,7 +264,8 @@ enum isc_kernel {
     ISC_KERNEL_RESIDENT = 2,
     ISC_KERNEL_RING = 3,
     ISC_KERNEL_GENERIC = 4,
-    ISC_KERNEL_FUSED_RING = 5
+    ISC_KERNEL_FUSED_RING = 5,
+    ISC_KERNEL_FUSED_REG = 6
 };
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel);
 

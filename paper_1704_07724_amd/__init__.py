@@ -350,7 +350,7 @@ def isc_repack_filter(w, out=None, stream=None):
     return RepackedFilter(data, K, C, R, S)
 
 
-KERNEL_NAMES = {0: "none", 1: "fused", 2: "resident", 3: "ring", 4: "generic", 5: "fused_ring"}
+KERNEL_NAMES = {0: "none", 1: "fused", 2: "resident", 3: "ring", 4: "generic", 5: "fused_ring", 6: "fused_reg"}
 
 
 def isc_sparse_kernel(desc: ConvDesc) -> str:

@@ -187,7 +187,8 @@ bool sparse_fused_applies(const SparseShape &sh);
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s, const Epilogue &epi = Epilogue{});
 bool sparse_fring_applies(const SparseShape &sh);
-// 1 (filter-resident), 5 (filter-ring) or 0 (neither): isc_sparse_kernel's ids.
+// 1 (filter-resident), 6 (filter-resident plan with the weights streamed to
+// registers), 5 (filter-ring) or 0 (none): isc_sparse_kernel's ids.
 int sparse_fused_kernel(const SparseShape &sh);
 hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s, const Epilogue &epi = Epilogue{});

@@ -56,7 +56,8 @@ struct FusedArgs {
 struct FusedPlan {
     int th, tw, cs;
     size_t lds;
-    int st;  // stride (1, or 2 with 8-column tiles)
+    int st;       // stride (1, or 2 with 8-column tiles)
+    bool wreg;    // weights streamed to registers (sparse_conv_fused_reg_kernel)
 };
 
 // Launchers of the kernels of one filter size (sparse_fused_r{1,3,5}.hip).
@@ -230,6 +231,145 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     }
 }
 
+// Variant for plans whose wavefronts share no input channel (cs == kWaves:
+// one row group, every wavefront its own channels): each wavefront streams
+// its channels' weights from the repacked filter (through L2) into
+// registers, one channel ahead of its walk, so LDS holds only the phase
+// tiles -- for four-row tiles of 8 columns little enough for two
+// workgroups per CU, four wavefronts per SIMD.  Stride 1; otherwise as the
+// kernel above.
+template <int RS_, int TH, int TW>
+__global__ __launch_bounds__(kWaves * kLanes, 4)
+void sparse_conv_fused_reg_kernel(FusedArgs a) {
+    using T = tile::Shape<RS_, RS_, 1, TH, TW>;
+    constexpr int RS2 = RS_ * RS_, EPL = T::EPL;
+    extern __shared__ float lds[];  // the phase tiles [wave][TH*TW][kRPad]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kLanes - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kLanes);
+    const int cs = kWaves;
+    const int phase = wave;
+    const int band = blockIdx.x % a.bands;
+    const int n = blockIdx.x / a.bands;
+    const int oy0 = band * TH;
+    const int C = a.C, H = a.H, W = a.W, P = a.P;
+    const bool rows_ok = oy0 < a.Ho;
+    const size_t HW = static_cast<size_t>(H) * W;
+    const float *x_n = a.x + static_cast<size_t>(n) * C * HW;
+    const int ncw = phase < C ? (C - 1 - phase) / cs + 1 : 0;
+
+    int xoff[EPL];
+    bool inwin[EPL];
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+        const int e = q * kLanes + lane;
+        const int wy = e / T::WCOLS;
+        const int y = oy0 - P + wy, xx = e - wy * T::WCOLS - P;
+        inwin[q] = rows_ok && e < T::WROWS * T::WCOLS && y >= 0 && y < H && xx >= 0 && xx < W;
+        xoff[q] = inwin[q] ? y * W + xx : 0;
+    }
+
+    // the next channel's window and weights (loaded a channel ahead; the
+    // last channel is loaded again past the end, keeping every load in
+    // bounds)
+    float xn[EPL];
+    float wn[RS2];
+    auto load_ch = [&](int i) {
+        const int c = phase + min(i, ncw - 1) * cs;
+        const float *plane = x_n + static_cast<size_t>(c) * HW;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) xn[q] = plane[xoff[q]];
+        const float *wc = a.wt + static_cast<size_t>(c) * RS2 * kWPitch + lane;
+#pragma unroll
+        for (int t = 0; t < RS2; ++t) wn[t] = wc[t * kWPitch];
+    };
+    if (ncw > 0) load_ch(0);
+
+    const bool run = decision_gate(a.dec, 1u);
+    if (!run) {
+        __builtin_amdgcn_s_waitcnt(0);
+        return;
+    }
+
+    tile::Acc<T> acc;
+#pragma unroll
+    for (int y = 0; y < TH; ++y)
+#pragma unroll
+        for (int x = 0; x < TW; ++x) acc[y][x][0] = 0.0f;
+
+#pragma unroll 1
+    for (int i = 0; i < ncw; ++i) {
+        // this channel's registers by explicit moves (which the compiler
+        // cannot forward, so the loaded registers are free for the next
+        // channel's loads and need no copy at the back edge), then the next
+        // channel's loads fly during this channel's walk
+        float cur[EPL];
+        tile::Wts<T> w;
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) asm volatile("v_mov_b32 %0, %1" : "=v"(cur[q]) : "v"(xn[q]));
+#pragma unroll
+        for (int t = 0; t < RS2; ++t) asm volatile("v_mov_b32 %0, %1" : "=v"(w[t / RS_][t % RS_][0]) : "v"(wn[t]));
+        if (i + 1 < ncw) load_ch(i + 1);
+        unsigned long long mask[EPL];
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) mask[q] = __ballot(inwin[q] && (__float_as_uint(cur[q]) & 0x7fffffffu) != 0u);
+        tile::walk_scan<T>(mask, cur, acc, w);
+    }
+
+    // step 3: the phase tiles summed through LDS in phase order and stored
+    // to NCHW, as in the kernel above (one row group)
+    constexpr int TP = TH * TW;
+    float *red = lds;
+#pragma unroll
+    for (int y = 0; y < TH; ++y)
+#pragma unroll
+        for (int x = 0; x < TW; ++x) red[(wave * TP + y * TW + x) * kRPad + lane] = acc[y][x][0];
+    __syncthreads();
+    const int Wo = a.Wo;
+    const int rows = min(TH, a.Ho - oy0);
+    const int npos = rows * Wo;  // <= kMaxTile
+    const int ostep = (kWaves * kLanes) / npos;
+    const int k0 = tid / npos;
+    const int pos = tid - k0 * npos;
+    const int oyl = pos / Wo;
+    const int ox = pos - oyl * Wo;
+    const size_t plane_out = static_cast<size_t>(a.Ho) * Wo;
+    const float *src = red + (oyl * TW + ox) * kRPad;
+    float *dst = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oy0) * Wo + pos;
+    const int relu = a.epi.relu;
+    uint32_t cnt = 0;
+    for (int k = k0 < ostep ? k0 : a.K; k < a.K; k += ostep) {
+        float part[kWaves];
+#pragma unroll
+        for (int p = 0; p < kWaves; ++p) part[p] = src[p * TP * kRPad + k];
+        float sum = part[0];
+#pragma unroll
+        for (int p = 1; p < kWaves; ++p) sum += part[p];
+        sum = epilogue_value(sum, relu);
+        cnt += nonzero_bit(sum);
+        dst[static_cast<size_t>(k) * plane_out] = sum;
+    }
+    if (a.epi.census) {
+        __syncthreads();
+        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(lds));
+    }
+}
+
+template <int RS_, int TH, int TW>
+hipError_t launch_fused_reg_t(const FusedArgs &a, size_t lds, hipStream_t s) {
+    auto kern = sparse_conv_fused_reg_kernel<RS_, TH, TW>;
+    if (lds > 64 * 1024) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (e != hipSuccess) return e;
+    }
+    const int64_t grid = static_cast<int64_t>(a.N) * a.bands;
+    if (a.epi.census && census_slots_for(grid) > a.epi.cap) return hipErrorInvalidValue;
+    kern<<<static_cast<unsigned>(grid), kWaves * kLanes, lds, s>>>(a);
+    return hipGetLastError();
+}
+
 template <int RS_, int TH, int TW, int ST>
 hipError_t launch_fused_t(const FusedArgs &a, size_t lds, hipStream_t s) {
     if constexpr (TH * TW > kMaxTile) {
@@ -262,6 +402,15 @@ hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s
 // (3x3 and 5x5 filters).
 template <int RS_>
 hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
+    if (p.wreg) {
+        // four-row tiles of 8 columns, 3x3 and 5x5 filters
+        if constexpr (RS_ == 1) {
+            return hipErrorInvalidValue;
+        } else {
+            if (p.th != 4 || p.tw != 8 || p.st != 1) return hipErrorInvalidValue;
+            return launch_fused_reg_t<RS_, 4, 8>(a, p.lds, s);
+        }
+    }
     if (p.st == 2) {
         if constexpr (RS_ == 1) {
             return hipErrorInvalidValue;

@@ -140,7 +140,7 @@ def test_sparse_kernel_choice(monkeypatch):
     """Host-side choice of the sparse kernel for the workload shapes."""
     monkeypatch.delenv("ISC_SPARSE_KERNEL", raising=False)
     d = isc.make_desc
-    assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused"    # LeNet conv2
+    assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused_reg"  # LeNet conv2
     assert isc.isc_sparse_kernel(d(128, 16, 28, 28, 32, 5, 5, 1, 2)) == "fused"    # inception 5x5
     assert isc.isc_sparse_kernel(d(128, 96, 27, 27, 256, 5, 5, 1, 2)) == "fused_ring"  # AlexNet conv2
     assert isc.isc_sparse_kernel(d(128, 384, 13, 13, 256, 3, 3, 1, 1)) == "fused_ring"  # AlexNet conv5

@@ -428,7 +428,7 @@ def test_sparse_conv_fused_entry(torch, isc, case):
     N, C, H, W, K, R, S, T, P, sp = case
     note("fused entry", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
-    assert isc.isc_sparse_kernel(desc) in ("fused", "fused_ring")
+    assert isc.isc_sparse_kernel(desc) in ("fused", "fused_reg", "fused_ring")
     x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=11 + sum(case[:9]))
     wt = isc.isc_repack_filter(to_dev(torch, w))
     y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
@@ -449,3 +449,24 @@ def test_sparse_conv_fused_rejects_ineligible(torch, isc):
     with pytest.raises(isc.IscError) as e:
         isc.isc_sparse_conv_fused(x, isc.isc_repack_filter(w), 1, 0)
     assert e.value.status == 3
+
+
+@pytest.mark.parametrize("case", [(3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9), (2, 24, 11, 11, 33, 5, 5, 1, 1, 0.85),
+                                  (2, 9, 8, 8, 64, 3, 3, 1, 1, 0.9)])
+def test_fused_weight_placements_agree(torch, isc, monkeypatch, case):
+    """Plans whose wavefronts share no channel stream the weights to
+    registers by default; the filter-in-LDS kernel (ISC_FUSED_W=0) on the
+    same shapes: both against the oracle, and bitwise equal to each other
+    (the same channel order per phase and phase order per output)."""
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("fused weight placement", case)
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=71 + sum(case[:9]))
+    wt = isc.isc_repack_filter(to_dev(torch, w))
+    want = oracle.conv2d_f64(x, w, T, P)
+    outs = []
+    for mode in ("1", "0"):
+        monkeypatch.setenv("ISC_FUSED_W", mode)
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+        assert_conv_close(y, want, "fused W=%s %s" % (mode, case))
+        outs.append(y)
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))

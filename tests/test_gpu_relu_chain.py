@@ -71,7 +71,7 @@ def expected_path(nnz, total):
 
 # N, C, H, W, K, R, S, T, P, sparsity, the sparse kernel the shape runs
 RELU_CASES = [
-    (3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9, "fused"),          # LeNet conv2-like, filter in LDS
+    (3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9, "fused_reg"),      # LeNet conv2-like, weights in registers
     (2, 9, 20, 20, 64, 5, 5, 1, 2, 0.9, "fused"),           # 16-column tiles, several row groups
     (2, 11, 13, 13, 384, 3, 3, 1, 1, 0.95, "fused_ring"),   # conv3/4-like, filter streamed
     (1, 7, 13, 13, 200, 3, 3, 1, 1, 0.9, "fused_ring"),     # ragged last map group
