@@ -26,7 +26,14 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
         if (std::atoi(env) == 0) return false;
     if (sh.T != 1 || sh.R == 1 || sh.Wo > 8) return false;
     const int tw = 8;
-    const int th = 4;
+    // four-row tiles; two-row tiles when four-row ones leave CUs without a
+    // workgroup (LeNet conv2 at batch 8: 7.7 -> 6.4 us; at batch 256 they
+    // cost 44 %).  ISC_FUSED_REG_TH = 2 or 4 fixes it (for measurements).
+    int th = static_cast<int64_t>(sh.N) * ((sh.Ho + 3) / 4) < kMinGroups ? 2 : 4;
+    if (const char *env = std::getenv("ISC_FUSED_REG_TH")) {
+        const int t = std::atoi(env);
+        if (t == 2 || t == 4) th = t;
+    }
     *plan = FusedPlan{th, tw, kWaves, sizeof(float) * kWaves * th * tw * kRPad, 1, true};
     return true;
 }

@@ -403,12 +403,13 @@ hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s
 template <int RS_>
 hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
     if (p.wreg) {
-        // four-row tiles of 8 columns, 3x3 and 5x5 filters
+        // four- or two-row tiles of 8 columns, 3x3 and 5x5 filters
         if constexpr (RS_ == 1) {
             return hipErrorInvalidValue;
         } else {
-            if (p.th != 4 || p.tw != 8 || p.st != 1) return hipErrorInvalidValue;
-            return launch_fused_reg_t<RS_, 4, 8>(a, p.lds, s);
+            if (p.tw != 8 || p.st != 1) return hipErrorInvalidValue;
+            return p.th == 4 ? launch_fused_reg_t<RS_, 4, 8>(a, p.lds, s)
+                             : (p.th == 2 ? launch_fused_reg_t<RS_, 2, 8>(a, p.lds, s) : hipErrorInvalidValue);
         }
     }
     if (p.st == 2) {
