@@ -179,10 +179,12 @@ struct SparseShape {
 };
 
 // ISC steps 1-3 in one launch, compacting on the fly from x, with the filter
-// repacked K-contiguous (launch_repack_filter's layout; stride 1, square
-// 1x1/3x3/5x5 filters).
-// The filter-resident kernel takes filters that fit in LDS (K <= 64); the
-// filter-ring kernel (sparse_fring.hip) streams larger ones through LDS.
+// repacked K-contiguous (launch_repack_filter's layout; square 1x1/3x3/5x5
+// filters at stride 1, 3x3/5x5 at stride 2 with at most 8 output columns).
+// The filter-resident kernel takes filters that fit in LDS (K <= 64; with
+// the weights streamed to registers when no two wavefronts share a
+// channel); the filter-ring kernel (sparse_fring.hip) streams larger ones
+// through LDS (stride 1).
 bool sparse_fused_applies(const SparseShape &sh);
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s, const Epilogue &epi = Epilogue{});

@@ -2,9 +2,10 @@
 // translation units that define ISC_FUSED_INSTANTIATE, the kernel and its
 // launchers).
 //
-// ISC steps 1-3 (Sec. "Sparse Convolution") in one launch, for stride-1
-// convolutions with square 1x1, 3x3 or 5x5 filters and at most 64 output
-// maps (few input maps: LeNet conv2, an inception 5x5 branch).
+// ISC steps 1-3 (Sec. "Sparse Convolution") in one launch, for convolutions
+// with square 1x1, 3x3 or 5x5 filters at stride 1 (3x3 and 5x5 also at
+// stride 2 with at most 8 output columns) and at most 64 output maps (few
+// input maps: LeNet conv2, an inception 5x5 branch, Tab. 2's LeNet conv2).
 //
 // The paper builds each input map's nonzero list on the fly before using it.
 // Here the list never leaves the wavefront: a wavefront loads the input rows

@@ -1,5 +1,6 @@
 // Register-tile machinery shared by the zero-skipping kernels (ISC steps 2
-// and 3, Sec. "Sparse Convolution"), stride 1, square R x S filters.
+// and 3, Sec. "Sparse Convolution"): square R x S filters, stride 1 (the
+// filter-resident kernel also at stride 2).
 //
 // A wavefront owns an output tile of TH rows x TW columns x 64*KPL output
 // maps: lane l accumulates maps kbase + l*KPL + j (j < KPL) in registers
