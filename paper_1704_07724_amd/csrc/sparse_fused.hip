@@ -18,9 +18,10 @@ size_t fused_lds(int crs, int th, int tw) {
 // Plans whose wavefronts share no channel (every wavefront its own phase)
 // gain nothing from the filter in LDS: with the weights streamed to
 // registers, LDS holds only the phase tiles, and four-row tiles of 8
-// columns let two workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us).
-// Taken wherever eligible: stride 1, 3x3 and 5x5 filters, at most 8 output
-// columns.  ISC_FUSED_W = 0 keeps the filter in LDS (for measurements).
+// columns let two workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us).  The
+// filter need not fit in LDS at all.  Taken wherever eligible: stride 1,
+// 3x3 and 5x5 filters, at most 64 maps and 8 output columns.  ISC_FUSED_W =
+// 0 keeps the filter in LDS (for measurements).
 bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
     if (const char *env = std::getenv("ISC_FUSED_W"))
         if (std::atoi(env) == 0) return false;
@@ -50,7 +51,9 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     if (!(sh.T == 1 || (sh.T == 2 && sh.R > 1 && sh.Wo <= 8))) return false;
     if (sh.Wo > 28 || sh.K > kLanes) return false;
     const int crs = sh.C * sh.R * sh.S;
-    if (static_cast<size_t>(crs) * kWPitch * sizeof(float) > kLdsMax) return false;
+    // a filter too large for LDS: only the register-weight kernel, which
+    // keeps none of it there, takes it (one phase per wavefront)
+    if (static_cast<size_t>(crs) * kWPitch * sizeof(float) > kLdsMax) return fused_wreg_plan(sh, plan);
     const int tw = fused_tw(sh.Wo);
     int th_cap = 8, cs_fix = 0;
     if (const char *env = std::getenv("ISC_FUSED_TH")) th_cap = std::max(1, std::atoi(env));
