@@ -17,23 +17,32 @@ size_t fused_lds(int crs, int th, int tw) {
 
 // Plans whose wavefronts share no channel (every wavefront its own phase)
 // gain nothing from the filter in LDS: with the weights streamed to
-// registers, LDS holds only the phase tiles, and four-row tiles of 8
-// columns let two workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us).  The
-// filter need not fit in LDS at all.  Taken wherever eligible: stride 1,
-// 3x3 and 5x5 filters, at most 64 maps and 8 output columns.  ISC_FUSED_W =
-// 0 keeps the filter in LDS (for measurements).
+// registers, LDS holds only the phase tiles, and 32-position tiles let two
+// workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us).  The filter need not
+// fit in LDS at all, and one workgroup per group of 64 maps takes any K
+// (AlexNet-ImageNet conv4 of Tab. 2 at batch 128: 259 us on the
+// filter-ring kernel -> 113 us).  Taken wherever eligible: stride 1, square
+// 1x1, 3x3 and 5x5 filters, at most 16 output columns.  ISC_FUSED_W = 0
+// keeps the filter in LDS, or in the ring beyond 64 maps (for measurements).
 bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
     if (const char *env = std::getenv("ISC_FUSED_W"))
         if (std::atoi(env) == 0) return false;
-    if (sh.T != 1 || sh.R == 1 || sh.Wo > 8) return false;
-    const int tw = 8;
-    // four-row tiles; two-row tiles when four-row ones leave CUs without a
-    // workgroup (LeNet conv2 at batch 8: 7.7 -> 6.4 us; at batch 256 they
-    // cost 44 %).  ISC_FUSED_REG_TH = 2 or 4 fixes it (for measurements).
-    int th = static_cast<int64_t>(sh.N) * ((sh.Ho + 3) / 4) < kMinGroups ? 2 : 4;
+    if (sh.T != 1 || sh.Wo > 16) return false;
+    // the kernel addresses the repacked filter with 32-bit byte offsets
+    const int64_t kp = (sh.K + kLanes - 1) / kLanes * kLanes;
+    if (static_cast<int64_t>(sh.C) * sh.R * sh.S * kp * static_cast<int64_t>(sizeof(float)) >= (1ll << 31))
+        return false;
+    // 4 x 8 or 2 x 16 tiles; half as many rows when full ones leave CUs
+    // without a workgroup (LeNet conv2 at batch 8: 7.7 -> 6.4 us; at batch
+    // 256 they cost 44 %).  ISC_FUSED_REG_TH fixes the rows (for
+    // measurements).
+    const int tw = sh.Wo <= 8 ? 8 : 16;
+    const int full = 32 / tw;
+    const int64_t kgroups = (sh.K + kLanes - 1) / kLanes;
+    int th = static_cast<int64_t>(sh.N) * ((sh.Ho + full - 1) / full) * kgroups < kMinGroups ? full / 2 : full;
     if (const char *env = std::getenv("ISC_FUSED_REG_TH")) {
         const int t = std::atoi(env);
-        if (t == 2 || t == 4) th = t;
+        if (t == full || t == full / 2) th = t;
     }
     *plan = FusedPlan{th, tw, kWaves, sizeof(float) * kWaves * th * tw * kRPad, 1, true};
     return true;
@@ -49,7 +58,8 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
 bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     if (sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     if (!(sh.T == 1 || (sh.T == 2 && sh.R > 1 && sh.Wo <= 8))) return false;
-    if (sh.Wo > 28 || sh.K > kLanes) return false;
+    if (sh.Wo > 28) return false;
+    if (sh.K > kLanes) return fused_wreg_plan(sh, plan);  // only the register-weight kernel takes K > 64
     const int crs = sh.C * sh.R * sh.S;
     // a filter too large for LDS: only the register-weight kernel, which
     // keeps none of it there, takes it (one phase per wavefront)
@@ -87,12 +97,14 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
 }  // namespace
 }  // namespace fused
 
-// The filter-resident kernel launches N * bands <= N * Ho workgroups; the
+// The filter-resident kernel launches N * bands <= N * Ho workgroups; its
+// register-weight variant N * bands * map groups, with bands <= Ho; the
 // filter-ring kernel N * bands * column tiles * map groups, with bands <=
 // ceil(Ho / 4), column tiles <= ceil(Wo / 16) and map groups <= ceil(K / 64).
 int64_t sparse_fused_max_groups(const SparseShape &sh) {
     const int64_t ring = static_cast<int64_t>((sh.Ho + 3) / 4) * ((sh.Wo + 15) / 16) * ((sh.K + 63) / 64);
-    return static_cast<int64_t>(sh.N) * std::max<int64_t>(sh.Ho, ring);
+    const int64_t reg = static_cast<int64_t>(sh.Ho) * ((sh.K + 63) / 64);  // register-weight kernel
+    return static_cast<int64_t>(sh.N) * std::max(ring, reg);
 }
 
 bool sparse_fused_applies(const SparseShape &sh) {
@@ -121,6 +133,8 @@ hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const floa
     a.cs = p.cs;
     a.rg = kWaves / p.cs;
     a.bands = (sh.Ho + a.rg * p.th - 1) / (a.rg * p.th);
+    a.Kp = (sh.K + kLanes - 1) / kLanes * kLanes;
+    a.kgroups = p.wreg ? a.Kp / kLanes : 1;
     a.dec = dec;
     a.epi = epi;
     switch (sh.R) {

@@ -29,6 +29,7 @@
 #pragma once
 
 #include "sparse_tile.hpp"
+#include <cstdlib>
 
 namespace isc {
 namespace fused {
@@ -40,6 +41,9 @@ constexpr int kRPad = 65;        // LDS pitch of one tile position's output maps
 constexpr int kMaxTile = 64;     // accumulators per lane
 constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
 constexpr int kWPitch = 64;      // maps per filter column in the repacked layout (K <= 64)
+// Word 3 of a raw buffer resource on gfx9-family chips (gfx950 included):
+// 32-bit data format, no swizzle, bounds checked against the record count.
+constexpr int kBufferFormat = 0x00020000;
 
 
 struct FusedArgs {
@@ -50,6 +54,8 @@ struct FusedArgs {
     int cs;           // channel phases per row group
     int rg;           // row groups per workgroup (kWaves / cs)
     int bands;        // groups of rg * TH output rows
+    int kgroups;      // groups of 64 output maps (register-weight kernel; 1 otherwise)
+    int Kp;           // maps per filter column of wt (K rounded up to 64)
     Decision dec;
     Epilogue epi;     // rectifier and census of y
 };
@@ -237,9 +243,10 @@ void sparse_conv_fused_kernel(FusedArgs a) {
 // its channels' weights from the repacked filter (through L2) into
 // registers, one channel ahead of its walk, so LDS holds only the phase
 // tiles -- for four-row tiles of 8 columns little enough for two
-// workgroups per CU, four wavefronts per SIMD.  Stride 1; otherwise as the
-// kernel above.
-template <int RS_, int TH, int TW>
+// workgroups per CU, four wavefronts per SIMD.  One workgroup per group of
+// 64 output maps (kgroups), lanes over the maps of its group.  Stride 1;
+// otherwise as the kernel above.
+template <int RS_, int TH, int TW, bool WIDE>
 __global__ __launch_bounds__(kWaves * kLanes, 4)
 void sparse_conv_fused_reg_kernel(FusedArgs a) {
     using T = tile::Shape<RS_, RS_, 1, TH, TW>;
@@ -251,9 +258,13 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid / kLanes);
     const int cs = kWaves;
     const int phase = wave;
-    const int band = blockIdx.x % a.bands;
-    const int n = blockIdx.x / a.bands;
+    const int kg = blockIdx.x % a.kgroups;  // this workgroup's 64 output maps
+    const int rest = blockIdx.x / a.kgroups;
+    const int band = rest % a.bands;
+    const int n = rest / a.bands;
     const int oy0 = band * TH;
+    const int kbase = kg * kLanes;
+    const int kcnt = min(kLanes, a.K - kbase);
     const int C = a.C, H = a.H, W = a.W, P = a.P;
     const bool rows_ok = oy0 < a.Ho;
     const size_t HW = static_cast<size_t>(H) * W;
@@ -273,7 +284,16 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
 
     // the next channel's window and weights (loaded a channel ahead; the
     // last channel is loaded again past the end, keeping every load in
-    // bounds)
+    // bounds).  One group of maps (WIDE false): the taps 64 floats apart,
+    // immediate offsets of one address.  Several (WIDE true): through a
+    // buffer resource over the repacked filter (its size checked below 2^31
+    // bytes by the plan), where the byte offset of tap t, t * Kp * 4, is the
+    // same for every channel and stays in a scalar register, and the
+    // channel's offset is one vector add, so a channel's RS2 loads take no
+    // address arithmetic of their own.
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(a.wt), 0, C * RS2 * a.Kp * static_cast<int>(sizeof(float)), kBufferFormat);
+    const int kp4 = a.Kp * static_cast<int>(sizeof(float));
     float xn[EPL];
     float wn[RS2];
     auto load_ch = [&](int i) {
@@ -281,9 +301,16 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
         const float *plane = x_n + static_cast<size_t>(c) * HW;
 #pragma unroll
         for (int q = 0; q < EPL; ++q) xn[q] = plane[xoff[q]];
-        const float *wc = a.wt + static_cast<size_t>(c) * RS2 * kWPitch + lane;
+        if constexpr (WIDE) {
+            const int voff = ((c * RS2 * a.Kp + kbase + lane) * static_cast<int>(sizeof(float)));
 #pragma unroll
-        for (int t = 0; t < RS2; ++t) wn[t] = wc[t * kWPitch];
+            for (int t = 0; t < RS2; ++t)
+                wn[t] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(wres, voff, t * kp4, 0));
+        } else {
+            const float *wc = a.wt + static_cast<size_t>(c) * RS2 * kWPitch + lane;
+#pragma unroll
+            for (int t = 0; t < RS2; ++t) wn[t] = wc[t * kWPitch];
+        }
     };
     if (ncw > 0) load_ch(0);
 
@@ -337,10 +364,11 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
     const int ox = pos - oyl * Wo;
     const size_t plane_out = static_cast<size_t>(a.Ho) * Wo;
     const float *src = red + (oyl * TW + ox) * kRPad;
-    float *dst = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oy0) * Wo + pos;
+    float *dst = a.y + (static_cast<size_t>(n) * a.K + kbase) * plane_out + static_cast<size_t>(oy0) * Wo + pos;
     const int relu = a.epi.relu;
     uint32_t cnt = 0;
-    for (int k = k0 < ostep ? k0 : a.K; k < a.K; k += ostep) {
+    // k: map within this workgroup's group of 64
+    for (int k = k0 < ostep ? k0 : kcnt; k < kcnt; k += ostep) {
         float part[kWaves];
 #pragma unroll
         for (int p = 0; p < kWaves; ++p) part[p] = src[p * TP * kRPad + k];
@@ -357,18 +385,29 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
     }
 }
 
-template <int RS_, int TH, int TW>
-hipError_t launch_fused_reg_t(const FusedArgs &a, size_t lds, hipStream_t s) {
-    auto kern = sparse_conv_fused_reg_kernel<RS_, TH, TW>;
+template <int RS_, int TH, int TW, bool WIDE>
+hipError_t launch_fused_reg_w(const FusedArgs &a, size_t lds, hipStream_t s) {
+    auto kern = sparse_conv_fused_reg_kernel<RS_, TH, TW, WIDE>;
     if (lds > 64 * 1024) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (e != hipSuccess) return e;
     }
-    const int64_t grid = static_cast<int64_t>(a.N) * a.bands;
+    const int64_t grid = static_cast<int64_t>(a.N) * a.bands * a.kgroups;
     if (a.epi.census && census_slots_for(grid) > a.epi.cap) return hipErrorInvalidValue;
     kern<<<static_cast<unsigned>(grid), kWaves * kLanes, lds, s>>>(a);
     return hipGetLastError();
+}
+
+// one group of 64 maps: filter taps at immediate offsets (kgroups == 1 and
+// Kp == 64); else through the buffer resource.  ISC_FUSED_REG_WIDE = 1 takes
+// the buffer path for one group too (for measurements).
+template <int RS_, int TH, int TW>
+hipError_t launch_fused_reg_t(const FusedArgs &a, size_t lds, hipStream_t s) {
+    bool wide = a.kgroups > 1;
+    if (const char *env = std::getenv("ISC_FUSED_REG_WIDE"))
+        if (std::atoi(env) == 1) wide = true;
+    return wide ? launch_fused_reg_w<RS_, TH, TW, true>(a, lds, s) : launch_fused_reg_w<RS_, TH, TW, false>(a, lds, s);
 }
 
 template <int RS_, int TH, int TW, int ST>
@@ -404,14 +443,17 @@ hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s
 template <int RS_>
 hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
     if (p.wreg) {
-        // four- or two-row tiles of 8 columns, 3x3 and 5x5 filters
-        if constexpr (RS_ == 1) {
-            return hipErrorInvalidValue;
-        } else {
-            if (p.tw != 8 || p.st != 1) return hipErrorInvalidValue;
+        // 4 x 8, 2 x 8, 2 x 16 and 1 x 16 tiles, stride 1
+        if (p.st != 1) return hipErrorInvalidValue;
+        if (p.tw == 8) {
             return p.th == 4 ? launch_fused_reg_t<RS_, 4, 8>(a, p.lds, s)
                              : (p.th == 2 ? launch_fused_reg_t<RS_, 2, 8>(a, p.lds, s) : hipErrorInvalidValue);
         }
+        if (p.tw == 16) {
+            return p.th == 2 ? launch_fused_reg_t<RS_, 2, 16>(a, p.lds, s)
+                             : (p.th == 1 ? launch_fused_reg_t<RS_, 1, 16>(a, p.lds, s) : hipErrorInvalidValue);
+        }
+        return hipErrorInvalidValue;
     }
     if (p.st == 2) {
         if constexpr (RS_ == 1) {

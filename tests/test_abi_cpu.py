@@ -143,7 +143,11 @@ def test_sparse_kernel_choice(monkeypatch):
     assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused_reg"  # LeNet conv2
     assert isc.isc_sparse_kernel(d(128, 16, 28, 28, 32, 5, 5, 1, 2)) == "fused"    # inception 5x5
     assert isc.isc_sparse_kernel(d(128, 96, 27, 27, 256, 5, 5, 1, 2)) == "fused_ring"  # AlexNet conv2
-    assert isc.isc_sparse_kernel(d(128, 384, 13, 13, 256, 3, 3, 1, 1)) == "fused_ring"  # AlexNet conv5
+    assert isc.isc_sparse_kernel(d(128, 384, 13, 13, 256, 3, 3, 1, 1)) == "fused_reg"  # AlexNet conv5
+    assert isc.isc_sparse_kernel(d(128, 384, 5, 5, 384, 3, 3, 1, 1)) == "fused_reg"   # Tab. 2 AlexNet conv4
+    assert isc.isc_sparse_kernel(d(1, 832, 7, 7, 256, 1, 1, 1, 0)) == "fused_reg"     # Tab. 2 inception 5a.1
+    assert isc.isc_sparse_kernel(d(128, 16, 17, 17, 32, 5, 5, 1, 2)) == "fused"       # 17 columns: filter in LDS
+    assert isc.isc_sparse_kernel(d(128, 16, 17, 17, 96, 5, 5, 1, 2)) == "fused_ring"  # 17 columns, K > 64
     assert isc.isc_sparse_kernel(d(128, 96, 28, 28, 128, 3, 3, 1, 1)) == "fused_ring"  # inception 3x3
     assert isc.isc_sparse_kernel(d(1, 3, 20, 200, 66, 3, 3, 1, 1)) == "fused_ring"     # column tiles
     assert isc.isc_sparse_kernel(d(2, 4, 11, 11, 64, 5, 5, 2, 1)) == "fused"       # stride 2, 5 x 5 output

@@ -470,3 +470,40 @@ def test_fused_weight_placements_agree(torch, isc, monkeypatch, case):
         assert_conv_close(y, want, "fused W=%s %s" % (mode, case))
         outs.append(y)
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+
+
+@pytest.mark.parametrize("case", [(2, 12, 7, 7, 150, 3, 3, 1, 1, 0.9), (3, 9, 8, 8, 128, 5, 5, 1, 2, 0.9),
+                                  (1, 5, 5, 6, 65, 3, 3, 1, 1, 0.8), (130, 4, 7, 7, 96, 3, 3, 1, 1, 0.9),
+                                  (2, 11, 13, 13, 200, 3, 3, 1, 1, 0.9), (40, 6, 14, 14, 70, 3, 3, 1, 1, 0.9),
+                                  (2, 7, 12, 12, 130, 5, 5, 1, 2, 0.9), (2, 40, 9, 9, 100, 1, 1, 1, 0, 0.9),
+                                  (3, 33, 16, 16, 80, 1, 1, 1, 0, 0.8)])
+def test_register_kernel_map_groups(torch, isc, monkeypatch, case):
+    """The register-weight kernel beyond 64 maps (one workgroup per group of
+    64, ragged last group included) and on 16-column tiles, every tile
+    height it takes: plain and rectified with the census, against the
+    oracle; and the filter-ring kernel (ISC_FUSED_W = 0) on the same shape."""
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("register kernel map groups", case)
+    desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
+    assert isc.isc_sparse_kernel(desc) == "fused_reg"
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=83 + sum(case[:9]))
+    wt = isc.isc_repack_filter(to_dev(torch, w))
+    want = oracle.conv2d_f64(x, w, T, P)
+    Wo = want.shape[3]
+    full = 4 if Wo <= 8 else 2
+    for th in (full, full // 2):
+        monkeypatch.setenv("ISC_FUSED_REG_TH", str(th))
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+        assert_conv_close(y, want, "register kernel th%d %s" % (th, case))
+    monkeypatch.delenv("ISC_FUSED_REG_TH")
+    yc = isc.census(desc)
+    z = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), T, P, path="sparse", y_census=yc,
+                            ws=isc.workspace(desc, "sparse")).cpu().numpy()
+    want_relu, _ = oracle.relu_conv2d_f64(x, w, T, P)
+    assert_conv_close(z, want_relu, "register kernel relu %s" % (case,))
+    assert isc.isc_census_read(yc) == (z.size, int(np.count_nonzero(z)))
+    monkeypatch.setenv("ISC_FUSED_W", "0")
+    other = isc.isc_sparse_kernel(desc)
+    assert other in ("fused", "fused_ring"), other
+    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+    assert_conv_close(y, want, "%s kernel %s" % (other, case))

@@ -73,8 +73,9 @@ def expected_path(nnz, total):
 RELU_CASES = [
     (3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9, "fused_reg"),      # LeNet conv2-like, weights in registers
     (2, 9, 20, 20, 64, 5, 5, 1, 2, 0.9, "fused"),           # 16-column tiles, several row groups
-    (2, 11, 13, 13, 384, 3, 3, 1, 1, 0.95, "fused_ring"),   # conv3/4-like, filter streamed
-    (1, 7, 13, 13, 200, 3, 3, 1, 1, 0.9, "fused_ring"),     # ragged last map group
+    (2, 11, 13, 13, 384, 3, 3, 1, 1, 0.95, "fused_reg"),    # conv3/4-like, six groups of 64 maps
+    (1, 7, 13, 13, 200, 3, 3, 1, 1, 0.9, "fused_reg"),      # ragged last map group, 16-column tiles
+    (1, 7, 20, 20, 200, 3, 3, 1, 1, 0.9, "fused_ring"),     # filter streamed, ragged last map group
     (1, 4, 9, 70, 96, 5, 5, 1, 2, 0.8, "fused_ring"),       # column tiles, ragged last tile
     (2, 4, 11, 11, 64, 5, 5, 2, 1, 0.8, "fused"),           # stride 2, filter resident
     (2, 4, 21, 21, 64, 5, 5, 2, 1, 0.8, "generic"),         # stride 2, 10 columns: lists, then the epilogue pass
