@@ -72,9 +72,26 @@ struct Decision {
 __device__ __forceinline__ unsigned long long sum_counts(const uint32_t *counts, int n) {
     unsigned long long s = 0;
     const uint4 *p = reinterpret_cast<const uint4 *>(counts);
-    for (int i = threadIdx.x & 63; i < n / 4; i += 64) {
-        const uint4 v = p[i];
-        s += static_cast<unsigned long long>(v.x) + v.y + v.z + v.w;
+    const int n4 = n / 4;
+    const int lane = threadIdx.x & 63;
+    if (n4 <= 64) {  // one load per lane at most
+        if (lane < n4) {
+            const uint4 v = p[lane];
+            s = static_cast<unsigned long long>(v.x) + v.y + v.z + v.w;
+        }
+    } else {
+        // eight loads in flight per lane (a census of thousands of slots would
+        // otherwise cost one dependent L2 round trip per 64 of them, in every
+        // wavefront's prologue); indices past the end load the last word again
+        // and are not added
+        for (int base = lane; base < n4; base += 8 * 64) {
+            uint4 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = p[min(base + j * 64, n4 - 1)];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (base + j * 64 < n4) s += static_cast<unsigned long long>(v[j].x) + v[j].y + v[j].z + v[j].w;
+        }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
