@@ -198,6 +198,17 @@ class LayerRun:
         del dy, ws, dw
         return res
 
+    def measure_library(self, steps, warmup, t_sparse_ms):
+        """The vendor library's forward convolution of the same layer (torch's
+        GPU conv2d in fp32, TF32 off, eager), a second dense reference beside
+        this library's own dense path."""
+        torch, L = self.torch, self.layer
+        torch.backends.cudnn.allow_tf32 = False
+        torch.backends.cuda.matmul.allow_tf32 = False
+        fn = lambda: torch.nn.functional.conv2d(self.x, self.w, stride=L.T, padding=L.P)
+        t = event_time_ms(torch, fn, max(20, steps), warmup)
+        return {"t_library_ms": t, "speedup_sparse_vs_library": round(t / t_sparse_ms, 3)}
+
     def summary(self, res):
         f, nzm = self.flops, self.nz_macs
         L = self.layer
@@ -499,6 +510,7 @@ def main():
 
     res = head.measure(args.steps, args.warmup, graphs=not args.no_graph)
     hs = head.summary(res)
+    lib = head.measure_library(args.steps, args.warmup, res["t_sparse_ms"])
     t_kernel = res["t_sparse_kernel_ms"]
     achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
     traffic = counted_traffic()
@@ -547,6 +559,9 @@ def main():
         "nonzero_mac_per_s": hs["nonzero_mac_per_s_auto"],
         "measured_sparsity": hs["measured_sparsity"],
         "dense_path_tflops": hs["tflops_dense"],
+        # the vendor library's fp32 forward convolution of the same layer
+        "library_conv2d_ms": round(lib["t_library_ms"], 6),
+        "speedup_vs_library": round(lib["t_library_ms"] / ms_per_step, 3),
         "roofline": roofline,
         "hbm": hbm,
         "timings_ms": {k: hs[k] for k in hs if k.startswith("t_")},
@@ -577,13 +592,15 @@ def main():
                 run = LayerRun(torch, isc, layer)
                 s = run.summary(run.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph))
                 s.update(run.measure_dw(max(20, args.steps // 4), 5, graphs=not args.no_graph))
+                s.update(run.measure_library(max(20, args.steps // 4), 5, s["t_sparse_ms"]))
                 rows.append(s)
                 dws = (" | dw sparse %.4f ms library %.4f (%.2fx)" % (
                     s["t_dw_sparse_ms"], s["t_dw_library_ms"], s["speedup_dw_vs_library"])
                        if "t_dw_sparse_ms" in s else "")
-                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx%s" % (
+                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx library %.4f (%.2fx)%s" % (
                     layer.name, s["t_auto_ms"], s["t_sparse_ms"], s["t_dense_ms"],
-                    s["speedup_sparse_vs_dense"], dws), file=sys.stderr, flush=True)
+                    s["speedup_sparse_vs_dense"], s["t_library_ms"], s["speedup_sparse_vs_library"], dws),
+                      file=sys.stderr, flush=True)
                 del run
                 torch.cuda.empty_cache()
         if args.out:
