@@ -232,8 +232,10 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
  * the zero test over its window, scanned in row-major order) and multiplies
  * each nonzero by the K-contiguous weight vectors of step 2, which it holds
  * in registers.  The filter is resident in LDS when it fits (K <= 64:
- * ISC_KERNEL_FUSED) and streamed through LDS otherwise
- * (ISC_KERNEL_FUSED_RING).  The kernels isc_conv2d's sparse path runs when
+ * ISC_KERNEL_FUSED), streamed from L2 into each wavefront's registers at
+ * stride 1 with at most 16 output columns, for any K (ISC_KERNEL_FUSED_REG,
+ * one workgroup per group of 64 output maps), and streamed through LDS
+ * otherwise (ISC_KERNEL_FUSED_RING).  The kernels isc_conv2d's sparse path runs when
  * isc_sparse_kernel reports either (isc_conv2d repacks the filter itself, in
  * the launch that counts the nonzeros); no sparse/dense decision here.
  *   x: device input as for isc_conv2d.
@@ -251,8 +253,8 @@ int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *w
  * *kernel: ISC_KERNEL_FUSED, ISC_KERNEL_FUSED_REG or ISC_KERNEL_FUSED_RING
  * (compaction on the fly, isc_sparse_conv_fused; filter resident in LDS,
  * each wavefront's own channels' weights streamed to registers -- for plans
- * whose wavefronts share no input channel, at stride 1 and at most 8 output
- * columns -- or filter streamed through LDS), else
+ * whose wavefronts share no input channel, at stride 1 and at most 16
+ * output columns, any K -- or filter streamed through LDS), else
  * the kernel over compacted lists that isc_sparse_conv also runs:
  * ISC_KERNEL_RESIDENT (filter resident in LDS), ISC_KERNEL_RING (filter
  * streamed through LDS) or ISC_KERNEL_GENERIC (any filter and stride);
