@@ -12,6 +12,7 @@
 #include "isc_internal.hpp"
 
 #include <algorithm>
+#include <cstdlib>
 
 namespace isc {
 namespace {
@@ -81,6 +82,13 @@ struct GemmArgs {
     int conv_hw;  // > 0: scatter column n to NCHW with Ho*Wo = conv_hw
     Decision dec;
     Epilogue epi;  // rectifier and census of c
+    // split reduction: workgroup z of the grid sums k in [z * kchunk,
+    // (z + 1) * kchunk) (kchunk a multiple of 32) and stores its raw partial
+    // tile to part[z][m][n]; gemm_split_reduce_kernel adds the partials in z
+    // order and applies the epilogue.  part == nullptr: one range, this
+    // kernel stores c.
+    float *part;
+    int kchunk;
     // implicit im2col: B[k][j] is gathered from the input x instead of read
     // from b (k = (c, r, s), j = (n, oy, ox))
     const float *x;
@@ -247,15 +255,17 @@ void gemm_f32_kernel(GemmArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    const int nk = (Kd + BK - 1) / BK;
-    load_slice(0);
+    const int kb = g.part ? static_cast<int>(blockIdx.z) * g.kchunk : 0;
+    const int ke = g.part ? min(Kd, kb + g.kchunk) : Kd;
+    const int nk = (ke - kb + BK - 1) / BK;
+    load_slice(kb);
     store_slice(0);
     __syncthreads();
     const int lrow = lane & 31;   // row (A) / column (B) within a 32-block
     const int lk = lane >> 5;     // which of the two k of an MFMA step
     for (int kt = 0; kt < nk; ++kt) {
         const int buf = kt & 1;
-        if (kt + 1 < nk) load_slice((kt + 1) * BK);
+        if (kt + 1 < nk) load_slice(kb + (kt + 1) * BK);
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 2) {
             float av[WM], bv[WN];
@@ -275,6 +285,22 @@ void gemm_f32_kernel(GemmArgs g) {
 
     // epilogue: accumulator register v of lane l holds row
     // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32 x 32 block
+    if (g.part) {  // a partial sum of the split reduction, stored raw
+        float *pz = g.part + static_cast<size_t>(blockIdx.z) * M * N;
+#pragma unroll
+        for (int j = 0; j < WN; ++j) {
+            const int nn = n0 + (wn * WN + j) * 32 + lrow;
+            if (nn >= N) continue;
+#pragma unroll
+            for (int i = 0; i < WM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = m0 + (wm * WM + i) * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+                    if (m < M) pz[static_cast<size_t>(m) * N + nn] = acc[i][j][v];
+                }
+        }
+        return;
+    }
     uint32_t cnt = 0;  // nonzero values stored (the census count)
 #pragma unroll
     for (int j = 0; j < WN; ++j) {
@@ -310,11 +336,54 @@ void gemm_f32_kernel(GemmArgs g) {
     }
 }
 
+// The split reduction's second pass: c = epilogue(sum over z of part[z]),
+// partials added in z order; each workgroup takes kReducePer consecutive
+// elements of the M x N result (consecutive threads on consecutive columns)
+// and commits its census slot.
+constexpr int kReducePer = 2048;
+
+__global__ __launch_bounds__(256)
+void gemm_split_reduce_kernel(GemmArgs g, int splits) {
+    if (!decision_gate(g.dec, 2u)) return;
+    const int64_t mn = static_cast<int64_t>(g.M) * g.N;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kReducePer;
+    uint32_t cnt = 0;
+    for (int r = 0; r < kReducePer / 256; ++r) {
+        const int64_t e = base + r * 256 + threadIdx.x;
+        if (e >= mn) break;
+        float sum = g.part[e];
+        for (int z = 1; z < splits; ++z) sum += g.part[static_cast<int64_t>(z) * mn + e];
+        const int m = static_cast<int>(e / g.N);
+        const int nn = static_cast<int>(e - static_cast<int64_t>(m) * g.N);
+        const float o = epilogue_value(sum, g.epi.relu);
+        cnt += nonzero_bit(o);
+        const int img = nn / g.conv_hw;
+        const int p = nn - img * g.conv_hw;
+        g.c[(static_cast<size_t>(img) * g.M + m) * g.conv_hw + p] = o;
+    }
+    if (g.epi.census) {
+        __shared__ uint32_t sums[4];
+        census_commit(g.epi, cnt, sums);
+    }
+}
+
 template <int WAVES_M, int WM, int WN, int BK = 16>
 hipError_t launch_gemm_t(const GemmArgs &g, bool a_vec, bool b_padded, bool implicit, hipStream_t s) {
     constexpr int BM = WAVES_M * WM * 32;
     constexpr int BN = (4 / WAVES_M) * WN * 32;
     dim3 grid((g.N + BN - 1) / BN, (g.M + BM - 1) / BM);
+    if (g.part) {  // split reduction (implicit im2col into NCHW only)
+        if (!implicit || g.conv_hw <= 0 || g.kchunk <= 0 || g.kchunk % 32 != 0) return hipErrorInvalidValue;
+        grid.z = static_cast<unsigned>((g.Kd + g.kchunk - 1) / g.kchunk);
+        const int64_t rgroups = (static_cast<int64_t>(g.M) * g.N + kReducePer - 1) / kReducePer;
+        if (g.epi.census && census_slots_for(rgroups) > g.epi.cap) return hipErrorInvalidValue;
+        if (a_vec) gemm_f32_kernel<WAVES_M, WM, WN, true, false, true, BK><<<grid, 256, 0, s>>>(g);
+        else gemm_f32_kernel<WAVES_M, WM, WN, false, false, true, BK><<<grid, 256, 0, s>>>(g);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        gemm_split_reduce_kernel<<<static_cast<unsigned>(rgroups), 256, 0, s>>>(g, static_cast<int>(grid.z));
+        return hipGetLastError();
+    }
     if (g.epi.census && census_slots_for(static_cast<int64_t>(grid.x) * grid.y) > g.epi.cap)
         return hipErrorInvalidValue;
     if (implicit) {
@@ -374,17 +443,54 @@ hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda
 int64_t gemm_max_groups(int64_t M, int64_t Ncols) {
     // the smallest tiles launch_gemm_any picks are 32 rows x 128 columns
     // (M <= 32) and 64 x 64 (M <= 64); the widest grid of any tile is at most
-    // ceil(M / 32) * ceil(Ncols / 64)
+    // ceil(M / 32) * ceil(Ncols / 64), and the split reduction's second pass
+    // ceil(M * Ncols / 2048) <= that
     return (M + 31) / 32 * ((Ncols + 63) / 64);
+}
+
+namespace {
+
+// Workgroups of the tile launch_gemm_any picks for an M x Ncols product.
+int64_t gemm_tiles(int64_t M, int64_t Ncols) {
+    if (M <= 32) return (Ncols + 255) / 256 >= 512 ? (Ncols + 255) / 256 : (Ncols + 127) / 128;
+    if (M <= 64) return (Ncols + 127) / 128 >= 512 ? (Ncols + 127) / 128 : (Ncols + 63) / 64;
+    return (M + 127) / 128 * ((Ncols + 127) / 128);
+}
+
+// Reduction range per workgroup, 0 for no split: a grid of fewer than 128
+// tiles (small batches: AlexNet-ImageNet conv4 at batch 1 is 3 tiles, each
+// walking all 3456 of C*R*S) splits C*R*S into ranges of at least 256, a
+// multiple of 32 (every K-slice of a range is whole), for a grid of about
+// 256 workgroups, at most 16 ranges.  ISC_GEMM_SPLIT = 0 turns it off (for
+// measurements).
+int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
+    if (const char *env = std::getenv("ISC_GEMM_SPLIT"))
+        if (std::atoi(env) == 0) return 0;
+    const int64_t tiles = gemm_tiles(M, Ncols);
+    if (tiles >= 128) return 0;
+    const int64_t splits = std::min<int64_t>({16, (256 + tiles - 1) / tiles, Kd / 256});
+    if (splits < 2) return 0;
+    return static_cast<int>((Kd + splits - 1) / splits + 31) / 32 * 32;
+}
+
+}  // namespace
+
+size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd) {
+    const int kc = gemm_kchunk(M, Ncols, Kd);
+    if (kc == 0) return 0;
+    return static_cast<size_t>((Kd + kc - 1) / kc) * static_cast<size_t>(M) * static_cast<size_t>(Ncols);
 }
 
 bool conv_gemm_implicit_ok(int C, int R, int S) { return static_cast<int64_t>(C) * R * S < (1 << 16); }
 
 hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
                             int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s,
-                            const Epilogue &epi) {
+                            const Epilogue &epi, float *part) {
     GemmArgs g{};
     g.epi = epi;
+    const int kc = part ? gemm_kchunk(K, static_cast<int64_t>(N) * Ho * Wo, C * R * S) : 0;
+    g.part = kc > 0 ? part : nullptr;
+    g.kchunk = kc;
     g.M = K;
     g.N = N * Ho * Wo;
     g.Kd = C * R * S;

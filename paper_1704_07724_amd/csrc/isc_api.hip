@@ -75,7 +75,7 @@ isc::SparseShape sparse_shape(const Shape &s) {
 }
 
 struct Layout {
-    size_t ctrl = 0, parts = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, total = 0;
+    size_t ctrl = 0, parts = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, split = 0, total = 0;
     bool sparse = false, dense = false;
     bool implicit = false;  // dense path gathers im2col inside the GEMM (no col buffer)
     bool fused = false;     // sparse path compacts on the fly (no lists; the repacked filter only)
@@ -107,6 +107,14 @@ Layout layout_for(const Shape &s, int32_t path) {
     if (L.dense && !L.implicit) {
         L.col = off;
         off = align_up(off + sizeof(float) * static_cast<size_t>(s.crs() * s.ldcol()), kAlign);
+    }
+    // the partial sums of the implicit GEMM's split reduction (small grids)
+    const size_t split = L.dense && L.implicit ? isc::conv_gemm_split_floats(static_cast<int>(s.K), s.ncols(),
+                                                                             static_cast<int>(s.crs()))
+                                               : 0;
+    if (split > 0) {
+        L.split = off;
+        off = align_up(off + sizeof(float) * split, kAlign);
     }
     L.total = off;
     return L;
@@ -278,8 +286,9 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
                           path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
         if (L.implicit) {
             // one launch: the GEMM gathers the im2col matrix from x
+            float *part = L.split ? reinterpret_cast<float *>(base + L.split) : nullptr;
             if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
-                                           sh.Wo, dec, hs, epi)) != hipSuccess)
+                                           sh.Wo, dec, hs, epi, part)) != hipSuccess)
                 return hip_status(e);
         } else {
             float *col = reinterpret_cast<float *>(base + L.col);

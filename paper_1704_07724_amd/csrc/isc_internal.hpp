@@ -118,7 +118,7 @@ __device__ __forceinline__ bool decision_gate(const Decision &d, uint32_t mine) 
     const unsigned long long total = decision_total(d);
     const bool sparse = total != ~0ull && total <= d.nnz_limit;
     const bool run = d.gate == kGateAlways || (d.gate == kGateIfSparse ? sparse : !sparse);
-    if (d.record && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) {
+    if (d.record && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) {
         d.record->nnz_total = total;
         d.record->path_taken = run ? mine : 3u - mine;
     }
@@ -251,9 +251,15 @@ hipError_t launch_gemm_f32(int M, int Ncols, int Kd, const float *a, int64_t lda
 // the im2col matrix gathered from x while loading (C*R*S < 2^16), output
 // scattered to NCHW.
 bool conv_gemm_implicit_ok(int C, int R, int S);
+// part: the partial sums of a split reduction (conv_gemm_split_floats
+// floats), or nullptr for one range.
 hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int C, int H, int W, int K, int R,
                             int S, int T, int P, int Ho, int Wo, const Decision &dec, hipStream_t s,
-                            const Epilogue &epi = Epilogue{});
+                            const Epilogue &epi = Epilogue{}, float *part = nullptr);
+// Floats of the partial sums launch_conv_gemm splits its reduction into for
+// an M x Ncols x Kd product, 0 when it does not split (grids that fill the
+// chip, or short reductions).
+size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd);
 // Upper bound of the GEMM's workgroups for an M x Ncols product (the census
 // slots its epilogue may write).
 int64_t gemm_max_groups(int64_t M, int64_t Ncols);

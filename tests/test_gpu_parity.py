@@ -507,3 +507,32 @@ def test_register_kernel_map_groups(torch, isc, monkeypatch, case):
     assert other in ("fused", "fused_ring"), other
     y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
     assert_conv_close(y, want, "%s kernel %s" % (other, case))
+
+
+@pytest.mark.parametrize("case", [(1, 384, 5, 5, 384, 3, 3, 1, 1, 0.9), (1, 100, 9, 7, 70, 3, 3, 1, 1, 0.5),
+                                  (2, 48, 7, 7, 128, 5, 5, 1, 2, 0.9), (1, 60, 6, 6, 20, 5, 5, 1, 2, 0.3),
+                                  (3, 800, 4, 4, 33, 1, 1, 1, 0, 0.6)])
+def test_dense_split_reduction(torch, isc, monkeypatch, case):
+    """The dense path's GEMM with its reduction split over C*R*S (grids of
+    fewer than 128 tiles): plain, rectified with the census, and under AUTO,
+    against the oracle; and the unsplit GEMM (ISC_GEMM_SPLIT = 0) on the same
+    shape."""
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("dense split", case)
+    desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=91 + sum(case[:9]))
+    want = oracle.conv2d_f64(x, w, T, P)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    ws = isc.workspace(desc, "dense")
+    y = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=ws).cpu().numpy()
+    assert_conv_close(y, want, "dense split %s" % (case,))
+    yc = isc.census(desc)
+    z = isc.isc_conv2d_relu(xd, wd, T, P, path="dense", y_census=yc, ws=ws).cpu().numpy()
+    want_relu, _ = oracle.relu_conv2d_f64(x, w, T, P)
+    assert_conv_close(z, want_relu, "dense split relu %s" % (case,))
+    assert isc.isc_census_read(yc) == (z.size, int(np.count_nonzero(z)))
+    a = isc.isc_conv2d(xd, wd, T, P, path="auto", threshold=0.99, ws=isc.workspace(desc, "auto")).cpu().numpy()
+    assert_conv_close(a, want, "auto (dense) split %s" % (case,))
+    monkeypatch.setenv("ISC_GEMM_SPLIT", "0")
+    u = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=isc.workspace(desc, "dense")).cpu().numpy()
+    assert_conv_close(u, want, "dense unsplit %s" % (case,))
