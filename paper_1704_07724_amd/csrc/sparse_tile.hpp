@@ -153,11 +153,33 @@ __device__ __forceinline__ void walk_mask(unsigned long long mask, int keyv, int
 // straight-line block.  The tests are wave-uniform scalar branches laid out
 // so that an empty group falls through (no fetch redirect), and there is no
 // dependent chain from one nonzero to the next.
+// The ballots as 32-bit halves, each through an opaque move so that the
+// scan's tests stay 32-bit (a 64-bit test of a group inside one half costs
+// a compare and a register move more): a single position is one bit test,
+// a group one AND whose result decides the branch.
+template <int EPL>
+__device__ __forceinline__ void split_mask(const unsigned long long (&mask)[EPL], uint32_t (&mh)[2 * EPL]) {
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+        asm("s_mov_b32 %0, %1" : "=s"(mh[2 * e]) : "s"(static_cast<uint32_t>(mask[e])));
+        asm("s_mov_b32 %0, %1" : "=s"(mh[2 * e + 1]) : "s"(static_cast<uint32_t>(mask[e] >> 32)));
+    }
+}
+
+// Whether any of the N positions from lane L of ballot E are set (N <= 16,
+// L a multiple of N: the group lies inside one half).
+template <int E, int L, int N>
+__device__ __forceinline__ bool group_set(const uint32_t *mh) {
+    static_assert(N <= 16 && (L % 32) + N <= 32, "group crosses the 32-bit halves");
+    constexpr uint32_t g = (N == 32 ? ~0u : ((1u << N) - 1u)) << (L % 32);
+    return (mh[2 * E + L / 32] & g) != 0u;
+}
+
 template <typename SH, int Q>
-__device__ __forceinline__ void scan_one(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+__device__ __forceinline__ void scan_one(const uint32_t (&mh)[2 * SH::EPL], const float (&xv)[SH::EPL],
                                          Acc<SH> &acc, const Wts<SH> &w) {
     constexpr int E = Q / kLanes, L = Q % kLanes;
-    if (__builtin_expect((mask[E] & (1ull << L)) != 0ull, 0)) {
+    if (__builtin_expect((mh[2 * E + L / 32] & (1u << (L % 32))) != 0u, 0)) {
         const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xv[E]), L));
         leaf<SH, Q / SH::WCOLS, Q % SH::WCOLS>(acc, w, v);
     }
@@ -166,20 +188,19 @@ __device__ __forceinline__ void scan_one(const unsigned long long (&mask)[SH::EP
 // Positions [Q0, Q0 + G) (G a power of two dividing 64, clipped to the
 // window), then the next level down.
 template <typename SH, int Q0, int G>
-__device__ __forceinline__ void scan_group(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
+__device__ __forceinline__ void scan_group(const uint32_t (&mh)[2 * SH::EPL], const float (&xv)[SH::EPL],
                                            Acc<SH> &acc, const Wts<SH> &w) {
     constexpr int NQ = SH::WROWS * SH::WCOLS;
     if constexpr (Q0 < NQ) {
         if constexpr (G == 1) {
-            scan_one<SH, Q0>(mask, xv, acc, w);
+            scan_one<SH, Q0>(mh, xv, acc, w);
         } else {
             constexpr int E = Q0 / kLanes, L = Q0 % kLanes;
             constexpr int N = (NQ - Q0) < G ? (NQ - Q0) : G;
-            constexpr unsigned long long gm = (N == 64 ? ~0ull : ((1ull << N) - 1)) << L;
-            if (__builtin_expect((mask[E] & gm) != 0ull, 0)) {
+            if (__builtin_expect(group_set<E, L, N>(mh), 0)) {
                 constexpr int G2 = G == 16 ? 4 : 1;
                 static_for<0, G / G2>([&](auto ic) {
-                    scan_group<SH, Q0 + decltype(ic)::value * G2, G2>(mask, xv, acc, w);
+                    scan_group<SH, Q0 + decltype(ic)::value * G2, G2>(mh, xv, acc, w);
                 });
             }
         }
@@ -190,37 +211,36 @@ template <typename SH>
 __device__ __forceinline__ void walk_scan(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
                                           Acc<SH> &acc, const Wts<SH> &w) {
     constexpr int NQ = SH::WROWS * SH::WCOLS;
-    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group<SH, decltype(gc)::value * 16, 16>(mask, xv, acc, w); });
+    uint32_t mh[2 * SH::EPL];
+    split_mask<SH::EPL>(mask, mh);
+    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group<SH, decltype(gc)::value * 16, 16>(mh, xv, acc, w); });
 }
 
 // The same static scan with the block of a set position supplied by the
 // caller: blk(integral_constant<WY>, integral_constant<XP>, v) for a nonzero v
 // at window row WY, shifted column XP (the weight-gradient kernel's leaves).
 template <typename SH, int Q, typename Blk>
-__device__ __forceinline__ void scan_one_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
-                                           Blk &blk) {
+__device__ __forceinline__ void scan_one_f(const uint32_t (&mh)[2 * SH::EPL], const float (&xv)[SH::EPL], Blk &blk) {
     constexpr int E = Q / kLanes, L = Q % kLanes;
-    if (__builtin_expect((mask[E] & (1ull << L)) != 0ull, 0)) {
+    if (__builtin_expect((mh[2 * E + L / 32] & (1u << (L % 32))) != 0u, 0)) {
         const float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xv[E]), L));
         blk(std::integral_constant<int, Q / SH::WCOLS>{}, std::integral_constant<int, Q % SH::WCOLS>{}, v);
     }
 }
 
 template <typename SH, int Q0, int G, typename Blk>
-__device__ __forceinline__ void scan_group_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
-                                             Blk &blk) {
+__device__ __forceinline__ void scan_group_f(const uint32_t (&mh)[2 * SH::EPL], const float (&xv)[SH::EPL], Blk &blk) {
     constexpr int NQ = SH::WROWS * SH::WCOLS;
     if constexpr (Q0 < NQ) {
         if constexpr (G == 1) {
-            scan_one_f<SH, Q0>(mask, xv, blk);
+            scan_one_f<SH, Q0>(mh, xv, blk);
         } else {
             constexpr int E = Q0 / kLanes, L = Q0 % kLanes;
             constexpr int N = (NQ - Q0) < G ? (NQ - Q0) : G;
-            constexpr unsigned long long gm = (N == 64 ? ~0ull : ((1ull << N) - 1)) << L;
-            if (__builtin_expect((mask[E] & gm) != 0ull, 0)) {
+            if (__builtin_expect(group_set<E, L, N>(mh), 0)) {
                 constexpr int G2 = G == 16 ? 4 : 1;
                 static_for<0, G / G2>([&](auto ic) {
-                    scan_group_f<SH, Q0 + decltype(ic)::value * G2, G2>(mask, xv, blk);
+                    scan_group_f<SH, Q0 + decltype(ic)::value * G2, G2>(mh, xv, blk);
                 });
             }
         }
@@ -231,7 +251,9 @@ template <typename SH, typename Blk>
 __device__ __forceinline__ void walk_scan_f(const unsigned long long (&mask)[SH::EPL], const float (&xv)[SH::EPL],
                                             Blk &blk) {
     constexpr int NQ = SH::WROWS * SH::WCOLS;
-    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group_f<SH, decltype(gc)::value * 16, 16>(mask, xv, blk); });
+    uint32_t mh[2 * SH::EPL];
+    split_mask<SH::EPL>(mask, mh);
+    static_for<0, (NQ + 15) / 16>([&](auto gc) { scan_group_f<SH, decltype(gc)::value * 16, 16>(mh, xv, blk); });
 }
 
 // Load one channel's weights for this lane: w[r][s][j] = wc[(r*S+s)*ld + lane*KPL + j]
