@@ -249,3 +249,21 @@ def test_dw_entry_validation():
     except Exception:
         pass
     assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n, None) == 7       # no gfx950 here
+
+
+def test_dense_split_workspace(monkeypatch):
+    """Host plan of the dense GEMM's split reduction: a grid under 128 tiles
+    splits C*R*S into ranges of at least 256 (multiples of 32, at most 16)
+    and the workspace holds ranges x K x N*Ho*Wo partial sums; grids that
+    fill the chip, or short reductions, do not split."""
+    d = isc.make_desc(1, 384, 5, 5, 384, 3, 3, 1, 1)     # 3 tiles, C*R*S 3456
+    monkeypatch.setenv("ISC_GEMM_SPLIT", "0")
+    base = isc.isc_workspace_size(d, "dense")
+    monkeypatch.delenv("ISC_GEMM_SPLIT")
+    split = isc.isc_workspace_size(d, "dense")
+    # min(16, ceil(256 / 3), 3456 // 256) = 13 ranges asked -> ranges of 288 -> 12 ranges
+    assert split - base == 12 * 384 * 25 * 4
+    lenet = isc.make_desc(256, 20, 12, 12, 50, 5, 5, 1, 0)  # 256 tiles of 64 x 64
+    assert isc.isc_workspace_size(lenet, "dense") == base
+    short = isc.make_desc(3, 500, 4, 4, 33, 1, 1, 1, 0)   # C*R*S 500 < 2 * 256
+    assert isc.isc_workspace_size(short, "dense") == base
