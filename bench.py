@@ -6,20 +6,29 @@
 A step is one pass of the whole hot path over one batch of synthetic input
 already resident in HBM: isc_conv2d on the AUTO path, i.e. the nonzero count
 of the input and the device-side sparse/dense decision, then the
-zero-skipping convolution (ISC steps 1-3: compaction on the fly for this
-layer, the multiply-adds over nonzeros only, the write-out to NCHW); the
-dense kernel is launched too and exits on the decision.  Steps are replayed
-from a HIP graph (the layer is launch-bound at microseconds per step).
+zero-skipping convolution (ISC steps 1-3: compaction on the fly, the
+multiply-adds over nonzeros only, the write-out to NCHW); the dense kernel is
+launched too and exits on the decision.
 
-Workload: LeNet conv2 (20 -> 50 maps, 12 x 12, 5 x 5, stride 1, no pad) at
-batch 256, input sparsity 0.9 (i.i.d. zeros, |N(0,1)| nonzeros, N(0, 0.1)
-weights), the sweep configuration whose 0.9 point the metric is quoted at.
+Workload: AlexNet conv2 (96 -> 256 maps, 27 x 27, 5 x 5, pad 2) at batch 128,
+input sparsity 0.9 (i.i.d. zeros, |N(0,1)| nonzeros, N(0, 0.01) weights): the
+largest single-GPU configuration at the sparsity the metric is quoted at.
+
+Timing protocol: each timed step (and each rep of every other figure) runs
+after a 512 MiB write that evicts the caches (twice the 256 MB last-level
+cache), outside the interval timed by HIP events on the launch stream; a
+step is replayed from a HIP graph whose launches are queued behind that
+write, so host-side enqueue time never enters the interval.  `value` is the
+dense-equivalent rate at the median of the K cold steps (p10 / p90 beside
+it); the warm figures (back-to-back replays, caches hot) come alongside.
 
 Prints ONE JSON line: value = dense-equivalent TFLOP/s of the step
 (2*N*K*C*R*S*Ho*Wo per step), speedup against the same GPU's dense path
-(fp32-MFMA GEMM with the im2col gather inside), the sparsity sweep 0.5 .. 0.99, the roofline of
-the dominant kernel (timed with HIP events on the launch stream), and the
-CPU oracle timed on a bounded sample of the same workload.
+(fp32-MFMA GEMM with the im2col gather inside) and against the vendor
+library's fp32 convolution, nonzero-MAC/s, the LeNet conv2 sparsity sweep
+0.5 .. 0.99 with roofline fractions per point, the roofline of the dominant
+kernel (HIP events on the launch stream), and the CPU oracle timed on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -68,6 +77,45 @@ def nonzero_macs(x, layer, Ho, Wo) -> int:
     ty = taps_per_coord(layer.H, layer.R, layer.P, layer.T, Ho)
     tx = taps_per_coord(layer.W, layer.S, layer.P, layer.T, Wo)
     return int(layer.K * (per_pos * ty[:, None] * tx[None, :]).sum())
+
+
+FLUSH_BYTES = 512 << 20   # twice the 256 MB last-level cache (MALL)
+
+
+class ColdTimer:
+    """Per-rep HIP-event times with the caches evicted before every rep: a
+    512 MiB write, then the start event, the work, the end event, all on the
+    current stream with no host synchronisation in between (so the work's
+    launches wait queued behind the write)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        self.count = 0
+
+    def flush(self):
+        self.count += 1
+        self.buf.fill_(float(self.count & 0xFFFF))
+
+    def times(self, fn, reps: int, warm: int = 2):
+        torch = self.torch
+        evs = []
+        for i in range(warm + reps):
+            self.flush()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs[warm:]]
+
+
+def stats(ms) -> dict:
+    """Median, p10, p90 and mean of per-rep milliseconds."""
+    a = np.asarray(ms, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 6), "p10": round(float(np.percentile(a, 10)), 6),
+            "p90": round(float(np.percentile(a, 90)), 6), "mean": round(float(a.mean()), 6), "reps": int(a.size)}
 
 
 def event_time_ms(torch, fn, reps: int, warm: int = 3) -> float:
@@ -132,10 +180,10 @@ class LayerRun:
         self.flops = dense_flops(L, self.Ho, self.Wo)
         self.nz_macs = nonzero_macs(x, L, self.Ho, self.Wo)
 
-    def conv(self, path):
+    def conv(self, path, threshold=None):
         L = self.layer
-        return lambda: self.isc.isc_conv2d(self.x, self.w, L.T, L.P, path=path, out=self.y,
-                                           ws=self.ws[path])
+        return lambda: self.isc.isc_conv2d(self.x, self.w, L.T, L.P, path=path, threshold=threshold,
+                                           out=self.y, ws=self.ws[path])
 
     def compact(self):
         return lambda: self.isc.isc_compact(self.x, out=self.lists)
@@ -158,21 +206,24 @@ class LayerRun:
             self.col = self.torch.empty((L.C * L.R * L.S, L.N * self.Ho * self.Wo), device="cuda")
         return lambda: self.isc.isc_im2col(self.x, L.R, L.S, L.T, L.P, out=self.col)
 
-    def measure(self, steps, warmup, graphs=True):
+    def measure(self, cold, reps, graphs=True):
+        """Cold medians (t_*_ms, with p10/p90 in t_*) and warm averages
+        (warm_*_ms) of the three paths, the stand-alone compaction and the
+        sparse path's main kernel alone."""
         torch = self.torch
         res = {}
-        for path in ("auto", "sparse", "dense"):
-            fn = self.conv(path)
+        fns = {"auto": self.conv("auto"), "sparse": self.conv("sparse"), "dense": self.conv("dense"),
+               "compact": self.compact(), "sparse_kernel": self.sparse_kernel()}
+        for name, fn in fns.items():
             if graphs:
-                g = graph_of(torch, fn)
-                fn = g.replay
-            res["t_%s_ms" % path] = event_time_ms(torch, fn, steps, warmup)
-        reps = max(100, steps)
-        res["t_compact_ms"] = kernel_time_ms(torch, self.compact(), reps, graphs)
-        res["t_sparse_kernel_ms"] = kernel_time_ms(torch, self.sparse_kernel(), reps, graphs)
+                fn = graph_of(torch, fn).replay
+            st = stats(cold.times(fn, reps))
+            res["t_%s_ms" % name] = st["median"]
+            res["t_%s" % name] = st
+            res["warm_%s_ms" % name] = round(event_time_ms(torch, fn, max(20, reps)), 6)
         return res
 
-    def measure_dw(self, steps, warmup, graphs=True):
+    def measure_dw(self, cold, reps, graphs=True):
         """The weight gradient (training) on this layer's input with a random
         output gradient: the zero-skipping kernel (isc_conv2d_dw, graph
         replayed) against torch's GPU weight gradient of the same
@@ -189,25 +240,31 @@ class LayerRun:
         ws = torch.empty(max(nbytes, 1), dtype=torch.uint8, device="cuda")
         dw = torch.empty((L.K, L.C, L.R, L.S), device="cuda")
         fn = lambda: isc.isc_conv2d_dw(self.x, dy, L.R, L.S, L.T, L.P, out=dw, ws=ws)
-        res = {"t_dw_sparse_ms": kernel_time_ms(torch, fn, max(20, steps), graphs, inner=5)}
+        if graphs:
+            fn = graph_of(torch, fn).replay
+        res = {"t_dw_sparse_ms": stats(cold.times(fn, reps))["median"]}
         ref = lambda: torch.nn.grad.conv2d_weight(self.x, (L.K, L.C, L.R, L.S), dy, stride=L.T, padding=L.P)
-        res["t_dw_library_ms"] = event_time_ms(torch, ref, max(20, steps), warmup)
+        ref()
+        res["t_dw_library_ms"] = stats(cold.times(ref, reps))["median"]
         res["speedup_dw_vs_library"] = round(res["t_dw_library_ms"] / res["t_dw_sparse_ms"], 3)
         res["dw_tflops_nonzero"] = round(2 * self.nz_macs / (res["t_dw_sparse_ms"] * 1e-3) / 1e12, 3)
         res["dw_tflops_dense_equiv"] = round(self.flops / (res["t_dw_sparse_ms"] * 1e-3) / 1e12, 3)
         del dy, ws, dw
         return res
 
-    def measure_library(self, steps, warmup, t_sparse_ms):
+    def measure_library(self, cold, reps, t_sparse_ms):
         """The vendor library's forward convolution of the same layer (torch's
         GPU conv2d in fp32, TF32 off, eager), a second dense reference beside
-        this library's own dense path."""
+        this library's own dense path: cold median and warm average."""
         torch, L = self.torch, self.layer
         torch.backends.cudnn.allow_tf32 = False
         torch.backends.cuda.matmul.allow_tf32 = False
         fn = lambda: torch.nn.functional.conv2d(self.x, self.w, stride=L.T, padding=L.P)
-        t = event_time_ms(torch, fn, max(20, steps), warmup)
-        return {"t_library_ms": t, "speedup_sparse_vs_library": round(t / t_sparse_ms, 3)}
+        fn()  # the library's algorithm search, outside every timing
+        st = stats(cold.times(fn, reps))
+        return {"t_library_ms": st["median"], "t_library": st,
+                "warm_library_ms": round(event_time_ms(torch, fn, max(20, reps)), 6),
+                "speedup_sparse_vs_library": round(st["median"] / t_sparse_ms, 3)}
 
     def summary(self, res):
         f, nzm = self.flops, self.nz_macs
@@ -219,13 +276,14 @@ class LayerRun:
             "dense_gflop": round(f / 1e9, 4), "nonzero_macs": nzm,
         }
         for k, v in res.items():
-            out[k] = round(v, 6)
+            out[k] = round(v, 6) if isinstance(v, float) else v
         for path in ("auto", "sparse", "dense"):
             out["tflops_%s" % path] = round(f / (res["t_%s_ms" % path] * 1e-3) / 1e12, 3)
         out["nonzero_mac_per_s_auto"] = nzm / (res["t_auto_ms"] * 1e-3)
         out["speedup_auto_vs_dense"] = round(res["t_dense_ms"] / res["t_auto_ms"], 3)
         out["speedup_sparse_vs_dense"] = round(res["t_dense_ms"] / res["t_sparse_ms"], 3)
         out["sparse_kernel_tflops_nonzero"] = round(2 * nzm / (res["t_sparse_kernel_ms"] * 1e-3) / 1e12, 3)
+        out["sparse_kernel_frac_valu_peak"] = round(out["sparse_kernel_tflops_nonzero"] / VALU_F32_PEAK_TFLOPS, 4)
         out["dense_frac_mfma_peak"] = round(f / (res["t_dense_ms"] * 1e-3) / 1e12 / MFMA_F32_PEAK_TFLOPS, 4)
         return out
 
@@ -263,7 +321,7 @@ class ChainRun:
         def run():
             x, xc = self.x0, None
             for i in range(len(L)):
-                isc.isc_conv2d_relu(x, self.w[i], L[i].T, L[i].P, x_census=xc, wt=self.wt[i],
+                isc.isc_conv2d_relu(x, self.w[i], L[i].T, L[i].P, path="auto", x_census=xc, wt=self.wt[i],
                                     y_census=self.census[i], out=self.ys[i], ws=self.ws[i]["auto"])
                 x, xc = self.ys[i], self.census[i]
         return run
@@ -274,7 +332,7 @@ class ChainRun:
         def run():
             x = self.x0
             for i in range(len(L)):
-                isc.isc_conv2d(x, self.w[i], L[i].T, L[i].P, out=self.ys[i], ws=self.ws[i]["auto"])
+                isc.isc_conv2d(x, self.w[i], L[i].T, L[i].P, path="auto", out=self.ys[i], ws=self.ws[i]["auto"])
                 torch.relu_(self.ys[i])
                 x = self.ys[i]
         return run
@@ -290,14 +348,17 @@ class ChainRun:
                 x = self.ys[i]
         return run
 
-    def measure(self, steps, warmup, graphs=True):
+    def measure(self, cold, reps, graphs=True):
         torch = self.torch
         res = {}
         for name in ("fused", "separate", "dense"):
             fn = getattr(self, name)()
             if graphs:
                 fn = graph_of(torch, fn).replay
-            res["t_chain_%s_ms" % name] = event_time_ms(torch, fn, steps, warmup)
+            st = stats(cold.times(fn, reps))
+            res["t_chain_%s_ms" % name] = st["median"]
+            res["t_chain_%s" % name] = st
+            res["warm_chain_%s_ms" % name] = round(event_time_ms(torch, fn, max(20, reps)), 6)
         # the activations of the fused run (the last one timed wrote the
         # dense run's outputs, equal up to rounding): run it once more
         self.fused()()
@@ -364,37 +425,47 @@ def cpu_baseline(layer, budget_s=10.0):
             "cpu_model": _cpu_model()}
 
 
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "lenet_conv2_s0.9_hbm_counters.md")
-SPARSE_SOURCES = [os.path.join(ROOT, "paper_1704_07724_amd", "csrc", f)
-                  for f in ("sparse_fused.hpp", "sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp")]
+CSRC = os.path.join(ROOT, "paper_1704_07724_amd", "csrc")
+# the sources of each sparse kernel (a counter summary holds only while they hash the same)
+KERNEL_SOURCES = {
+    "fused": ("sparse_fused.hpp", "sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp"),
+    "fused_reg": ("sparse_fused.hpp", "sparse_fused.hip", "sparse_tile.hpp", "isc_internal.hpp"),
+    "fused_ring": ("sparse_fring.hpp", "sparse_fring.hip", "sparse_tile.hpp", "isc_internal.hpp"),
+}
 
 
-def sparse_source_hash() -> str:
-    """First 16 hex digits of the SHA-256 of the headline sparse kernel's
-    sources, concatenated in SPARSE_SOURCES order."""
+def counters_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", "%s_hbm_counters.md" % workload)
+
+
+def sparse_source_hash(kernel: str) -> str:
+    """First 16 hex digits of the SHA-256 of a sparse kernel's sources,
+    concatenated in KERNEL_SOURCES order."""
     import hashlib
     h = hashlib.sha256()
-    for f in SPARSE_SOURCES:
-        with open(f, "rb") as fh:
+    for f in KERNEL_SOURCES.get(kernel, ()):
+        with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def counted_traffic():
+def counted_traffic(workload: str, kernel: str):
     """HBM bytes per launch of the sparse kernel from the committed counter
-    summary (FETCH_SIZE and WRITE_SIZE scaled by a copy kernel), or None when
-    the kernel's sources have changed since the counters were taken."""
+    summary of the workload (FETCH_SIZE and WRITE_SIZE scaled by a copy
+    kernel), or None when the kernel's sources have changed since the
+    counters were taken."""
     import re
+    path = counters_file(workload)
     try:
-        text = open(COUNTERS_FILE).read()
+        text = open(path).read()
     except OSError:
         return None
     m = re.search(r"^traffic_bytes_per_launch (\S+): read=(\d+) write=(\d+) source_sha256=([0-9a-f]+)",
                   text, re.M)
-    if not m or m.group(4) != sparse_source_hash():
+    if not m or m.group(4) != sparse_source_hash(kernel):
         return None
     return {"kernel": m.group(1), "read_bytes": int(m.group(2)), "write_bytes": int(m.group(3)),
-            "bytes": int(m.group(2)) + int(m.group(3)), "source": os.path.relpath(COUNTERS_FILE, ROOT)}
+            "bytes": int(m.group(2)) + int(m.group(3)), "source": os.path.relpath(path, ROOT)}
 
 
 def algorithmic_bytes(run) -> dict:
@@ -430,22 +501,27 @@ def algorithmic_bytes(run) -> dict:
 def probe(torch, isc, layer, n):
     """Short eager program for counter runs: a copy kernel moving a known
     number of bytes (the scale of the HBM counters), then n launches each of
-    the sparse kernel alone, the whole AUTO step (count and repack, sparse
-    kernel, the dense kernel that exits on the decision) and the dense path."""
+    the sparse kernel alone, the stand-alone compaction, the whole AUTO step
+    (count and repack, sparse kernel, the dense kernel that exits on the
+    decision) and the dense path, each launch after the 512 MiB cache-evicting
+    write (so the counters see cold traffic)."""
     run = LayerRun(torch, isc, layer)
+    cold = ColdTimer(torch)
     src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")  # 256 MiB
     dst = torch.empty_like(src)
     steps = [("copy", lambda: torch.mul(src, 1.0, out=dst)), ("sparse_kernel", run.sparse_kernel()),
-             ("auto", run.conv("auto")), ("dense", run.conv("dense"))]
+             ("compact", run.compact()), ("auto", run.conv("auto")), ("dense", run.conv("dense"))]
     for name, fn in steps:
         for _ in range(n):
+            cold.flush()
             fn()
         torch.cuda.synchronize()
         print("# probe %s x%d done" % (name, n), file=sys.stderr, flush=True)
     alg = algorithmic_bytes(run)
     alg["copy"] = {"read": src.numel() * 4, "write": dst.numel() * 4}
-    print(json.dumps({"probe": layer.name, "launches_each": n, "nnz": run.nnz,
-                      "algorithmic_bytes": alg}), flush=True)
+    print(json.dumps({"probe": layer.name, "kernel": run.kernel, "launches_each": n, "nnz": run.nnz,
+                      "nonzero_macs": run.nz_macs, "algorithmic_bytes": alg,
+                      "source_sha256": sparse_source_hash(run.kernel)}), flush=True)
 
 
 def _cpu_model():
@@ -458,16 +534,33 @@ def _cpu_model():
     return None
 
 
+def sweep_point(torch, isc, cold, layer, reps, graphs, run=None):
+    """One point of a sparsity sweep: cold medians of the three paths and of
+    the sparse kernel alone, rates and roofline fractions."""
+    run = run or LayerRun(torch, isc, layer)
+    sm = run.summary(run.measure(cold, reps, graphs))
+    keep = ("target_sparsity", "measured_sparsity", "t_auto_ms", "t_sparse_ms", "t_dense_ms",
+            "t_compact_ms", "t_sparse_kernel_ms", "warm_auto_ms", "warm_sparse_kernel_ms", "tflops_auto",
+            "tflops_sparse", "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense",
+            "speedup_sparse_vs_dense", "sparse_kernel_tflops_nonzero", "sparse_kernel_frac_valu_peak",
+            "dense_frac_mfma_peak")
+    out = {k: sm[k] for k in keep}
+    _, out["auto_path"] = isc.isc_decision(run.desc, run.ws["auto"])
+    out["sparse_kernel"] = run.kernel
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[1])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-graph", action="store_true", help="launch eagerly instead of graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--all", action="store_true", help="also measure every workload layer")
     ap.add_argument("--out", default=None, help="JSONL file for --all rows")
+    ap.add_argument("--workload", default="alexnet_conv2", help="headline workload (a workloads.py layer name)")
     ap.add_argument("--probe", type=int, default=0, metavar="N",
                     help="only launch each kernel of the headline layer N times, eagerly, after "
                          "a copy kernel of known size, and print their algorithmic bytes "
@@ -486,40 +579,52 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
 
-    sweep_layers = workloads.WORKLOADS["lenet_conv2_batch"].layers
-    head_layer = [l for l in sweep_layers if l.sparsity == 0.9][0]
+    layers = {l.name: l for wl in workloads.WORKLOADS.values() for l in wl.layers}
+    head_layer = layers[args.workload]
     if args.probe:
         probe(torch, isc, head_layer, args.probe)
         return
+    graphs = not args.no_graph
+    cold = ColdTimer(torch)
 
-    # headline: whole hot path, AUTO, K timed steps bracketed by synchronize
+    # headline: whole hot path, AUTO with the library's default threshold,
+    # K cold steps bracketed by synchronize; each timed by HIP events
     head = LayerRun(torch, isc, head_layer)
     step_fn = head.conv("auto")
-    if not args.no_graph:
+    if graphs:
         step_fn = graph_of(torch, step_fn).replay
-    for _ in range(args.warmup):
-        step_fn()
+    cold.times(step_fn, args.warmup, warm=0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step_fn()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed * 1e3 / args.steps
+    step_ms = cold.times(step_fn, args.steps, warm=0)
+    wall_s = time.perf_counter() - t0
+    st = stats(step_ms)
+    ms_per_step = st["median"]
     value = head.flops / (ms_per_step * 1e-3) / 1e12
+    _, head_path = isc.isc_decision(head.desc, head.ws["auto"])
+    print("# headline %s: AUTO (%s) cold median %.4f ms (p10 %.4f, p90 %.4f)" % (
+        head_layer.name, head_path, st["median"], st["p10"], st["p90"]), file=sys.stderr, flush=True)
 
-    res = head.measure(args.steps, args.warmup, graphs=not args.no_graph)
+    reps = max(10, args.steps)
+    res = head.measure(cold, reps, graphs)
     hs = head.summary(res)
-    lib = head.measure_library(args.steps, args.warmup, res["t_sparse_ms"])
-    t_kernel = res["t_sparse_kernel_ms"]
+    lib = head.measure_library(cold, reps, ms_per_step)
+    print("# paths: sparse %.4f dense %.4f library %.4f ms; sparse kernel %.4f ms" % (
+        res["t_sparse_ms"], res["t_dense_ms"], lib["t_library_ms"], res["t_sparse_kernel_ms"]),
+        file=sys.stderr, flush=True)
+
+    # the dominant kernel: the sparse kernel alone, average of its cold launches
+    t_kernel = res["t_sparse_kernel"]["mean"]
     achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
-    traffic = counted_traffic()
+    traffic = counted_traffic(head_layer.name, head.kernel)
     roofline = {"bound": "alu", "kernel": "sparse_conv_%s_kernel" % head.kernel,
                 "achieved": round(achieved, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4),
                 "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
                 "per_launch": {"nonzero_macs": head.nz_macs, "flops": 2 * head.nz_macs,
-                               "avg_duration_ms": round(t_kernel, 6)},
+                               "avg_duration_ms": round(t_kernel, 6),
+                               "median_duration_ms": res["t_sparse_kernel"]["median"],
+                               "warm_avg_duration_ms": res["warm_sparse_kernel_ms"]},
                 "frac_vs_packed_peak": round(achieved / VALU_F32_PACKED_PEAK_TFLOPS, 4)}
 
     alg = algorithmic_bytes(head)
@@ -531,40 +636,41 @@ def main():
 
     sweep = []
     if not args.no_sweep:
-        for layer in sweep_layers:
-            run = head if layer is head_layer else LayerRun(torch, isc, layer)
-            r = res if layer is head_layer else run.measure(max(50, args.steps // 2), 10,
-                                                            graphs=not args.no_graph)
-            s = run.summary(r)
-            sweep.append({k: s[k] for k in (
-                "target_sparsity", "measured_sparsity", "t_auto_ms", "t_sparse_ms", "t_dense_ms",
-                "t_compact_ms", "t_sparse_kernel_ms", "tflops_auto", "tflops_sparse",
-                "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense",
-                "speedup_sparse_vs_dense", "sparse_kernel_tflops_nonzero")})
-            if run is not head:
-                del run
-                torch.cuda.empty_cache()
+        for layer in workloads.WORKLOADS["lenet_conv2_batch"].layers:
+            pt = sweep_point(torch, isc, cold, layer, max(10, args.steps // 2), graphs)
+            sweep.append(pt)
+            print("# sweep %s: auto %.4f sparse %.4f dense %.4f ms (%s)" % (
+                layer.name, pt["t_auto_ms"], pt["t_sparse_ms"], pt["t_dense_ms"], pt["auto_path"]),
+                file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
 
     line = {
         "metric": METRIC, "value": round(value, 4), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 6),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "lenet_conv2_batch", "N": head_layer.N, "C": head_layer.C,
+        "config": {"workload": head_layer.name, "N": head_layer.N, "C": head_layer.C,
                    "H": head_layer.H, "W": head_layer.W, "K": head_layer.K, "R": head_layer.R,
                    "S": head_layer.S, "stride": head_layer.T, "pad": head_layer.P,
-                   "sparsity": head_layer.sparsity, "path": "auto", "threshold": 0.9,
-                   "launch": "eager" if args.no_graph else "hip_graph"},
-        "speedup_vs_dense": hs["speedup_auto_vs_dense"],
-        "nonzero_mac_per_s": hs["nonzero_mac_per_s_auto"],
+                   "sparsity": head_layer.sparsity, "path": "auto",
+                   "threshold": "per-shape crossover" if isc.default_threshold() < 0 else isc.default_threshold(),
+                   "launch": "eager" if not graphs else "hip_graph", "caches": "cold (512 MiB flush per step)"},
+        "step_ms": st,
+        "wall_s_timed_steps": round(wall_s, 4),
+        "auto_path": head_path,
+        "speedup_vs_dense": round(res["t_dense_ms"] / ms_per_step, 3),
+        "speedup_vs_library": round(lib["t_library_ms"] / ms_per_step, 3),
+        "nonzero_mac_per_s": head.nz_macs / (ms_per_step * 1e-3),
         "measured_sparsity": hs["measured_sparsity"],
         "dense_path_tflops": hs["tflops_dense"],
-        # the vendor library's fp32 forward convolution of the same layer
-        "library_conv2d_ms": round(lib["t_library_ms"], 6),
-        "speedup_vs_library": round(lib["t_library_ms"] / ms_per_step, 3),
+        "dense_frac_mfma_peak": hs["dense_frac_mfma_peak"],
+        "library_conv2d_ms": lib["t_library_ms"],
+        "warm": {"auto_ms": res["warm_auto_ms"], "sparse_ms": res["warm_sparse_ms"],
+                 "dense_ms": res["warm_dense_ms"], "library_ms": lib["warm_library_ms"],
+                 "tflops_auto": round(head.flops / (res["warm_auto_ms"] * 1e-3) / 1e12, 3)},
         "roofline": roofline,
         "hbm": hbm,
-        "timings_ms": {k: hs[k] for k in hs if k.startswith("t_")},
+        "timings_ms": {k: hs[k] for k in hs if k.startswith("t_") and isinstance(hs[k], float)},
         "sweep": sweep,
     }
     if not args.no_cpu_baseline:
@@ -575,7 +681,7 @@ def main():
         for wl in workloads.WORKLOADS.values():
             if wl.name == "alexnet_chain345":
                 chain = ChainRun(torch, isc, wl)
-                r = chain.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph)
+                r = chain.measure(cold, max(10, args.steps // 2), graphs)
                 r["workload"] = wl.name
                 rows.append(r)
                 print("# %s: fused %.4f ms separate %.4f dense %.4f (fused vs separate %.2fx, vs dense %.2fx) "
@@ -590,15 +696,16 @@ def main():
                 if wl.name == "lenet_conv2_batch":
                     continue
                 run = LayerRun(torch, isc, layer)
-                s = run.summary(run.measure(max(20, args.steps // 4), 5, graphs=not args.no_graph))
-                s.update(run.measure_dw(max(20, args.steps // 4), 5, graphs=not args.no_graph))
-                s.update(run.measure_library(max(20, args.steps // 4), 5, s["t_sparse_ms"]))
+                s = run.summary(run.measure(cold, max(10, args.steps // 2), graphs))
+                _, s["auto_path"] = isc.isc_decision(run.desc, run.ws["auto"])
+                s.update(run.measure_dw(cold, max(10, args.steps // 2), graphs))
+                s.update(run.measure_library(cold, max(10, args.steps // 2), s["t_sparse_ms"]))
                 rows.append(s)
                 dws = (" | dw sparse %.4f ms library %.4f (%.2fx)" % (
                     s["t_dw_sparse_ms"], s["t_dw_library_ms"], s["speedup_dw_vs_library"])
                        if "t_dw_sparse_ms" in s else "")
-                print("# %s: auto %.4f ms sparse %.4f dense %.4f speedup %.2fx library %.4f (%.2fx)%s" % (
-                    layer.name, s["t_auto_ms"], s["t_sparse_ms"], s["t_dense_ms"],
+                print("# %s: auto %.4f ms (%s) sparse %.4f dense %.4f speedup %.2fx library %.4f (%.2fx)%s" % (
+                    layer.name, s["t_auto_ms"], s["auto_path"], s["t_sparse_ms"], s["t_dense_ms"],
                     s["speedup_sparse_vs_dense"], s["t_library_ms"], s["speedup_sparse_vs_library"], dws),
                       file=sys.stderr, flush=True)
                 del run

@@ -87,6 +87,30 @@ enum isc_status {
     ISC_ERR_ARG = 10       /* other bad argument (threshold outside [0,1], ...) */
 };
 
+/* Per-call plan overrides, in the manner of a DNN library's per-call
+ * algorithm argument, for measurements and tests.  Every field 0 means "the
+ * library chooses"; a forced value the shape cannot take is ignored (the
+ * library's own choice runs), so isc_sparse_plan reports what a call would
+ * actually run.  A NULL pointer stands for all zeros.  Nothing in the
+ * environment changes a plan: the library reads no environment variables. */
+typedef struct isc_tuning {
+    int32_t kernel;        /* sparse kernel (an isc_kernel value) to run when it
+                              takes the shape */
+    int32_t rows;          /* output rows of a wavefront's tile */
+    int32_t cols;          /* output columns of a wavefront's tile */
+    int32_t maps_per_lane; /* output maps per lane (64 * this per wavefront) */
+    int32_t phases;        /* channel phases of the filter-resident kernel */
+    int32_t wide_loads;    /* 1: the register-weight kernel loads its weights
+                              through a buffer resource on one map group too */
+    int32_t gemm_split;    /* -1: the dense GEMM never splits its reduction */
+    int32_t reserved;      /* must be 0 */
+} isc_tuning;
+
+/* threshold value that asks AUTO for the library's per-shape crossover (the
+ * sparsity at which the zero-skipping path starts to beat the dense path for
+ * this shape on this GPU) instead of a fixed sparsity. */
+#define ISC_THRESHOLD_CROSSOVER (-1.0f)
+
 /* Output extent (Sec. "Sparsity of ReLUs" output-size formula, read as
  * floor((H + 2P - R)/T) + 1; the printed (H + 2P - R + 1)/T agrees at T = 1).
  * Host-only.  Ho/Wo receive the sizes.  Errors: NULL, SHAPE. */
@@ -107,9 +131,11 @@ int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes);
  *     bytes, 256-byte aligned; contents on entry are ignored.
  *   path: isc_path.  threshold: the sparsity (fraction of zero inputs,
  *     Sec. "Sparse Convolution") at or above which AUTO takes the sparse
- *     path; the paper's experiments use 0.9 (Abstract, Sec. "Experiments").
- *     The decision is made on the device from the compaction's count, with no
- *     host synchronisation; isc_decision reads it back.
+ *     path (the paper's experiments use 0.9: Abstract, Sec. "Experiments"),
+ *     or ISC_THRESHOLD_CROSSOVER for the library's per-shape crossover.
+ *     The decision is made on the device from the count of the input's
+ *     nonzeros, with no host synchronisation; isc_decision and
+ *     isc_read_decision read it back.
  *   stream: hipStream_t or NULL.
  * A value counts as zero iff its bits with the sign cleared are zero.
  * fp32 throughout; the sparse path accumulates in fp32 in an order of its
@@ -119,6 +145,12 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
                void *ws, size_t ws_bytes, int32_t path, float threshold,
                void *stream);
 
+/* isc_conv2d with plan overrides (tuning may be NULL: isc_conv2d itself).
+ * Errors: as isc_conv2d; ARG for a nonzero reserved field. */
+int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, float *y,
+                     void *ws, size_t ws_bytes, int32_t path, float threshold,
+                     const isc_tuning *tuning, void *stream);
+
 /* After isc_conv2d has completed on `stream` (this call synchronises the
  * stream): the number of nonzero inputs the compaction counted (UINT64_MAX
  * if the call ran the dense path only) and the path taken (ISC_PATH_SPARSE
@@ -126,6 +158,15 @@ int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y,
  * WORKSPACE, HIP. */
 int isc_decision(const isc_conv_desc *d, const void *ws, size_t ws_bytes,
                  uint64_t *nnz_total, int32_t *path_taken, void *stream);
+
+/* The same record read by the host once the caller has synchronised the
+ * call that wrote it (this call waits for nothing): the path taken
+ * (ISC_PATH_SPARSE or ISC_PATH_DENSE) and the input's nonzero count behind
+ * the decision (sparsity = 1 - nnz / (N*C*H*W), the definition under Tab. 2
+ * and the density rho of Sec. "Sparse Convolution"; UINT64_MAX when no
+ * count was taken).  ws: the workspace the call used (its first 16 bytes
+ * hold the record).  Errors: NULL, DEVICE, HIP. */
+int isc_read_decision(const void *ws, int32_t *path, uint64_t *nnz);
 
 /* ---- Layer chains: the rectifier of Eq. 2 in the convolution's epilogue ----
  *
@@ -160,6 +201,7 @@ int isc_census_size(const isc_conv_desc *d, size_t *bytes);
  *     call.  Used by the on-the-fly sparse kernels.
  *   y_census, y_census_bytes: at least isc_census_size(d) bytes, 16-byte
  *     aligned, or NULL for no census.
+ *   tuning: plan overrides, or NULL.
  * The filter-resident, filter-ring and GEMM kernels rectify and count as
  * they store y; after a kernel over compacted lists, one more launch
  * rectifies y in place and counts it.  y must not overlap x, w, wt, ws or a
@@ -169,7 +211,7 @@ int isc_census_size(const isc_conv_desc *d, size_t *bytes);
 int isc_conv2d_relu(const isc_conv_desc *d, const float *x, const void *x_census,
                     size_t x_census_bytes, const float *w, const float *wt, float *y,
                     void *y_census, size_t y_census_bytes, void *ws, size_t ws_bytes,
-                    int32_t path, float threshold, void *stream);
+                    int32_t path, float threshold, const isc_tuning *tuning, void *stream);
 
 /* After the call that wrote `census` has completed on `stream` (this call
  * synchronises the stream): the number of entries the census covers and how
@@ -219,13 +261,14 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
  *   wt: the repacked filter of isc_repack_filter (16-byte aligned).
  *   y: device output N x K x Ho x Wo, fully written, must not overlap the
  *     inputs.
+ *   tuning: plan overrides (kernel, rows, maps_per_lane, phases), or NULL.
  * One launch, no workspace, deterministic (each output is summed by one
  * lane in list order).  Several convolutions of the same input (for example
  * the branches of an inception block) can share one compaction.  Errors:
  * NULL, SHAPE, LIMIT (no LDS tiling fits the shape), ALIAS, ALIGN, DEVICE,
  * HIP. */
 int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz *nz,
-                    const float *wt, float *y, void *stream);
+                    const float *wt, float *y, const isc_tuning *tuning, void *stream);
 
 /* ISC steps 1-3 (Sec. "Sparse Convolution") in one launch with no workspace:
  * each wavefront compacts the input rows it needs on the fly (a ballot of
@@ -242,12 +285,13 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
  *   wt: the repacked filter of isc_repack_filter for K, C, R, S of d.
  *   y: device output N x K x Ho x Wo, fully written, must not overlap x or
  *     wt.
+ *   tuning: plan overrides, or NULL.
  * Deterministic (fixed summation order per output).  Errors: NULL, SHAPE,
  * LIMIT (shape not eligible: a square 1x1, 3x3 or 5x5 filter at stride 1,
  * or a 3x3 or 5x5 filter at stride 2 with K <= 64, a filter that fits in LDS
  * and at most 8 output columns), ALIAS, ALIGN, DEVICE, HIP. */
 int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y,
-                          void *stream);
+                          const isc_tuning *tuning, void *stream);
 
 /* Which kernel isc_conv2d's sparse path runs for this descriptor, reported in
  * *kernel: ISC_KERNEL_FUSED, ISC_KERNEL_FUSED_REG or ISC_KERNEL_FUSED_RING
@@ -271,6 +315,21 @@ enum isc_kernel {
 };
 int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel);
 
+/* The whole plan of the sparse path for this descriptor under the given
+ * overrides (tuning may be NULL): the kernel, its wavefront tile (rows x
+ * cols x 64*maps_per_lane output maps), the channel phases per tile, the
+ * wavefronts per workgroup and the workgroups of its launch.  Host-only.
+ * Errors: NULL, SHAPE, LIMIT, ARG (nonzero reserved field). */
+typedef struct isc_plan {
+    int32_t kernel;         /* isc_kernel value; ISC_KERNEL_NONE: no sparse kernel fits */
+    int32_t rows, cols;     /* output tile of one wavefront */
+    int32_t maps_per_lane;  /* output maps per lane */
+    int32_t phases;         /* channel phases summed per tile (1: none) */
+    int32_t waves;          /* wavefronts per workgroup */
+    int64_t workgroups;     /* workgroups of the launch */
+} isc_plan;
+int isc_sparse_plan(const isc_conv_desc *d, const isc_tuning *tuning, isc_plan *plan);
+
 /* ---- Training: the weight gradient with zero skipping ----
  *
  * The paper measures the sparsity of the rectified inputs during training
@@ -292,12 +351,14 @@ int isc_conv2d_dw_workspace_size(const isc_conv_desc *d, size_t *bytes);
  *   dw: device K x C x R x S, fully written; must not overlap x, dy or ws.
  *   ws, ws_bytes: workspace of isc_conv2d_dw_workspace_size bytes, 256-byte
  *     aligned; contents on entry are ignored.
+ *   tuning: plan overrides (rows, maps_per_lane), or NULL; the workspace
+ *     size holds for every override.
  * Two launches: one wavefront per 64 or 128 output maps, a few input channels
  * and a range of output rows sums in registers over the nonzero inputs of
  * its range; the ranges' sums are then added in order.  fp32, deterministic.
  * Errors: NULL, SHAPE, LIMIT, WORKSPACE, ALIAS, ALIGN, DEVICE, HIP. */
 int isc_conv2d_dw(const isc_conv_desc *d, const float *x, const float *dy, float *dw,
-                  void *ws, size_t ws_bytes, void *stream);
+                  void *ws, size_t ws_bytes, const isc_tuning *tuning, void *stream);
 
 /* The unrolled input matrix M_I of the matrix-multiplication formulation
  * (Sec. "Sparse Convolution", Fig. 3), with the batch as extra columns:

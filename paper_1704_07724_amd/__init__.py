@@ -6,15 +6,27 @@ memory and the current stream.  The binding refuses to work without the built
 library (there is no fallback of any kind).
 
 The functions carry the C names:
-    isc_out_shape, isc_workspace_size, isc_conv2d, isc_decision,
+    isc_out_shape, isc_workspace_size, isc_conv2d (isc_conv2d_tuned when a
+    tuning is given), isc_decision, isc_read_decision,
     isc_census_size, isc_conv2d_relu, isc_census_read,
     isc_conv2d_dw_workspace_size, isc_conv2d_dw,
     isc_compact, isc_repacked_filter_size, isc_repack_filter,
-    isc_sparse_conv, isc_sparse_conv_fused, isc_sparse_kernel,
+    isc_sparse_conv, isc_sparse_conv_fused, isc_sparse_kernel, isc_sparse_plan,
     isc_im2col, isc_gemm_f32, isc_status_str, isc_version
+
+Defaults a user may set in the environment (read here, by the binding, at
+each call; the C library reads no environment): ISC_PATH = auto | sparse |
+dense (the path when a call names none) and ISC_SPARSE_THRESHOLD (AUTO's
+fixed sparsity threshold when a call names none; unset, AUTO uses the
+library's per-shape crossover).
+
+Stream safety: every temporary (workspace, contiguous copies, outputs) is
+allocated on the stream the call is enqueued on, so torch's caching
+allocator never hands it to another stream while the kernels still use it.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 
@@ -30,7 +42,8 @@ STATUS = {
     4: "ISC_ERR_WORKSPACE", 5: "ISC_ERR_ALIAS", 6: "ISC_ERR_PATH", 7: "ISC_ERR_DEVICE",
     8: "ISC_ERR_HIP", 9: "ISC_ERR_ALIGN", 10: "ISC_ERR_ARG",
 }
-EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_decision",
+EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_conv2d_tuned", "isc_decision",
+           "isc_read_decision", "isc_sparse_plan",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
            "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
            "isc_census_size", "isc_conv2d_relu", "isc_census_read",
@@ -43,6 +56,44 @@ class IscError(RuntimeError):
         self.status = status
         super().__init__("%s: %s (%s)" % (where, STATUS.get(status, status),
                                           status_str(status)))
+
+
+THRESHOLD_CROSSOVER = -1.0  # ISC_THRESHOLD_CROSSOVER: AUTO's per-shape crossover
+
+KERNEL_IDS = {"none": 0, "fused": 1, "resident": 2, "ring": 3, "generic": 4, "fused_ring": 5, "fused_reg": 6}
+
+
+class Tuning(ctypes.Structure):
+    """isc_tuning: per-call plan overrides (0 = the library chooses)."""
+    _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "rows", "cols", "maps_per_lane", "phases",
+                                               "wide_loads", "gemm_split", "reserved")]
+
+
+class Plan(ctypes.Structure):
+    """isc_plan: the sparse path's kernel and launch shape for a descriptor."""
+    _fields_ = [("kernel", ctypes.c_int32), ("rows", ctypes.c_int32), ("cols", ctypes.c_int32),
+                ("maps_per_lane", ctypes.c_int32), ("phases", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("workgroups", ctypes.c_int64)]
+
+    def asdict(self):
+        d = {f: getattr(self, f) for f, _ in self._fields_}
+        d["kernel"] = KERNEL_NAMES.get(d["kernel"], d["kernel"])
+        return d
+
+
+def tuning(**kw):
+    """A Tuning from keyword fields; kernel may be a name ("fused_reg", ...)."""
+    if "kernel" in kw and isinstance(kw["kernel"], str):
+        kw["kernel"] = KERNEL_IDS[kw["kernel"]]
+    return Tuning(**kw)
+
+
+def _tuning_ref(t):
+    if t is None:
+        return None
+    if isinstance(t, dict):
+        t = tuning(**t)
+    return ctypes.byref(t)
 
 
 class ConvDesc(ctypes.Structure):
@@ -69,21 +120,25 @@ def lib():
     dp = ctypes.POINTER(ConvDesc)
     L.isc_out_shape.argtypes = [dp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     L.isc_workspace_size.argtypes = [dp, i32, ctypes.POINTER(sz)]
+    tp = ctypes.POINTER(Tuning)
     L.isc_conv2d.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, vp]
+    L.isc_conv2d_tuned.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, tp, vp]
     L.isc_decision.argtypes = [dp, vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(i32), vp]
+    L.isc_read_decision.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint64)]
+    L.isc_sparse_plan.argtypes = [dp, tp, ctypes.POINTER(Plan)]
     L.isc_compact.argtypes = [dp, vp, vp, vp, vp, vp]
     L.isc_repacked_filter_size.argtypes = [dp, ctypes.POINTER(sz)]
     L.isc_repack_filter.argtypes = [dp, vp, vp, vp]
-    L.isc_sparse_conv.argtypes = [dp, vp, vp, vp, vp, vp]
+    L.isc_sparse_conv.argtypes = [dp, vp, vp, vp, vp, tp, vp]
     L.isc_im2col.argtypes = [dp, vp, vp, i64, vp]
     L.isc_gemm_f32.argtypes = [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp]
-    L.isc_sparse_conv_fused.argtypes = [dp, vp, vp, vp, vp]
+    L.isc_sparse_conv_fused.argtypes = [dp, vp, vp, vp, tp, vp]
     L.isc_sparse_kernel.argtypes = [dp, ctypes.POINTER(i32)]
     L.isc_census_size.argtypes = [dp, ctypes.POINTER(sz)]
-    L.isc_conv2d_relu.argtypes = [dp, vp, vp, sz, vp, vp, vp, vp, sz, vp, sz, i32, ctypes.c_float, vp]
+    L.isc_conv2d_relu.argtypes = [dp, vp, vp, sz, vp, vp, vp, vp, sz, vp, sz, i32, ctypes.c_float, tp, vp]
     L.isc_census_read.argtypes = [vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(ctypes.c_uint64), vp]
     L.isc_conv2d_dw_workspace_size.argtypes = [dp, ctypes.POINTER(sz)]
-    L.isc_conv2d_dw.argtypes = [dp, vp, vp, vp, vp, sz, vp]
+    L.isc_conv2d_dw.argtypes = [dp, vp, vp, vp, vp, sz, tp, vp]
     for name in EXPORTS[:-2]:
         getattr(L, name).restype = ctypes.c_int
     L.isc_status_str.argtypes = [ctypes.c_int]
@@ -156,6 +211,34 @@ def _stream(stream):
     return ctypes.c_void_p(int(stream))
 
 
+def _on(stream):
+    """Context in which the call's temporaries are allocated: the caller's
+    stream when one is given (so that the caching allocator keeps them for
+    that stream), else the current one."""
+    if stream is None:
+        return contextlib.nullcontext()
+    torch = _torch()
+    if not isinstance(stream, torch.cuda.Stream):
+        stream = torch.cuda.ExternalStream(int(stream))
+    return torch.cuda.stream(stream)
+
+
+def default_path(path=None):
+    """The path of a call: the argument, else ISC_PATH, else "auto"."""
+    if path is None:
+        path = os.environ.get("ISC_PATH", "auto") or "auto"
+    return path
+
+
+def default_threshold(threshold=None):
+    """AUTO's threshold: the argument, else ISC_SPARSE_THRESHOLD, else the
+    library's per-shape crossover (THRESHOLD_CROSSOVER)."""
+    if threshold is None:
+        env = os.environ.get("ISC_SPARSE_THRESHOLD")
+        threshold = float(env) if env else THRESHOLD_CROSSOVER
+    return float(threshold)
+
+
 def _dev_f32(t, name):
     torch = _torch()
     if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32:
@@ -170,29 +253,49 @@ def workspace(desc: ConvDesc, path="auto", device=None):
     return torch.empty(max(n, 1), dtype=torch.uint8, device=device or "cuda")
 
 
-def isc_conv2d(x, w, stride=1, pad=0, path="auto", threshold=0.9, out=None, ws=None,
-               stream=None):
+def isc_conv2d(x, w, stride=1, pad=0, path=None, threshold=None, out=None, ws=None,
+               stream=None, tuning=None):
     """y = conv(x, w) (Eq. 1 with batch, stride, zero padding) on the GPU.
 
     x: [N, C, H, W] float32, w: [K, C, R, S] float32 (device tensors).
-    path: "auto" | "sparse" | "dense"; threshold: sparsity at or above which
-    "auto" takes the sparse path.  Returns y [N, K, Ho, Wo] (``out`` if given).
+    path: "auto" | "sparse" | "dense" (default: ISC_PATH or "auto");
+    threshold: sparsity at or above which "auto" takes the sparse path
+    (default: ISC_SPARSE_THRESHOLD, else the per-shape crossover);
+    tuning: plan overrides (a Tuning or a dict of its fields).  Returns y
+    [N, K, Ho, Wo] (``out`` if given).
     """
     torch = _torch()
-    x = _dev_f32(x, "x")
-    w = _dev_f32(w, "w")
-    desc = _desc_of(x.shape, w.shape, stride, pad)
-    ho, wo = isc_out_shape(desc)
-    if out is None:
-        out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
-    elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
-        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
-    if ws is None:
-        ws = workspace(desc, path, x.device)
-    _check(lib().isc_conv2d(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
-                            ws.data_ptr(), ws.numel() * ws.element_size(), _path(path),
-                            float(threshold), _stream(stream)), "isc_conv2d")
+    path = default_path(path)
+    threshold = default_threshold(threshold)
+    with _on(stream):
+        x = _dev_f32(x, "x")
+        w = _dev_f32(w, "w")
+        desc = _desc_of(x.shape, w.shape, stride, pad)
+        ho, wo = isc_out_shape(desc)
+        if out is None:
+            out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
+        elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
+            raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+        if ws is None:
+            ws = workspace(desc, path, x.device)
+        if tuning is None:
+            st = lib().isc_conv2d(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                                  ws.data_ptr(), _nbytes(ws), _path(path), threshold, _stream(stream))
+        else:
+            st = lib().isc_conv2d_tuned(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                                        ws.data_ptr(), _nbytes(ws), _path(path), threshold,
+                                        _tuning_ref(tuning), _stream(stream))
+        _check(st, "isc_conv2d")
     return out
+
+
+def isc_read_decision(ws):
+    """(path_name, nnz) from the workspace record, read by the host; the
+    caller has synchronised the call that wrote it."""
+    nnz = ctypes.c_uint64()
+    path = ctypes.c_int32()
+    _check(lib().isc_read_decision(ws.data_ptr(), ctypes.byref(path), ctypes.byref(nnz)), "isc_read_decision")
+    return PATH_NAMES.get(path.value, path.value), nnz.value
 
 
 def isc_decision(desc: ConvDesc, ws, stream=None):
@@ -223,32 +326,37 @@ def _nbytes(t):
     return t.numel() * t.element_size()
 
 
-def isc_conv2d_relu(x, w, stride=1, pad=0, path="auto", threshold=0.9, x_census=None, wt=None,
-                    y_census=None, out=None, ws=None, stream=None):
+def isc_conv2d_relu(x, w, stride=1, pad=0, path=None, threshold=None, x_census=None, wt=None,
+                    y_census=None, out=None, ws=None, stream=None, tuning=None):
     """y = max(0, conv(x, w)) (Eq. 1, then the rectifier of Eq. 2) with the
     nonzero count of y written to ``y_census`` (a buffer from ``census``)
     when given.  ``x_census``: the census of x from the call that wrote x
     (AUTO then decides from it instead of counting x).  ``wt``: a
-    RepackedFilter of w (else w is repacked in the workspace).  Returns y."""
+    RepackedFilter of w (else w is repacked in the workspace).  path,
+    threshold, tuning: as for isc_conv2d.  Returns y."""
     torch = _torch()
-    x = _dev_f32(x, "x")
-    w = _dev_f32(w, "w")
-    desc = _desc_of(x.shape, w.shape, stride, pad)
-    ho, wo = isc_out_shape(desc)
-    if out is None:
-        out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
-    elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
-        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
-    if ws is None:
-        ws = workspace(desc, path, x.device)
-    if wt is not None and (wt.K, wt.C, wt.R, wt.S) != tuple(int(v) for v in w.shape):
-        raise ValueError("repacked filter does not match w")
-    _check(lib().isc_conv2d_relu(
-        ctypes.byref(desc), x.data_ptr(),
-        None if x_census is None else x_census.data_ptr(), 0 if x_census is None else _nbytes(x_census),
-        w.data_ptr(), None if wt is None else wt.data.data_ptr(), out.data_ptr(),
-        None if y_census is None else y_census.data_ptr(), 0 if y_census is None else _nbytes(y_census),
-        ws.data_ptr(), _nbytes(ws), _path(path), float(threshold), _stream(stream)), "isc_conv2d_relu")
+    path = default_path(path)
+    threshold = default_threshold(threshold)
+    with _on(stream):
+        x = _dev_f32(x, "x")
+        w = _dev_f32(w, "w")
+        desc = _desc_of(x.shape, w.shape, stride, pad)
+        ho, wo = isc_out_shape(desc)
+        if out is None:
+            out = torch.empty((desc.N, desc.K, ho, wo), dtype=torch.float32, device=x.device)
+        elif not out.is_contiguous() or tuple(out.shape) != (desc.N, desc.K, ho, wo):
+            raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+        if ws is None:
+            ws = workspace(desc, path, x.device)
+        if wt is not None and (wt.K, wt.C, wt.R, wt.S) != tuple(int(v) for v in w.shape):
+            raise ValueError("repacked filter does not match w")
+        _check(lib().isc_conv2d_relu(
+            ctypes.byref(desc), x.data_ptr(),
+            None if x_census is None else x_census.data_ptr(), 0 if x_census is None else _nbytes(x_census),
+            w.data_ptr(), None if wt is None else wt.data.data_ptr(), out.data_ptr(),
+            None if y_census is None else y_census.data_ptr(), 0 if y_census is None else _nbytes(y_census),
+            ws.data_ptr(), _nbytes(ws), _path(path), threshold, _tuning_ref(tuning), _stream(stream)),
+            "isc_conv2d_relu")
     return out
 
 
@@ -267,26 +375,27 @@ def isc_conv2d_dw_workspace_size(desc: ConvDesc) -> int:
     return n.value
 
 
-def isc_conv2d_dw(x, dy, R, S, stride=1, pad=0, out=None, ws=None, stream=None):
+def isc_conv2d_dw(x, dy, R, S, stride=1, pad=0, out=None, ws=None, stream=None, tuning=None):
     """The weight gradient dw [K, C, R, S] of Eq. 1 from x [N, C, H, W] and
     the output gradient dy [N, K, Ho, Wo], over the nonzero inputs only."""
     torch = _torch()
-    x = _dev_f32(x, "x")
-    dy = _dev_f32(dy, "dy")
-    N, C, H, W = (int(v) for v in x.shape)
-    K = int(dy.shape[1])
-    desc = make_desc(N, C, H, W, K, int(R), int(S), int(stride), int(pad))
-    ho, wo = isc_out_shape(desc)
-    if tuple(dy.shape) != (N, K, ho, wo):
-        raise ValueError("dy must be [N, K, Ho, Wo] = %r" % ((N, K, ho, wo),))
-    if out is None:
-        out = torch.empty((K, C, int(R), int(S)), dtype=torch.float32, device=x.device)
-    elif not out.is_contiguous() or tuple(out.shape) != (K, C, int(R), int(S)):
-        raise ValueError("out must be a contiguous [K, C, R, S] tensor")
-    if ws is None:
-        ws = torch.empty(max(isc_conv2d_dw_workspace_size(desc), 1), dtype=torch.uint8, device=x.device)
-    _check(lib().isc_conv2d_dw(ctypes.byref(desc), x.data_ptr(), dy.data_ptr(), out.data_ptr(), ws.data_ptr(),
-                               _nbytes(ws), _stream(stream)), "isc_conv2d_dw")
+    with _on(stream):
+        x = _dev_f32(x, "x")
+        dy = _dev_f32(dy, "dy")
+        N, C, H, W = (int(v) for v in x.shape)
+        K = int(dy.shape[1])
+        desc = make_desc(N, C, H, W, K, int(R), int(S), int(stride), int(pad))
+        ho, wo = isc_out_shape(desc)
+        if tuple(dy.shape) != (N, K, ho, wo):
+            raise ValueError("dy must be [N, K, Ho, Wo] = %r" % ((N, K, ho, wo),))
+        if out is None:
+            out = torch.empty((K, C, int(R), int(S)), dtype=torch.float32, device=x.device)
+        elif not out.is_contiguous() or tuple(out.shape) != (K, C, int(R), int(S)):
+            raise ValueError("out must be a contiguous [K, C, R, S] tensor")
+        if ws is None:
+            ws = torch.empty(max(isc_conv2d_dw_workspace_size(desc), 1), dtype=torch.uint8, device=x.device)
+        _check(lib().isc_conv2d_dw(ctypes.byref(desc), x.data_ptr(), dy.data_ptr(), out.data_ptr(), ws.data_ptr(),
+                                   _nbytes(ws), _tuning_ref(tuning), _stream(stream)), "isc_conv2d_dw")
     return out
 
 
@@ -303,18 +412,19 @@ def isc_compact(x, stream=None, out=None):
     be passed to isc_sparse_conv.  ``out`` reuses (row_ptr, entries, total).
     """
     torch = _torch()
-    x = _dev_f32(x, "x")
-    N, C, H, W = (int(v) for v in x.shape)
-    desc = make_desc(N, C, H, W, 1, 1, 1, 1, 0)
-    if out is None:
-        row_ptr = torch.empty((N * C, H + 1), dtype=torch.int32, device=x.device)
-        buf = torch.zeros((N * C * H * W + NZ_TAIL, 2), dtype=torch.int32, device=x.device)
-        nz = buf[:N * C * H * W].view(N * C, H * W, 2)
-        total = torch.empty(1, dtype=torch.int64, device=x.device)
-    else:
-        row_ptr, nz, total = out
-    _check(lib().isc_compact(ctypes.byref(desc), x.data_ptr(), row_ptr.data_ptr(), nz.data_ptr(),
-                             total.data_ptr(), _stream(stream)), "isc_compact")
+    with _on(stream):
+        x = _dev_f32(x, "x")
+        N, C, H, W = (int(v) for v in x.shape)
+        desc = make_desc(N, C, H, W, 1, 1, 1, 1, 0)
+        if out is None:
+            row_ptr = torch.empty((N * C, H + 1), dtype=torch.int32, device=x.device)
+            buf = torch.zeros((N * C * H * W + NZ_TAIL, 2), dtype=torch.int32, device=x.device)
+            nz = buf[:N * C * H * W].view(N * C, H * W, 2)
+            total = torch.empty(1, dtype=torch.int64, device=x.device)
+        else:
+            row_ptr, nz, total = out
+        _check(lib().isc_compact(ctypes.byref(desc), x.data_ptr(), row_ptr.data_ptr(), nz.data_ptr(),
+                                 total.data_ptr(), _stream(stream)), "isc_compact")
     return row_ptr, nz, total
 
 
@@ -340,50 +450,62 @@ class RepackedFilter:
 def isc_repack_filter(w, out=None, stream=None):
     """ISC step 2's filter layout for w [K, C, R, S] (a RepackedFilter)."""
     torch = _torch()
-    w = _dev_f32(w, "w")
-    K, C, R, S = (int(v) for v in w.shape)
-    desc = make_desc(1, C, R, S, K, R, S, 1, 0)
-    n = isc_repacked_filter_size(desc) // 4
-    data = out if out is not None else torch.empty(n, dtype=torch.float32, device=w.device)
-    _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), data.data_ptr(),
-                                   _stream(stream)), "isc_repack_filter")
+    with _on(stream):
+        w = _dev_f32(w, "w")
+        K, C, R, S = (int(v) for v in w.shape)
+        desc = make_desc(1, C, R, S, K, R, S, 1, 0)
+        n = isc_repacked_filter_size(desc) // 4
+        data = out if out is not None else torch.empty(n, dtype=torch.float32, device=w.device)
+        _check(lib().isc_repack_filter(ctypes.byref(desc), w.data_ptr(), data.data_ptr(),
+                                       _stream(stream)), "isc_repack_filter")
     return RepackedFilter(data, K, C, R, S)
 
 
 KERNEL_NAMES = {0: "none", 1: "fused", 2: "resident", 3: "ring", 4: "generic", 5: "fused_ring", 6: "fused_reg"}
 
 
-def isc_sparse_kernel(desc: ConvDesc) -> str:
-    """Which kernel isc_conv2d's sparse path runs for desc: "fused" (on-the-fly
-    compaction), "resident", "ring" or "generic" (over compacted lists), or
-    "none"."""
+def isc_sparse_kernel(desc: ConvDesc, tuning=None) -> str:
+    """Which kernel isc_conv2d's sparse path runs for desc (under the given
+    overrides): "fused", "fused_reg", "fused_ring" (on-the-fly compaction),
+    "resident", "ring" or "generic" (over compacted lists), or "none"."""
+    if tuning is not None:
+        return isc_sparse_plan(desc, tuning)["kernel"]
     which = ctypes.c_int32(-1)
     _check(lib().isc_sparse_kernel(ctypes.byref(desc), ctypes.byref(which)), "isc_sparse_kernel")
     return KERNEL_NAMES[which.value]
 
 
-def isc_sparse_conv_fused(x, wt, stride=1, pad=0, out=None, stream=None):
+def isc_sparse_plan(desc: ConvDesc, tuning=None) -> dict:
+    """The sparse path's plan for desc: kernel, rows, cols, maps_per_lane,
+    phases, waves, workgroups."""
+    p = Plan()
+    _check(lib().isc_sparse_plan(ctypes.byref(desc), _tuning_ref(tuning), ctypes.byref(p)), "isc_sparse_plan")
+    return p.asdict()
+
+
+def isc_sparse_conv_fused(x, wt, stride=1, pad=0, out=None, stream=None, tuning=None):
     """ISC steps 1-3 in one launch (compaction on the fly) with a
     RepackedFilter (isc_repack_filter), no workspace; returns y [N, K, Ho,
     Wo].  Raises IscError (LIMIT) for shapes the kernel does not take."""
     torch = _torch()
-    x = _dev_f32(x, "x")
-    N, C, H, W = (int(v) for v in x.shape)
-    K, R, S = wt.K, wt.R, wt.S
-    if C != wt.C:
-        raise ValueError("channel mismatch")
-    desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
-    ho, wo = isc_out_shape(desc)
-    if out is None:
-        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=x.device)
-    elif not out.is_contiguous() or tuple(out.shape) != (N, K, ho, wo):
-        raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
-    _check(lib().isc_sparse_conv_fused(ctypes.byref(desc), x.data_ptr(), wt.data.data_ptr(), out.data_ptr(),
-                                       _stream(stream)), "isc_sparse_conv_fused")
+    with _on(stream):
+        x = _dev_f32(x, "x")
+        N, C, H, W = (int(v) for v in x.shape)
+        K, R, S = wt.K, wt.R, wt.S
+        if C != wt.C:
+            raise ValueError("channel mismatch")
+        desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
+        ho, wo = isc_out_shape(desc)
+        if out is None:
+            out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=x.device)
+        elif not out.is_contiguous() or tuple(out.shape) != (N, K, ho, wo):
+            raise ValueError("out must be a contiguous [N, K, Ho, Wo] tensor")
+        _check(lib().isc_sparse_conv_fused(ctypes.byref(desc), x.data_ptr(), wt.data.data_ptr(), out.data_ptr(),
+                                           _tuning_ref(tuning), _stream(stream)), "isc_sparse_conv_fused")
     return out
 
 
-def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):
+def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None, tuning=None):
     """ISC steps 2-3 from compacted lists (isc_compact's (row_ptr, entries,
     ...)) and a RepackedFilter; returns y [N, K, Ho, Wo]."""
     torch = _torch()
@@ -394,11 +516,12 @@ def isc_sparse_conv(x_shape, lists, wt, stride=1, pad=0, out=None, stream=None):
     row_ptr, nz = lists[0], lists[1]
     desc = make_desc(N, C, H, W, K, R, S, int(stride), int(pad))
     ho, wo = isc_out_shape(desc)
-    if out is None:
-        out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=wt.data.device)
-    _check(lib().isc_sparse_conv(ctypes.byref(desc), row_ptr.data_ptr(), nz.data_ptr(),
-                                 wt.data.data_ptr(), out.data_ptr(), _stream(stream)),
-           "isc_sparse_conv")
+    with _on(stream):
+        if out is None:
+            out = torch.empty((N, K, ho, wo), dtype=torch.float32, device=wt.data.device)
+        _check(lib().isc_sparse_conv(ctypes.byref(desc), row_ptr.data_ptr(), nz.data_ptr(),
+                                     wt.data.data_ptr(), out.data_ptr(), _tuning_ref(tuning), _stream(stream)),
+               "isc_sparse_conv")
     return out
 
 
@@ -406,6 +529,11 @@ def isc_im2col(x, R, S, stride=1, pad=0, ldc=None, out=None, stream=None):
     """The unrolled input matrix M_I (Fig. 3) on the GPU: [C*R*S, ldc] float32
     (written into `out` when given: contiguous, that shape)."""
     torch = _torch()
+    with _on(stream):
+        return _im2col(torch, x, R, S, stride, pad, ldc, out, stream)
+
+
+def _im2col(torch, x, R, S, stride, pad, ldc, out, stream):
     x = _dev_f32(x, "x")
     N, C, H, W = (int(v) for v in x.shape)
     desc = make_desc(N, C, H, W, 1, int(R), int(S), int(stride), int(pad))
@@ -426,6 +554,11 @@ def isc_im2col(x, R, S, stride=1, pad=0, ldc=None, out=None, stream=None):
 def isc_gemm_f32(a, b, out=None, stream=None):
     """c = a @ b on the fp32 matrix cores (a [M, Kd], b [Kd, N], row-major)."""
     torch = _torch()
+    with _on(stream):
+        return _gemm(torch, a, b, out, stream)
+
+
+def _gemm(torch, a, b, out, stream):
     a = _dev_f32(a, "a")
     b = _dev_f32(b, "b")
     M, Kd = (int(v) for v in a.shape)

@@ -461,11 +461,9 @@ int64_t gemm_tiles(int64_t M, int64_t Ncols) {
 // tiles (small batches: AlexNet-ImageNet conv4 at batch 1 is 3 tiles, each
 // walking all 3456 of C*R*S) splits C*R*S into ranges of at least 256, a
 // multiple of 32 (every K-slice of a range is whole), for a grid of about
-// 256 workgroups, at most 16 ranges.  ISC_GEMM_SPLIT = 0 turns it off (for
-// measurements).
+// 256 workgroups, at most 16 ranges.  (A caller's gemm_split = -1 passes no
+// partial-sum buffer, which turns it off.)
 int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
-    if (const char *env = std::getenv("ISC_GEMM_SPLIT"))
-        if (std::atoi(env) == 0) return 0;
     const int64_t tiles = gemm_tiles(M, Ncols);
     if (tiles >= 128) return 0;
     const int64_t splits = std::min<int64_t>({16, (256 + tiles - 1) / tiles, Kd / 256});

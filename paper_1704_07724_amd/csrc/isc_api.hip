@@ -67,12 +67,15 @@ int check_desc(const isc_conv_desc *d, Shape *sh) {
 
 bool valid_path(int32_t p) { return p == ISC_PATH_AUTO || p == ISC_PATH_SPARSE || p == ISC_PATH_DENSE; }
 
-isc::SparseShape sparse_shape(const Shape &s) {
-    return isc::SparseShape{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
-                            static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
-                            static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
-                            static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
+isc::SparseShape sparse_shape(const Shape &s, const isc_tuning *tu = nullptr) {
+    return isc::SparseShape{static_cast<int>(s.N),  static_cast<int>(s.C), static_cast<int>(s.H),
+                            static_cast<int>(s.W),  static_cast<int>(s.K), static_cast<int>(s.R),
+                            static_cast<int>(s.S),  static_cast<int>(s.T), static_cast<int>(s.P),
+                            static_cast<int>(s.Ho), static_cast<int>(s.Wo), tu ? *tu : isc_tuning{}};
 }
+
+// A caller's overrides are well formed (the reserved field is zero).
+bool tuning_ok(const isc_tuning *tu) { return tu == nullptr || tu->reserved == 0; }
 
 struct Layout {
     size_t ctrl = 0, parts = 0, row_ptr = 0, nz = 0, wt = 0, col = 0, split = 0, total = 0;
@@ -127,7 +130,13 @@ bool overlap(const void *a, size_t an, const void *b, size_t bn) {
     return x0 < y0 + bn && y0 < x0 + an;
 }
 
-// The current device must be a gfx950; cached per device id.
+// The current device must be a gfx950.  The answer is kept per device id:
+// the architecture of a device cannot change while the process runs, and
+// asking the runtime for the device's properties on every launch would add
+// host time to every call.  This memo is the library's only state besides
+// the per-kernel LDS-size grants (hipFuncSetAttribute is asked once per
+// kernel) and, for the allocation-free entry point, each device's scratch
+// address.
 int check_device() {
     static std::atomic<int> state[64];  // 0 unknown, 1 gfx950, 2 other
     int dev = -1;
@@ -188,13 +197,14 @@ size_t census_bytes(const Shape &s) {
 }
 
 int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws, size_t ws_bytes,
-              int32_t path, float threshold, void *stream, const Chain *ch) {
+              int32_t path, float threshold, void *stream, const Chain *ch, const isc_tuning *tu) {
     Shape s;
     int st = check_desc(d, &s);
     if (st) return st;
     if (!x || !w || !y || !ws) return ISC_ERR_NULL;
     if (!valid_path(path)) return ISC_ERR_PATH;
-    if (!(threshold >= 0.0f && threshold <= 1.0f)) return ISC_ERR_ARG;
+    if (!(threshold >= 0.0f && threshold <= 1.0f) && !(threshold < 0.0f)) return ISC_ERR_ARG;
+    if (!tuning_ok(tu)) return ISC_ERR_ARG;
     if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
     const Layout L = layout_for(s, path);
     if (ws_bytes < L.total) return ISC_ERR_WORKSPACE;
@@ -218,7 +228,7 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
             return ISC_ERR_ALIAS;
     }
 
-    const isc::SparseShape sh = sparse_shape(s);
+    const isc::SparseShape sh = sparse_shape(s, tu);
     const bool sparse_fits = L.fused || isc::sparse_conv_feasible(sh);
     if (path == ISC_PATH_SPARSE && !sparse_fits) return ISC_ERR_LIMIT;
     if (path == ISC_PATH_AUTO && !sparse_fits) path = ISC_PATH_DENSE;  // dense buffers are in L
@@ -232,7 +242,8 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
     hipError_t e = hipSuccess;
     uint32_t *parts = L.sparse ? reinterpret_cast<uint32_t *>(base + L.parts) : nullptr;
     int nparts = 0;
-    const unsigned long long limit = nnz_limit_for(s.in_elems(), threshold);
+    const unsigned long long limit =
+        threshold < 0.0f ? isc::crossover_nnz_limit(sh) : nnz_limit_for(s.in_elems(), threshold);
     const int gate_sparse = path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways;
 
     if (path != ISC_PATH_DENSE) {
@@ -286,7 +297,8 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
                           path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
         if (L.implicit) {
             // one launch: the GEMM gathers the im2col matrix from x
-            float *part = L.split ? reinterpret_cast<float *>(base + L.split) : nullptr;
+            float *part = L.split && !(tu && tu->gemm_split < 0) ? reinterpret_cast<float *>(base + L.split)
+                                                                  : nullptr;
             if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
                                            sh.Wo, dec, hs, epi, part)) != hipSuccess)
                 return hip_status(e);
@@ -352,7 +364,12 @@ int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes) {
 
 int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
                size_t ws_bytes, int32_t path, float threshold, void *stream) {
-    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, nullptr);
+    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, nullptr, nullptr);
+}
+
+int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
+                     size_t ws_bytes, int32_t path, float threshold, const isc_tuning *tuning, void *stream) {
+    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, nullptr, tuning);
 }
 
 int isc_census_size(const isc_conv_desc *d, size_t *bytes) {
@@ -366,7 +383,7 @@ int isc_census_size(const isc_conv_desc *d, size_t *bytes) {
 
 int isc_conv2d_relu(const isc_conv_desc *d, const float *x, const void *x_census, size_t x_census_bytes,
                     const float *w, const float *wt, float *y, void *y_census, size_t y_census_bytes, void *ws,
-                    size_t ws_bytes, int32_t path, float threshold, void *stream) {
+                    size_t ws_bytes, int32_t path, float threshold, const isc_tuning *tuning, void *stream) {
     Shape s;
     const int st = check_desc(d, &s);
     if (st) return st;
@@ -389,7 +406,7 @@ int isc_conv2d_relu(const isc_conv_desc *d, const float *x, const void *x_census
         ch.y_census_bytes = y_census_bytes;
     }
     if (wt && !aligned(wt, 16)) return ISC_ERR_ALIGN;
-    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, &ch);
+    return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, &ch, tuning);
 }
 
 int isc_census_read(const void *census, size_t bytes, uint64_t *elems, uint64_t *nnz, void *stream) {
@@ -417,13 +434,15 @@ int isc_census_read(const void *census, size_t bytes, uint64_t *elems, uint64_t 
     return ISC_OK;
 }
 
-int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y, void *stream) {
+int isc_sparse_conv_fused(const isc_conv_desc *d, const float *x, const float *wt, float *y,
+                          const isc_tuning *tuning, void *stream) {
     Shape s;
     int st = check_desc(d, &s);
     if (st) return st;
     if (!x || !wt || !y) return ISC_ERR_NULL;
+    if (!tuning_ok(tuning)) return ISC_ERR_ARG;
     if (!aligned(x, 4) || !aligned(wt, 4) || !aligned(y, 4)) return ISC_ERR_ALIGN;
-    const isc::SparseShape sh = sparse_shape(s);
+    const isc::SparseShape sh = sparse_shape(s, tuning);
     if (!isc::sparse_fused_applies(sh)) return ISC_ERR_LIMIT;
     const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
     const size_t wtbytes = sizeof(float) * isc::repacked_filter_floats(sh.K, sh.C, sh.R, sh.S);
@@ -447,13 +466,14 @@ int isc_conv2d_dw_workspace_size(const isc_conv_desc *d, size_t *bytes) {
 }
 
 int isc_conv2d_dw(const isc_conv_desc *d, const float *x, const float *dy, float *dw, void *ws, size_t ws_bytes,
-                  void *stream) {
+                  const isc_tuning *tuning, void *stream) {
     Shape s;
     int st = check_desc(d, &s);
     if (st) return st;
     if (!x || !dy || !dw || !ws) return ISC_ERR_NULL;
+    if (!tuning_ok(tuning)) return ISC_ERR_ARG;
     if (!aligned(x, 4) || !aligned(dy, 4) || !aligned(dw, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
-    const isc::SparseShape sh = sparse_shape(s);
+    const isc::SparseShape sh = sparse_shape(s, tuning);
     if (!isc::sparse_dw_applies(sh)) return ISC_ERR_LIMIT;
     const size_t need = align_up(sizeof(float) * isc::sparse_dw_workspace_floats(sh), kAlign);
     if (ws_bytes < need) return ISC_ERR_WORKSPACE;
@@ -476,6 +496,34 @@ int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {
     const isc::SparseShape sh = sparse_shape(s);
     const int fused = isc::sparse_fused_kernel(sh);
     *kernel = fused ? fused : isc::list_kernel_for(sh);
+    return ISC_OK;
+}
+
+int isc_sparse_plan(const isc_conv_desc *d, const isc_tuning *tuning, isc_plan *plan) {
+    if (!plan) return ISC_ERR_NULL;
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!tuning_ok(tuning)) return ISC_ERR_ARG;
+    const isc::SparseShape sh = sparse_shape(s, tuning);
+    isc_plan p{};
+    if (!isc::sparse_fused_plan_info(sh, &p)) {
+        p = isc_plan{};
+        p.kernel = isc::list_kernel_for(sh);
+        p.waves = p.kernel == ISC_KERNEL_NONE ? 0 : isc::list_kernel_waves(p.kernel);
+    }
+    *plan = p;
+    return ISC_OK;
+}
+
+int isc_read_decision(const void *ws, int32_t *path, uint64_t *nnz) {
+    if (!ws || !path || !nnz) return ISC_ERR_NULL;
+    const int st = check_device();
+    if (st) return st;
+    Ctrl c;
+    if (hipMemcpy(&c, ws, sizeof(Ctrl), hipMemcpyDeviceToHost) != hipSuccess) return ISC_ERR_HIP;
+    *path = static_cast<int32_t>(c.path_taken);
+    *nnz = c.nnz_total;
     return ISC_OK;
 }
 
@@ -552,11 +600,12 @@ int isc_repack_filter(const isc_conv_desc *d, const float *w, float *wt, void *s
 }
 
 int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz *nz, const float *wt,
-                    float *y, void *stream) {
+                    float *y, const isc_tuning *tuning, void *stream) {
     Shape s;
     int st = check_desc(d, &s);
     if (st) return st;
     if (!row_ptr || !nz || !wt || !y) return ISC_ERR_NULL;
+    if (!tuning_ok(tuning)) return ISC_ERR_ARG;
     if (!aligned(row_ptr, 4) || !aligned(nz, 8) || !aligned(wt, 16) || !aligned(y, 4)) return ISC_ERR_ALIGN;
     const size_t yb = sizeof(float) * static_cast<size_t>(s.out_elems());
     const size_t tb = sizeof(float) * isc::repacked_filter_floats(static_cast<int>(s.K), static_cast<int>(s.C),
@@ -565,10 +614,7 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
         overlap(y, yb, nz, sizeof(isc_nz) * static_cast<size_t>(s.in_elems() + kNzTail)) ||
         overlap(y, yb, wt, tb))
         return ISC_ERR_ALIAS;
-    isc::SparseShape sh{static_cast<int>(s.N), static_cast<int>(s.C), static_cast<int>(s.H),
-                        static_cast<int>(s.W), static_cast<int>(s.K), static_cast<int>(s.R),
-                        static_cast<int>(s.S), static_cast<int>(s.T), static_cast<int>(s.P),
-                        static_cast<int>(s.Ho), static_cast<int>(s.Wo)};
+    const isc::SparseShape sh = sparse_shape(s, tuning);
     if (!isc::sparse_conv_feasible(sh)) return ISC_ERR_LIMIT;
     st = check_device();
     if (st) return st;

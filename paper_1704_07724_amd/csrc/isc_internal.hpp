@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include "isc.h"
 #include <cstddef>
 #include <cstdint>
 
@@ -193,6 +194,7 @@ hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, floa
 
 struct SparseShape {
     int N, C, H, W, K, R, S, T, P, Ho, Wo;
+    isc_tuning tu;  // the caller's plan overrides (all zero: the library chooses)
 };
 
 // ISC steps 1-3 in one launch, compacting on the fly from x, with the filter
@@ -211,6 +213,9 @@ bool sparse_fring_applies(const SparseShape &sh);
 int sparse_fused_kernel(const SparseShape &sh);
 hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
                                hipStream_t s, const Epilogue &epi = Epilogue{});
+// The plan the on-the-fly kernels take for a shape (false: none takes it).
+bool sparse_fused_plan_info(const SparseShape &sh, isc_plan *out);
+bool sparse_fring_plan_info(const SparseShape &sh, isc_plan *out);
 // Upper bound of the workgroups of the on-the-fly kernels' launch for a
 // shape (the census slots their epilogue may write).
 int64_t sparse_fused_max_groups(const SparseShape &sh);
@@ -227,6 +232,13 @@ hipError_t launch_sparse_dw(const SparseShape &sh, const float *x, const float *
 // of isc_sparse_kernel in the C ABI).
 enum ListKernel : int { kListNone = 0, kListResident = 2, kListRing = 3, kListGeneric = 4 };
 int list_kernel_for(const SparseShape &sh);
+// Wavefronts per workgroup of a list kernel.
+int list_kernel_waves(int kernel);
+
+// AUTO's per-shape crossover: the largest nonzero count of the input at
+// which the sparse path is expected to be faster than the dense path for
+// this shape (crossover.cpp).
+unsigned long long crossover_nnz_limit(const SparseShape &sh);
 
 // ISC steps 2 and 3: zero-skipping convolution over the compacted lists.
 hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr,

@@ -282,7 +282,7 @@ bool tiling_for(const SparseShape &sh, size_t extra, int *TH, int *bands, int *T
     }
     const int bands0 = (sh.Ho + kWaves * th - 1) / (kWaves * th);
     th = (sh.Ho + bands0 * kWaves - 1) / (bands0 * kWaves);  // balance rows over wavefronts
-    if (const char *env = std::getenv("ISC_SPARSE_TH")) th = std::max(1, std::atoi(env));
+    if (sh.tu.rows > 0) th = sh.tu.rows;
     if (acc_bytes(th, wa) + extra > kLdsMax) return false;
     *TH = th;
     *bands = (sh.Ho + kWaves * th - 1) / (kWaves * th);
@@ -318,16 +318,17 @@ bool sparse_tiling(const SparseShape &sh, int *TH, int *bands, int *TW, int *cti
 
 bool sparse_conv_feasible(const SparseShape &sh) { return list_kernel_for(sh) != kListNone; }
 
+int list_kernel_waves(int kernel) { return kernel == kListResident ? 16 : 4; }
+
 // Kernel over compacted lists: the filter-resident register kernel when the
 // filter of 64 output maps fits in LDS, else the filter-ring register kernel,
 // else the LDS-accumulator kernel (any filter, any stride).
-// ISC_SPARSE_KERNEL = "generic" | "ring" | "res" restricts the choice (for
-// measurements).
+// A caller's tuning.kernel naming one of the three restricts the choice.
 int list_kernel_for(const SparseShape &sh) {
-    const char *env = std::getenv("ISC_SPARSE_KERNEL");
-    const bool any = env == nullptr || env[0] == 0;
-    if ((any || std::strcmp(env, "res") == 0) && sparse_res_applies(sh)) return kListResident;
-    if ((any || std::strcmp(env, "ring") == 0) && sparse_ring_applies(sh)) return kListRing;
+    const int want = sh.tu.kernel;
+    const bool any = want != kListResident && want != kListRing && want != kListGeneric;
+    if ((any || want == kListResident) && sparse_res_applies(sh)) return kListResident;
+    if ((any || want == kListRing) && sparse_ring_applies(sh)) return kListRing;
     int th, bands, tw, ct, wa, hx;
     return tiling_for(sh, 0, &th, &bands, &tw, &ct, &wa, &hx) ? kListGeneric : kListNone;
 }

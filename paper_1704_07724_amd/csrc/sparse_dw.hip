@@ -24,22 +24,18 @@ void dw_reduce_kernel(const float *__restrict__ part, int splits, int64_t n, flo
 //  - 5x5 and 1x1 filters: two-row tiles (each scanned nonzero feeds two
 //    output rows), two maps per lane -- one when K > 64 with 5x5 filters,
 //    which keeps three channels per wavefront instead of one.
-// ISC_DW_KPL (1, 2, 4) and ISC_DW_TH (1, 2) override the choice, for
-// measurements (four maps per lane only with one-row 16-column tiles, two
-// rows only with one or two maps per lane).
+// A caller's tuning maps_per_lane (1, 2, 4) and rows (1, 2) override the
+// choice (four maps per lane only with one-row 16-column tiles, two rows
+// only with one or two maps per lane).
 int dw_th(const SparseShape &sh) {
-    if (const char *env = std::getenv("ISC_DW_TH")) {
-        const int t = std::atoi(env);
-        if (t == 1 || t == 2) return t;
-    }
+    const int t = sh.tu.rows;
+    if (t == 1 || t == 2) return t;
     return sh.R == 3 ? 1 : 2;
 }
 
 int dw_kpl(const SparseShape &sh, int th) {
-    if (const char *env = std::getenv("ISC_DW_KPL")) {
-        const int k = std::atoi(env);
-        if ((k == 1 || k == 2) || (k == 4 && th == 1 && sh.Wo <= 16)) return k;
-    }
+    const int k = sh.tu.maps_per_lane;
+    if ((k == 1 || k == 2) || (k == 4 && th == 1 && sh.Wo <= 16)) return k;
     return sh.R == 5 && sh.K > kLanes ? 1 : 2;
 }
 int dw_tw(int Wo) { return Wo <= 16 ? 16 : 28; }
@@ -74,10 +70,20 @@ bool sparse_dw_applies(const SparseShape &sh) {
     return dwk::dw_plan(sh, &p);
 }
 
+// The largest partial-sum buffer of any tile the overrides may force, so
+// that one workspace size holds for every plan.
 size_t sparse_dw_workspace_floats(const SparseShape &sh) {
-    dwk::DwPlan p;
-    if (!dwk::dw_plan(sh, &p)) return 0;
-    return static_cast<size_t>(p.splits) * sh.K * sh.C * sh.R * sh.S;
+    size_t most = 0;
+    for (int th : {1, 2})
+        for (int kpl : {1, 2, 4}) {
+            SparseShape v = sh;
+            v.tu = isc_tuning{};
+            v.tu.rows = th;
+            v.tu.maps_per_lane = kpl;
+            dwk::DwPlan p;
+            if (dwk::dw_plan(v, &p)) most = std::max(most, static_cast<size_t>(p.splits) * sh.K * sh.C * sh.R * sh.S);
+        }
+    return most;
 }
 
 hipError_t launch_sparse_dw(const SparseShape &sh, const float *x, const float *dy, float *dw, float *part,

@@ -18,19 +18,16 @@ int fring_tw(int Wo) { return Wo <= 16 ? 16 : 28; }
 // rows per wavefront (each weight read from LDS serves twice the outputs,
 // which counts at high sparsity, where a channel's weight reads cost more
 // than the few multiply-adds they feed), then to more maps per lane.  Tie
-// order measured on AlexNet conv2-5 and the inception 3x3 branch; ISC_FRING_KPL /
-// ISC_FRING_TH restrict the choice (for measurements).
-bool fring_choose(const SparseShape &sh, int tw, TileChoice *tc) {
-    int kpl_fix = 0, th_fix = 0;
-    if (const char *env = std::getenv("ISC_FRING_KPL")) kpl_fix = std::atoi(env);
-    if (const char *env = std::getenv("ISC_FRING_TH")) th_fix = std::atoi(env);
+// order measured on AlexNet conv2-5 and the inception 3x3 branch; a caller's
+// tuning maps_per_lane / rows restrict the choice.
+bool fring_choose_fixed(const SparseShape &sh, int tw, int kpl_fix, int th_fix, TileChoice *tc) {
     bool found = false;
     double best = 0.0;
     int best_rank = 0;
     for (int kpl : {6, 4, 2, 1}) {
-        if (kpl_fix && kpl != kpl_fix) continue;
+        if (kpl_fix > 0 && kpl != kpl_fix) continue;
         for (int th : {2, 1}) {
-            if (th_fix && th != th_fix) continue;
+            if (th_fix > 0 && th != th_fix) continue;
             if (!fring_fits(sh.R, kpl, th, tw)) continue;
             const int kw = kLanes * kpl, rows = kWaves * th;
             const double lanes = static_cast<double>((sh.K + kw - 1) / kw * kw) / sh.K;
@@ -48,6 +45,11 @@ bool fring_choose(const SparseShape &sh, int tw, TileChoice *tc) {
     return found;
 }
 
+// The caller's overrides when the shape takes them, else the choice above.
+bool fring_choose(const SparseShape &sh, int tw, TileChoice *tc) {
+    return fring_choose_fixed(sh, tw, sh.tu.maps_per_lane, sh.tu.rows, tc) || fring_choose_fixed(sh, tw, 0, 0, tc);
+}
+
 }  // namespace
 }  // namespace fring
 
@@ -55,6 +57,18 @@ bool sparse_fring_applies(const SparseShape &sh) {
     if (sh.T != 1 || sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     fring::TileChoice tc;
     return fring::fring_choose(sh, fring::fring_tw(sh.Wo), &tc);
+}
+
+bool sparse_fring_plan_info(const SparseShape &sh, isc_plan *out) {
+    using namespace fring;
+    const int tw = fring_tw(sh.Wo);
+    TileChoice tc;
+    if (!sparse_fring_applies(sh) || !fring_choose(sh, tw, &tc)) return false;
+    const int twr = std::min(tw, sh.Wo);
+    const int64_t groups = static_cast<int64_t>(sh.N) * ((sh.Ho + kWaves * tc.th - 1) / (kWaves * tc.th)) *
+                           ((sh.Wo + twr - 1) / twr) * ((sh.K + kLanes * tc.kpl - 1) / (kLanes * tc.kpl));
+    *out = isc_plan{ISC_KERNEL_FUSED_RING, tc.th, twr, tc.kpl, 1, kWaves, groups};
+    return true;
 }
 
 hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,

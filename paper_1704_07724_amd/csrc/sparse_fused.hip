@@ -22,11 +22,11 @@ size_t fused_lds(int crs, int th, int tw) {
 // fit in LDS at all, and one workgroup per group of 64 maps takes any K
 // (AlexNet-ImageNet conv4 of Tab. 2 at batch 128: 259 us on the
 // filter-ring kernel -> 113 us).  Taken wherever eligible: stride 1, square
-// 1x1, 3x3 and 5x5 filters, at most 16 output columns.  ISC_FUSED_W = 0
-// keeps the filter in LDS, or in the ring beyond 64 maps (for measurements).
+// 1x1, 3x3 and 5x5 filters, at most 16 output columns.  A caller's tuning
+// kernel FUSED or FUSED_RING keeps the filter in LDS, or in the ring beyond
+// 64 maps.
 bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
-    if (const char *env = std::getenv("ISC_FUSED_W"))
-        if (std::atoi(env) == 0) return false;
+    if (sh.tu.kernel == ISC_KERNEL_FUSED || sh.tu.kernel == ISC_KERNEL_FUSED_RING) return false;
     if (sh.T != 1 || sh.Wo > 16) return false;
     // the kernel addresses the repacked filter with 32-bit byte offsets
     const int64_t kp = (sh.K + kLanes - 1) / kLanes * kLanes;
@@ -34,16 +34,12 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
         return false;
     // 4 x 8 or 2 x 16 tiles; half as many rows when full ones leave CUs
     // without a workgroup (LeNet conv2 at batch 8: 7.7 -> 6.4 us; at batch
-    // 256 they cost 44 %).  ISC_FUSED_REG_TH fixes the rows (for
-    // measurements).
+    // 256 they cost 44 %).  A caller's tuning rows fixes the rows.
     const int tw = sh.Wo <= 8 ? 8 : 16;
     const int full = 32 / tw;
     const int64_t kgroups = (sh.K + kLanes - 1) / kLanes;
     int th = static_cast<int64_t>(sh.N) * ((sh.Ho + full - 1) / full) * kgroups < kMinGroups ? full / 2 : full;
-    if (const char *env = std::getenv("ISC_FUSED_REG_TH")) {
-        const int t = std::atoi(env);
-        if (t == full || t == full / 2) th = t;
-    }
+    if (sh.tu.rows == full || sh.tu.rows == full / 2) th = sh.tu.rows;
     *plan = FusedPlan{th, tw, kWaves, sizeof(float) * kWaves * th * tw * kRPad, 1, true};
     return true;
 }
@@ -53,9 +49,11 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
 // tile (up to kMaxTile accumulators per lane), then the fewest phases that
 // leave no row group of a workgroup idle (rg <= ceil(Ho / TH)), preferring
 // plans with at least kMinGroups workgroups; else the plan with most
-// workgroups.  ISC_FUSED_TH caps the tile height and ISC_FUSED_CS fixes the
-// phases (for measurements).
+// workgroups.  A caller's tuning rows caps the tile height and phases fixes
+// the phases; tuning kernel FUSED_RING leaves the shape to the filter-ring
+// kernel.
 bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
+    if (sh.tu.kernel == ISC_KERNEL_FUSED_RING && sparse_fring_applies(sh)) return false;
     if (sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     if (!(sh.T == 1 || (sh.T == 2 && sh.R > 1 && sh.Wo <= 8))) return false;
     if (sh.Wo > 28) return false;
@@ -65,9 +63,8 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     // keeps none of it there, takes it (one phase per wavefront)
     if (static_cast<size_t>(crs) * kWPitch * sizeof(float) > kLdsMax) return fused_wreg_plan(sh, plan);
     const int tw = fused_tw(sh.Wo);
-    int th_cap = 8, cs_fix = 0;
-    if (const char *env = std::getenv("ISC_FUSED_TH")) th_cap = std::max(1, std::atoi(env));
-    if (const char *env = std::getenv("ISC_FUSED_CS")) cs_fix = std::atoi(env);
+    const int th_cap = sh.tu.rows > 0 ? sh.tu.rows : 8;
+    const int cs_fix = sh.tu.phases == 1 || sh.tu.phases == 2 || sh.tu.phases == 4 || sh.tu.phases == 8 ? sh.tu.phases : 0;
     bool found = false, done = false;
     int64_t best_groups = 0;
     for (int th : {8, 4, 2, 1}) {
@@ -118,6 +115,18 @@ int sparse_fused_kernel(const SparseShape &sh) {
     return sparse_fring_applies(sh) ? 5 : 0;
 }
 
+bool sparse_fused_plan_info(const SparseShape &sh, isc_plan *out) {
+    using namespace fused;
+    FusedPlan p;
+    if (!fused_plan(sh, &p)) return sparse_fring_plan_info(sh, out);
+    const int rg = kWaves / p.cs;
+    const int64_t bands = (sh.Ho + rg * p.th - 1) / (rg * p.th);
+    const int64_t kgroups = p.wreg ? (sh.K + kLanes - 1) / kLanes : 1;
+    *out = isc_plan{p.wreg ? ISC_KERNEL_FUSED_REG : ISC_KERNEL_FUSED, p.th, p.tw, 1, p.cs, kWaves,
+                    static_cast<int64_t>(sh.N) * bands * kgroups};
+    return true;
+}
+
 // The filter-resident kernel when the filter fits in LDS, else the
 // filter-ring kernel.
 hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const float *wt, float *y, const Decision &dec,
@@ -135,6 +144,7 @@ hipError_t launch_sparse_fused(const SparseShape &sh, const float *x, const floa
     a.bands = (sh.Ho + a.rg * p.th - 1) / (a.rg * p.th);
     a.Kp = (sh.K + kLanes - 1) / kLanes * kLanes;
     a.kgroups = p.wreg ? a.Kp / kLanes : 1;
+    a.wide = a.kgroups > 1 || sh.tu.wide_loads == 1;
     a.dec = dec;
     a.epi = epi;
     switch (sh.R) {

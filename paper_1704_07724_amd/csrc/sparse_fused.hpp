@@ -29,7 +29,6 @@
 #pragma once
 
 #include "sparse_tile.hpp"
-#include <cstdlib>
 
 namespace isc {
 namespace fused {
@@ -56,6 +55,7 @@ struct FusedArgs {
     int bands;        // groups of rg * TH output rows
     int kgroups;      // groups of 64 output maps (register-weight kernel; 1 otherwise)
     int Kp;           // maps per filter column of wt (K rounded up to 64)
+    int wide;         // register-weight kernel: weights through a buffer resource
     Decision dec;
     Epilogue epi;     // rectifier and census of y
 };
@@ -400,14 +400,11 @@ hipError_t launch_fused_reg_w(const FusedArgs &a, size_t lds, hipStream_t s) {
 }
 
 // one group of 64 maps: filter taps at immediate offsets (kgroups == 1 and
-// Kp == 64); else through the buffer resource.  ISC_FUSED_REG_WIDE = 1 takes
-// the buffer path for one group too (for measurements).
+// Kp == 64); else, or when the caller asks (a.wide), through the buffer
+// resource.
 template <int RS_, int TH, int TW>
 hipError_t launch_fused_reg_t(const FusedArgs &a, size_t lds, hipStream_t s) {
-    bool wide = a.kgroups > 1;
-    if (const char *env = std::getenv("ISC_FUSED_REG_WIDE"))
-        if (std::atoi(env) == 1) wide = true;
-    return wide ? launch_fused_reg_w<RS_, TH, TW, true>(a, lds, s) : launch_fused_reg_w<RS_, TH, TW, false>(a, lds, s);
+    return a.wide ? launch_fused_reg_w<RS_, TH, TW, true>(a, lds, s) : launch_fused_reg_w<RS_, TH, TW, false>(a, lds, s);
 }
 
 template <int RS_, int TH, int TW, int ST>

@@ -265,8 +265,8 @@ hipError_t launch_sparse_ring(const SparseShape &sh, const int32_t *row_ptr, con
     a.P = sh.P; a.Ho = sh.Ho; a.Wo = sh.Wo;
     const int tw = ring_tw(sh.Wo);
     int kpl = ring_kpl(sh.K, sh.R, tw);
-    if (const char *env = std::getenv("ISC_RING_KPL")) {  // tuning override
-        const int v = std::atoi(env);
+    {  // a caller's override
+        const int v = sh.tu.maps_per_lane;
         if ((v == 1 || v == 2 || v == 4 || v == 6) && ring_fits(sh.R, v, tw)) kpl = v;
     }
     a.TWr = std::min(tw, sh.Wo);

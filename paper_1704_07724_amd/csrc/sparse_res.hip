@@ -329,8 +329,8 @@ hipError_t launch_sparse_res(const SparseShape &sh, const int32_t *row_ptr, cons
                              float *y, const Decision &dec, hipStream_t s) {
     ResPlan p;
     if (!res_plan(sh, &p)) return hipErrorInvalidValue;
-    if (const char *env = std::getenv("ISC_RES_CS")) {  // tuning override
-        const int v = std::atoi(env);
+    if (sh.tu.phases > 0) {  // a caller's override
+        const int v = sh.tu.phases;
         ResPlan q = p;
         q.cs = v;
         if (v >= 1 && v <= kWaves && kWaves % v == 0 && v <= sh.C) {

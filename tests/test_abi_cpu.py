@@ -127,18 +127,40 @@ def test_compact_im2col_gemm_validation():
     assert L.isc_gemm_f32(4, 4, 4, 0x1000, 4, 0x2000, 4, 0x1000, 4, None) == 5  # c overlaps a
 
 
-def test_dispatch_threshold_reading():
-    # the AUTO decision is "sparsity = 1 - nnz/total >= threshold"; the
-    # default threshold follows the abstract's "not less than 0.9"
-    import inspect
-    sig = inspect.signature(isc.isc_conv2d)
-    assert sig.parameters["threshold"].default == 0.9
-    assert sig.parameters["path"].default == "auto"
+def test_dispatch_defaults_from_the_binding(monkeypatch):
+    """The path and AUTO's threshold default to ISC_PATH / ISC_SPARSE_THRESHOLD,
+    read by the binding (the library reads no environment); unset, AUTO runs
+    the library's per-shape crossover and the path is AUTO."""
+    monkeypatch.delenv("ISC_PATH", raising=False)
+    monkeypatch.delenv("ISC_SPARSE_THRESHOLD", raising=False)
+    assert isc.default_path() == "auto"
+    assert isc.default_threshold() == isc.THRESHOLD_CROSSOVER == -1.0
+    assert isc.default_threshold(0.9) == 0.9
+    monkeypatch.setenv("ISC_PATH", "dense")
+    monkeypatch.setenv("ISC_SPARSE_THRESHOLD", "0.9")
+    assert isc.default_path() == "dense" and isc.default_path("sparse") == "sparse"
+    assert isc.default_threshold() == 0.9
 
 
-def test_sparse_kernel_choice(monkeypatch):
+def test_library_reads_no_environment():
+    """No plan of the library depends on an inherited environment: the
+    shared object imports no getenv."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", isc.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    imported = {line.split()[-1].split("@")[0] for line in out.splitlines() if line.strip()}
+    assert "getenv" not in imported and "secure_getenv" not in imported
+
+
+def test_crossover_threshold_accepted():
+    # a negative threshold asks for the per-shape crossover; NaN is rejected
+    good = isc.make_desc(2, 3, 8, 8, 4, 3, 3, 1, 1)
+    assert _conv(good, th=-1.0) in (0, 7)                     # valid (no device here: DEVICE)
+    assert _conv(good, th=float("nan")) == 10
+
+
+def test_sparse_kernel_choice():
     """Host-side choice of the sparse kernel for the workload shapes."""
-    monkeypatch.delenv("ISC_SPARSE_KERNEL", raising=False)
     d = isc.make_desc
     assert isc.isc_sparse_kernel(d(256, 20, 12, 12, 50, 5, 5, 1, 0)) == "fused_reg"  # LeNet conv2
     assert isc.isc_sparse_kernel(d(128, 16, 28, 28, 32, 5, 5, 1, 2)) == "fused"    # inception 5x5
@@ -164,13 +186,15 @@ def test_fused_entry_validation():
     big_k = isc.make_desc(1, 2, 12, 12, 65, 7, 7, 1, 0)       # 7 x 7 filter: not taken
     strided = isc.make_desc(1, 2, 24, 24, 8, 5, 5, 2, 0)      # stride 2 with 10 output columns: not taken
     x, w, y = 0x1000, 0x200000, 0x400000
-    assert L.isc_sparse_conv_fused(None, x, w, y, None) == 1
-    assert L.isc_sparse_conv_fused(ctypes.byref(ok), None, w, y, None) == 1
-    assert L.isc_sparse_conv_fused(ctypes.byref(big_k), x, w, y, None) == 3
-    assert L.isc_sparse_conv_fused(ctypes.byref(strided), x, w, y, None) == 3
-    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, x + 4, None) == 5   # y overlaps x
-    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x + 2, w, y, None) == 9   # misaligned
-    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, y, None) == 7       # no gfx950 here
+    assert L.isc_sparse_conv_fused(None, x, w, y, None, None) == 1
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), None, w, y, None, None) == 1
+    assert L.isc_sparse_conv_fused(ctypes.byref(big_k), x, w, y, None, None) == 3
+    assert L.isc_sparse_conv_fused(ctypes.byref(strided), x, w, y, None, None) == 3
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, x + 4, None, None) == 5   # y overlaps x
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x + 2, w, y, None, None) == 9   # misaligned
+    bad = isc.Tuning(reserved=1)
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, y, ctypes.byref(bad), None) == 10
+    assert L.isc_sparse_conv_fused(ctypes.byref(ok), x, w, y, None, None) == 7       # no gfx950 here
 
 
 def test_census_size():
@@ -191,7 +215,7 @@ def test_census_size():
 def _relu(desc, x=0x1000, xc=None, xcb=0, w=0x200000, wt=None, y=0x400000, yc=None, ycb=0,
           ws=0x800000, ws_bytes=1 << 30, path=0, th=0.9):
     return isc.lib().isc_conv2d_relu(ctypes.byref(desc), x, xc, xcb, w, wt, y, yc, ycb, ws, ws_bytes,
-                                     path, ctypes.c_float(th), None)
+                                     path, ctypes.c_float(th), None, None)
 
 
 def test_conv2d_relu_validation():
@@ -238,32 +262,61 @@ def test_dw_entry_validation():
         isc.isc_conv2d_dw_workspace_size(isc.make_desc(2, 3, 9, 9, 8, 7, 7, 1, 3))
     assert e.value.status == 3
     x, dy, dw, ws = 0x1000, 0x100000, 0x200000, 0x300000
-    assert L.isc_conv2d_dw(ctypes.byref(d), None, dy, dw, ws, n, None) == 1
-    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n - 1, None) == 4    # workspace too small
-    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, x, ws, n, None) == 5        # dw overlaps x
-    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws + 16, n, None) == 9  # workspace misaligned
+    assert L.isc_conv2d_dw(ctypes.byref(d), None, dy, dw, ws, n, None, None) == 1
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n - 1, None, None) == 4    # workspace too small
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, x, ws, n, None, None) == 5        # dw overlaps x
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws + 16, n, None, None) == 9  # workspace misaligned
     try:
         import torch
         if torch.cuda.is_available():
             return
     except Exception:
         pass
-    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n, None) == 7       # no gfx950 here
+    assert L.isc_conv2d_dw(ctypes.byref(d), x, dy, dw, ws, n, None, None) == 7       # no gfx950 here
 
 
-def test_dense_split_workspace(monkeypatch):
+def test_dense_split_workspace():
     """Host plan of the dense GEMM's split reduction: a grid under 128 tiles
     splits C*R*S into ranges of at least 256 (multiples of 32, at most 16)
     and the workspace holds ranges x K x N*Ho*Wo partial sums; grids that
     fill the chip, or short reductions, do not split."""
     d = isc.make_desc(1, 384, 5, 5, 384, 3, 3, 1, 1)     # 3 tiles, C*R*S 3456
-    monkeypatch.setenv("ISC_GEMM_SPLIT", "0")
-    base = isc.isc_workspace_size(d, "dense")
-    monkeypatch.delenv("ISC_GEMM_SPLIT")
+    lenet = isc.make_desc(256, 20, 12, 12, 50, 5, 5, 1, 0)  # 256 tiles of 64 x 64: no split
+    base = isc.isc_workspace_size(lenet, "dense")          # the control block alone
     split = isc.isc_workspace_size(d, "dense")
     # min(16, ceil(256 / 3), 3456 // 256) = 13 ranges asked -> ranges of 288 -> 12 ranges
     assert split - base == 12 * 384 * 25 * 4
-    lenet = isc.make_desc(256, 20, 12, 12, 50, 5, 5, 1, 0)  # 256 tiles of 64 x 64
-    assert isc.isc_workspace_size(lenet, "dense") == base
     short = isc.make_desc(3, 500, 4, 4, 33, 1, 1, 1, 0)   # C*R*S 500 < 2 * 256
     assert isc.isc_workspace_size(short, "dense") == base
+
+
+def test_sparse_plan_and_overrides():
+    """The plan query reports the kernel and launch shape, and a per-call
+    tuning forces what the shape can take and is ignored otherwise."""
+    d = isc.make_desc
+    lenet = d(256, 20, 12, 12, 50, 5, 5, 1, 0)
+    p = isc.isc_sparse_plan(lenet)
+    assert p["kernel"] == "fused_reg" and p["phases"] == 8 and p["waves"] == 8
+    assert (p["rows"], p["cols"]) == (4, 8) and p["workgroups"] == 256 * 2
+    # the filter in LDS instead of the register-weight kernel
+    q = isc.isc_sparse_plan(lenet, {"kernel": "fused"})
+    assert q["kernel"] == "fused" and q["rows"] * q["cols"] <= 64
+    # the register-weight kernel's two tile heights
+    assert isc.isc_sparse_plan(lenet, {"rows": 2})["rows"] == 2
+    conv2 = d(128, 96, 27, 27, 256, 5, 5, 1, 2)
+    r = isc.isc_sparse_plan(conv2, {"kernel": "fused_ring", "maps_per_lane": 2, "rows": 1})
+    assert (r["kernel"], r["maps_per_lane"], r["rows"]) == ("fused_ring", 2, 1)
+    assert r["workgroups"] == 128 * 7 * 1 * 2
+    # five maps per lane: no such tile, the library's own choice runs
+    assert isc.isc_sparse_plan(conv2, {"kernel": "fused_ring", "maps_per_lane": 5}) == isc.isc_sparse_plan(conv2)
+    assert isc.isc_sparse_plan(d(2, 4, 21, 21, 64, 5, 5, 2, 1))["kernel"] == "generic"
+    with pytest.raises(isc.IscError) as e:
+        isc.isc_sparse_plan(lenet, isc.Tuning(reserved=3))
+    assert e.value.status == 10
+
+
+def test_read_decision_validation():
+    L = isc.lib()
+    p, n = ctypes.c_int32(), ctypes.c_uint64()
+    assert L.isc_read_decision(None, ctypes.byref(p), ctypes.byref(n)) == 1
+    assert L.isc_read_decision(0x1000, None, ctypes.byref(n)) == 1

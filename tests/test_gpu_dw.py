@@ -110,27 +110,22 @@ def test_dw_zero_input_and_rejects(torch, isc):
     assert e.value.status == 3
 
 
-def test_dw_full_size_sampled(torch, isc):
+def test_dw_full_size_every_entry(torch, isc):
     """AlexNet conv2 at full size (batch 128, 96 -> 256, 27x27, 5x5, pad 2,
-    sparsity 0.9) as the benchmark runs it; the gradient of a map depends on
-    that map's output gradients and of a channel on that channel's inputs, so
-    the oracle on a few maps and channels gives exact reference slices."""
+    sparsity 0.9) as the benchmark runs it: every entry of K x C x R x S
+    against the oracle's full weight gradient."""
     layer = [l for l in workloads.WORKLOADS["alexnet_conv2"].layers][0]
     note("dw full", layer.x_shape, layer.w_shape)
     x, _ = workloads.make_inputs(layer)
     Ho = oracle.out_size(layer.H, layer.R, layer.P, 1)
     dy = _dy((layer.N, layer.K, Ho, Ho), 49)
     got = isc.isc_conv2d_dw(to_dev(torch, x), to_dev(torch, dy), layer.R, layer.S, 1, layer.P).cpu().numpy()
-    rng = np.random.default_rng(50)
-    ks = np.sort(rng.choice(layer.K, size=6, replace=False))
-    cs = np.sort(rng.choice(layer.C, size=3, replace=False))
-    want = oracle.conv2d_dw_f64(np.ascontiguousarray(x[:, cs]), np.ascontiguousarray(dy[:, ks]), layer.R, layer.S, 1,
-                                layer.P)
-    assert_close(got[np.ix_(ks, cs)], want, "dw full size")
+    want = oracle.conv2d_dw_f64(x, dy, layer.R, layer.S, 1, layer.P)
+    assert_close(got, want, "dw full size")
 
 
 @pytest.mark.parametrize("R,W", [(1, 13), (3, 13), (3, 30), (5, 11), (5, 27)])
-def test_dw_every_tile_variant(torch, isc, monkeypatch, R, W):
+def test_dw_every_tile_variant(torch, isc, R, W):
     """Every compiled tile (rows per tile, maps per lane, 16- or 28-column
     tiles), forced through the measurement overrides, against the oracle on
     ragged maps and channels."""
@@ -142,7 +137,6 @@ def test_dw_every_tile_variant(torch, isc, monkeypatch, R, W):
     variants = [(1, 1), (2, 1), (1, 2), (2, 2)] + ([(4, 1)] if Wo <= 16 else [])
     for kpl, th in variants:
         note("dw variant", R, W, "kpl", kpl, "th", th)
-        monkeypatch.setenv("ISC_DW_KPL", str(kpl))
-        monkeypatch.setenv("ISC_DW_TH", str(th))
-        got = isc.isc_conv2d_dw(to_dev(torch, x), to_dev(torch, dy), R, R, 1, P).cpu().numpy()
+        got = isc.isc_conv2d_dw(to_dev(torch, x), to_dev(torch, dy), R, R, 1, P,
+                                tuning={"maps_per_lane": kpl, "rows": th}).cpu().numpy()
         assert_close(got, want, "dw R%d W%d kpl%d th%d" % (R, W, kpl, th))

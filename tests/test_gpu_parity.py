@@ -246,8 +246,10 @@ def test_auto_dispatch_choice(torch, isc, sparsity):
     x, w = workloads.make_case(4, 10, 12, 12, 50, 5, 5, 1, 0, sparsity, seed=int(sparsity * 100))
     desc = isc.make_desc(4, 10, 12, 12, 50, 5, 5, 1, 0)
     ws = isc.workspace(desc, "auto")
-    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path="auto", ws=ws)
+    y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), 1, 0, path="auto", threshold=0.9, ws=ws)
     nnz, taken = isc.isc_decision(desc, ws)
+    torch.cuda.synchronize()
+    assert isc.isc_read_decision(ws) == (taken, nnz)
     want_path, want_nnz = oracle_choice(x, 0.9)
     assert nnz == want_nnz
     assert taken == want_path
@@ -356,43 +358,43 @@ def test_sparse_conv_entry_from_lists(torch, isc):
 def full_layers():
     for wl in workloads.WORKLOADS.values():
         for layer in wl.layers:
-            if wl.name == "lenet_conv2_batch" and layer.sparsity not in (0.5, 0.9, 0.99):
-                continue
             yield pytest.param(layer, id=layer.name)
 
 
+def _compact_every_plane(ent, rp_o, v_o, ys_o, xs_o, H):
+    """Every plane's list against the oracle's, vectorised: values bit for
+    bit, rows and columns, and nothing but the plane's own entries."""
+    counts = rp_o[:, H]
+    slots = np.arange(ent.shape[1])[None, :]
+    used = slots < counts[:, None]
+    got_v = ent[:, :, 0].view(np.uint32)
+    got_yx = ent[:, :, 1].view(np.uint32)
+    assert np.array_equal(got_v[used], v_o.view(np.uint32)[used])
+    assert np.array_equal((got_yx >> 16)[used], ys_o.astype(np.uint32)[used])
+    assert np.array_equal((got_yx & 0xFFFF)[used], xs_o.astype(np.uint32)[used])
+
+
 @pytest.mark.parametrize("layer", list(full_layers()))
-def test_full_size_sampled(torch, isc, layer):
+def test_full_size_every_output(torch, isc, layer):
     """Workload shapes at full size, in the launch configuration the benchmark
-    times: compaction bit-exact in full, convolution outputs checked at
-    sampled positions against the oracle evaluated point by point."""
+    times: compaction bit-exact on every plane, and every output of the
+    sparse, dense and AUTO paths against the oracle's full convolution."""
     note("full", layer.name, layer.x_shape, layer.w_shape)
     x, w = workloads.make_inputs(layer)
     xd, wd = to_dev(torch, x), to_dev(torch, w)
     T, P = layer.T, layer.P
-    # compaction: totals and a bit-exact comparison on a sample of planes
     row_ptr, nz, total = isc.isc_compact(xd)
     rp_o, v_o, ys_o, xs_o, tot_o = oracle.compact(x)
     assert int(total.item()) == tot_o
     assert np.array_equal(row_ptr.cpu().numpy(), rp_o)
-    ent = nz.cpu().numpy()
-    rng = np.random.default_rng(layer.seed)
-    H = layer.H
-    for p in rng.choice(ent.shape[0], size=min(256, ent.shape[0]), replace=False):
-        cnt = rp_o[p, H]
-        assert np.array_equal(ent[p, :cnt, 0].view(np.uint32), v_o[p, :cnt].view(np.uint32))
-        yx = ent[p, :cnt, 1].view(np.uint32)
-        assert np.array_equal(yx >> 16, ys_o[p, :cnt].astype(np.uint32))
-        assert np.array_equal(yx & 0xFFFF, xs_o[p, :cnt].astype(np.uint32))
-    del row_ptr, nz, ent
+    _compact_every_plane(nz.cpu().numpy(), rp_o, v_o, ys_o, xs_o, layer.H)
+    del row_ptr, nz, v_o, ys_o, xs_o
+    want = oracle.conv2d_f64(x, w, T, P)
     for path in ("sparse", "dense", "auto"):
         y = isc.isc_conv2d(xd, wd, T, P, path=path)
-        flat = y.view(-1)
-        idx = rng.choice(flat.numel(), size=1500, replace=False)
-        got = flat[torch.from_numpy(idx).cuda()].cpu().numpy()
-        want = oracle.conv2d_f64_at(x, w, T, P, idx)
-        assert_conv_close(got, want, "%s %s" % (layer.name, path))
+        assert_conv_close(y.cpu().numpy(), want, "%s %s" % (layer.name, path))
         del y
+    del want
     torch.cuda.empty_cache()
 
 
@@ -453,9 +455,9 @@ def test_sparse_conv_fused_rejects_ineligible(torch, isc):
 
 @pytest.mark.parametrize("case", [(3, 20, 12, 12, 50, 5, 5, 1, 0, 0.9), (2, 24, 11, 11, 33, 5, 5, 1, 1, 0.85),
                                   (2, 9, 8, 8, 64, 3, 3, 1, 1, 0.9)])
-def test_fused_weight_placements_agree(torch, isc, monkeypatch, case):
+def test_fused_weight_placements_agree(torch, isc, case):
     """Plans whose wavefronts share no channel stream the weights to
-    registers by default; the filter-in-LDS kernel (ISC_FUSED_W=0) on the
+    registers by default; the filter-in-LDS kernel (tuning kernel "fused") on the
     same shapes: both against the oracle, and bitwise equal to each other
     (the same channel order per phase and phase order per output)."""
     N, C, H, W, K, R, S, T, P, sp = case
@@ -464,10 +466,11 @@ def test_fused_weight_placements_agree(torch, isc, monkeypatch, case):
     wt = isc.isc_repack_filter(to_dev(torch, w))
     want = oracle.conv2d_f64(x, w, T, P)
     outs = []
-    for mode in ("1", "0"):
-        monkeypatch.setenv("ISC_FUSED_W", mode)
-        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
-        assert_conv_close(y, want, "fused W=%s %s" % (mode, case))
+    desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
+    assert isc.isc_sparse_kernel(desc, {"kernel": "fused"}) == "fused"
+    for tu in (None, {"kernel": "fused"}):
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning=tu).cpu().numpy()
+        assert_conv_close(y, want, "fused %s %s" % (tu, case))
         outs.append(y)
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
 
@@ -477,11 +480,11 @@ def test_fused_weight_placements_agree(torch, isc, monkeypatch, case):
                                   (2, 11, 13, 13, 200, 3, 3, 1, 1, 0.9), (40, 6, 14, 14, 70, 3, 3, 1, 1, 0.9),
                                   (2, 7, 12, 12, 130, 5, 5, 1, 2, 0.9), (2, 40, 9, 9, 100, 1, 1, 1, 0, 0.9),
                                   (3, 33, 16, 16, 80, 1, 1, 1, 0, 0.8)])
-def test_register_kernel_map_groups(torch, isc, monkeypatch, case):
+def test_register_kernel_map_groups(torch, isc, case):
     """The register-weight kernel beyond 64 maps (one workgroup per group of
     64, ragged last group included) and on 16-column tiles, every tile
     height it takes: plain and rectified with the census, against the
-    oracle; and the filter-ring kernel (ISC_FUSED_W = 0) on the same shape."""
+    oracle; and the filter-ring kernel (tuning kernel "fused_ring") on the same shape."""
     N, C, H, W, K, R, S, T, P, sp = case
     note("register kernel map groups", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
@@ -492,31 +495,30 @@ def test_register_kernel_map_groups(torch, isc, monkeypatch, case):
     Wo = want.shape[3]
     full = 4 if Wo <= 8 else 2
     for th in (full, full // 2):
-        monkeypatch.setenv("ISC_FUSED_REG_TH", str(th))
-        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+        assert isc.isc_sparse_plan(desc, {"rows": th})["rows"] == th
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning={"rows": th}).cpu().numpy()
         assert_conv_close(y, want, "register kernel th%d %s" % (th, case))
-    monkeypatch.delenv("ISC_FUSED_REG_TH")
     yc = isc.census(desc)
     z = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), T, P, path="sparse", y_census=yc,
                             ws=isc.workspace(desc, "sparse")).cpu().numpy()
     want_relu, _ = oracle.relu_conv2d_f64(x, w, T, P)
     assert_conv_close(z, want_relu, "register kernel relu %s" % (case,))
     assert isc.isc_census_read(yc) == (z.size, int(np.count_nonzero(z)))
-    monkeypatch.setenv("ISC_FUSED_W", "0")
-    other = isc.isc_sparse_kernel(desc)
+    tu = {"kernel": "fused_ring"}
+    other = isc.isc_sparse_kernel(desc, tu)
     assert other in ("fused", "fused_ring"), other
-    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P).cpu().numpy()
+    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning=tu).cpu().numpy()
     assert_conv_close(y, want, "%s kernel %s" % (other, case))
 
 
 @pytest.mark.parametrize("case", [(1, 384, 5, 5, 384, 3, 3, 1, 1, 0.9), (1, 100, 9, 7, 70, 3, 3, 1, 1, 0.5),
                                   (2, 48, 7, 7, 128, 5, 5, 1, 2, 0.9), (1, 60, 6, 6, 20, 5, 5, 1, 2, 0.3),
                                   (3, 800, 4, 4, 33, 1, 1, 1, 0, 0.6)])
-def test_dense_split_reduction(torch, isc, monkeypatch, case):
+def test_dense_split_reduction(torch, isc, case):
     """The dense path's GEMM with its reduction split over C*R*S (grids of
     fewer than 128 tiles): plain, rectified with the census, and under AUTO,
-    against the oracle; and the unsplit GEMM (ISC_GEMM_SPLIT = 0) on the same
-    shape."""
+    against the oracle; and the unsplit GEMM (tuning gemm_split = -1) on the
+    same shape."""
     N, C, H, W, K, R, S, T, P, sp = case
     note("dense split", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
@@ -533,6 +535,26 @@ def test_dense_split_reduction(torch, isc, monkeypatch, case):
     assert isc.isc_census_read(yc) == (z.size, int(np.count_nonzero(z)))
     a = isc.isc_conv2d(xd, wd, T, P, path="auto", threshold=0.99, ws=isc.workspace(desc, "auto")).cpu().numpy()
     assert_conv_close(a, want, "auto (dense) split %s" % (case,))
-    monkeypatch.setenv("ISC_GEMM_SPLIT", "0")
-    u = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=isc.workspace(desc, "dense")).cpu().numpy()
+    u = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=isc.workspace(desc, "dense"),
+                       tuning={"gemm_split": -1}).cpu().numpy()
     assert_conv_close(u, want, "dense unsplit %s" % (case,))
+
+
+def test_side_stream_parity(torch, isc):
+    """Calls enqueued on a stream other than the current one: temporaries are
+    allocated on that stream, and the results equal the oracle's after the
+    stream is synchronised, with other work running on the current stream."""
+    note("side stream")
+    x, w = workloads.make_case(4, 12, 27, 27, 100, 5, 5, 1, 2, 0.9, seed=44)
+    want = oracle.conv2d_f64(x, w, 1, 2)
+    xd, wd = to_dev(torch, x), to_dev(torch, w)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    outs = []
+    for path in ("sparse", "dense", "auto"):
+        outs.append(isc.isc_conv2d(xd, wd, 1, 2, path=path, stream=side))
+        junk = torch.empty(1 << 22, device="cuda")          # reuse pressure on the current stream
+        junk.fill_(float("nan"))
+    side.synchronize()
+    for path, y in zip(("sparse", "dense", "auto"), outs):
+        assert_conv_close(y.cpu().numpy(), want, "side stream %s" % path)

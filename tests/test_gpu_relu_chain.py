@@ -87,8 +87,8 @@ def _relu_layer(torch, isc, x, w, T, P, path, census=True, wt=None):
     desc = isc.make_desc(*x.shape, w.shape[0], w.shape[2], w.shape[3], T, P)
     yc = isc.census(desc) if census else None
     ws = isc.workspace(desc, path)
-    y = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), T, P, path=path, y_census=yc, ws=ws,
-                            wt=wt)
+    y = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), T, P, path=path, threshold=THRESHOLD,
+                            y_census=yc, ws=ws, wt=wt)
     return desc, y, yc, ws
 
 
@@ -169,8 +169,8 @@ def _chain_on_gpu(torch, isc, x0, ws_list, use_census=True, use_wt=True, path="a
         wt = isc.isc_repack_filter(wd) if use_wt else None
         yc = isc.census(desc)
         ws = isc.workspace(desc, path)
-        y = isc.isc_conv2d_relu(x, wd, 1, 1, path=path, x_census=xc if use_census else None, wt=wt,
-                                y_census=yc, ws=ws)
+        y = isc.isc_conv2d_relu(x, wd, 1, 1, path=path, threshold=THRESHOLD, x_census=xc if use_census else None,
+                                wt=wt, y_census=yc, ws=ws)
         out.append((x, y, isc.isc_decision(desc, ws), yc))
         x, xc = y, yc
     return out
@@ -222,7 +222,8 @@ def test_stale_or_foreign_census_runs_dense(torch, isc):
     garbage.fill_(0xFF)
     for xc in (foreign, garbage):
         ws = isc.workspace(desc, "auto")
-        y = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), 1, 1, x_census=xc, ws=ws)
+        y = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), 1, 1, path="auto", threshold=THRESHOLD,
+                                x_census=xc, ws=ws)
         assert_close(y.cpu().numpy(), want, "foreign census")
         nnz, taken = isc.isc_decision(desc, ws)
         assert taken == "dense" and nnz == 2 ** 64 - 1
@@ -231,24 +232,23 @@ def test_stale_or_foreign_census_runs_dense(torch, isc):
     assert e.value.status == 10
 
 
-def test_chain_full_size_sampled(torch, isc):
-    """The chain at its full size (batch 128), as the benchmark runs it:
-    outputs at sampled positions against the oracle evaluated point by point
-    on the GPU's own input of each layer, and every census against a count of
-    the output it describes."""
+@pytest.mark.parametrize("path", ["auto", "dense"])
+def test_chain_full_size_every_output(torch, isc, path):
+    """The chain at its full size (batch 128), as the benchmark runs it: every
+    output of every layer against the oracle on the GPU's own input of that
+    layer, and every census against a count of the output it describes."""
     chain = workloads.WORKLOADS["alexnet_chain345"]
     x0, ws_list = workloads.make_chain(chain)
-    note("chain full", x0.shape)
-    layers = _chain_on_gpu(torch, isc, x0, ws_list)
-    rng = np.random.default_rng(chain.layers[0].seed)
+    note("chain full", path, x0.shape)
+    layers = _chain_on_gpu(torch, isc, x0, ws_list, path=path)
     for i, ((xd, yd, (nnz_in, taken), yc), w) in enumerate(zip(layers, ws_list)):
-        assert nnz_in == int(torch.count_nonzero(xd).item())
-        assert taken == expected_path(nnz_in, xd.numel())
+        if path == "auto":
+            assert nnz_in == int(torch.count_nonzero(xd).item())
+            assert taken == expected_path(nnz_in, xd.numel())
         assert isc.isc_census_read(yc) == (yd.numel(), int(torch.count_nonzero(yd).item()))
         assert not bool(torch.signbit(yd).any())
-        idx = rng.choice(yd.numel(), size=1500, replace=False)
-        got = yd.view(-1)[torch.from_numpy(idx).cuda()].cpu().numpy()
-        want = np.maximum(oracle.conv2d_f64_at(xd.cpu().numpy(), w, 1, 1, idx), 0.0)
-        assert_close(got, want, "chain full layer %d" % i)
+        want, _ = oracle.relu_conv2d_f64(xd.cpu().numpy(), w, 1, 1)
+        assert_close(yd.cpu().numpy(), want, "chain full %s layer %d" % (path, i))
+        del want
     del layers
     torch.cuda.empty_cache()
