@@ -151,6 +151,23 @@ int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, flo
                      void *ws, size_t ws_bytes, int32_t path, float threshold,
                      const isc_tuning *tuning, void *stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * isc_conv2d with its workspace taken from a buffer the library keeps in
+ * device memory, ISC_NOALLOC_SCRATCH_BYTES on every GPU it runs on, held
+ * until the process ends.  The caller passes only inputs and outputs; the
+ * call allocates nothing.  Every call on one GPU shares that GPU's buffer:
+ * calls that overlap in time on one GPU (on different streams without
+ * synchronisation, or from several threads) race and must not be made; the
+ * buffer needs no clearing (the path writes every word it reads).
+ *   x, w, y, path, threshold, stream: as for isc_conv2d.
+ * Errors: as isc_conv2d (no WORKSPACE); LIMIT also when the workspace this
+ * descriptor and path need (isc_workspace_size) exceeds
+ * ISC_NOALLOC_SCRATCH_BYTES. */
+#define ISC_NOALLOC_SCRATCH_BYTES (16u << 20)
+int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, float *y,
+                       int32_t path, float threshold, void *stream);
+
 /* After isc_conv2d has completed on `stream` (this call synchronises the
  * stream): the number of nonzero inputs the compaction counted (UINT64_MAX
  * if the call ran the dense path only) and the path taken (ISC_PATH_SPARSE

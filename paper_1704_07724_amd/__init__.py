@@ -7,7 +7,7 @@ library (there is no fallback of any kind).
 
 The functions carry the C names:
     isc_out_shape, isc_workspace_size, isc_conv2d (isc_conv2d_tuned when a
-    tuning is given), isc_decision, isc_read_decision,
+    tuning is given), isc_conv2d_noalloc, isc_decision, isc_read_decision,
     isc_census_size, isc_conv2d_relu, isc_census_read,
     isc_conv2d_dw_workspace_size, isc_conv2d_dw,
     isc_compact, isc_repacked_filter_size, isc_repack_filter,
@@ -43,7 +43,7 @@ STATUS = {
     8: "ISC_ERR_HIP", 9: "ISC_ERR_ALIGN", 10: "ISC_ERR_ARG",
 }
 EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_conv2d_tuned", "isc_decision",
-           "isc_read_decision", "isc_sparse_plan",
+           "isc_read_decision", "isc_sparse_plan", "isc_conv2d_noalloc",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
            "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
            "isc_census_size", "isc_conv2d_relu", "isc_census_read",
@@ -124,6 +124,7 @@ def lib():
     L.isc_conv2d.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, vp]
     L.isc_conv2d_tuned.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, tp, vp]
     L.isc_decision.argtypes = [dp, vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(i32), vp]
+    L.isc_conv2d_noalloc.argtypes = [dp, vp, vp, vp, i32, ctypes.c_float, vp]
     L.isc_read_decision.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint64)]
     L.isc_sparse_plan.argtypes = [dp, tp, ctypes.POINTER(Plan)]
     L.isc_compact.argtypes = [dp, vp, vp, vp, vp, vp]
@@ -286,6 +287,27 @@ def isc_conv2d(x, w, stride=1, pad=0, path=None, threshold=None, out=None, ws=No
                                         ws.data_ptr(), _nbytes(ws), _path(path), threshold,
                                         _tuning_ref(tuning), _stream(stream))
         _check(st, "isc_conv2d")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # ISC_NOALLOC_SCRATCH_BYTES
+
+
+def isc_conv2d_noalloc(x, w, out, stride=1, pad=0, path=None, threshold=None, stream=None):
+    """isc_conv2d with the library's own per-device scratch as workspace: the
+    C call allocates nothing (x, w and out are the caller's device tensors,
+    all contiguous).  Calls that overlap in time on one GPU race."""
+    torch = _torch()
+    for t, name in ((x, "x"), (w, "w"), (out, "out")):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 or not t.is_contiguous():
+            raise TypeError("%s must be a contiguous float32 CUDA/HIP tensor" % name)
+    desc = _desc_of(x.shape, w.shape, stride, pad)
+    ho, wo = isc_out_shape(desc)
+    if tuple(out.shape) != (desc.N, desc.K, ho, wo):
+        raise ValueError("out must be [N, K, Ho, Wo]")
+    _check(lib().isc_conv2d_noalloc(ctypes.byref(desc), x.data_ptr(), w.data_ptr(), out.data_ptr(),
+                                    _path(default_path(path)), default_threshold(threshold), _stream(stream)),
+           "isc_conv2d_noalloc")
     return out
 
 

@@ -170,6 +170,30 @@ unsigned long long nnz_limit_for(int64_t total, float threshold) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? ISC_OK : ISC_ERR_HIP; }
 
+// Workspace of isc_conv2d_noalloc: a device array each GPU holds until the
+// process ends.  In host code its name is a host-side stand-in, not a device
+// address; the device address comes from hipGetSymbolAddress, once per
+// device with that device current, and only that address is ever handed to
+// a kernel or a copy.
+constexpr size_t kScratchBytes = ISC_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::atomic<void *> scratch_addr[kMaxDevices];
+
+// The current device's scratch address, looked up on the first call on the
+// device (ISC_ERR_DEVICE or ISC_ERR_HIP on failure).
+int scratch_for_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ISC_ERR_DEVICE;
+    void *p = scratch_addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return ISC_ERR_HIP;
+        scratch_addr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return ISC_OK;
+}
+
 // What isc_conv2d_relu adds to isc_conv2d: the epilogue (rectifier and
 // census of y), the census of x, and a caller's repacked filter.
 struct Chain {
@@ -365,6 +389,22 @@ int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes) {
 int isc_conv2d(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
                size_t ws_bytes, int32_t path, float threshold, void *stream) {
     return conv_impl(d, x, w, y, ws, ws_bytes, path, threshold, stream, nullptr, nullptr);
+}
+
+int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, float *y, int32_t path,
+                       float threshold, void *stream) {
+    Shape s;
+    int st = check_desc(d, &s);
+    if (st) return st;
+    if (!x || !w || !y) return ISC_ERR_NULL;
+    if (!valid_path(path)) return ISC_ERR_PATH;
+    if (layout_for(s, path).total > kScratchBytes) return ISC_ERR_LIMIT;
+    st = check_device();
+    if (st) return st;
+    void *ws = nullptr;
+    st = scratch_for_current_device(&ws);
+    if (st) return st;
+    return conv_impl(d, x, w, y, ws, kScratchBytes, path, threshold, stream, nullptr, nullptr);
 }
 
 int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,
