@@ -100,6 +100,7 @@ typedef struct isc_tuning {
     int32_t cols;          /* output columns of a wavefront's tile */
     int32_t maps_per_lane; /* output maps per lane (64 * this per wavefront) */
     int32_t phases;        /* channel phases of the filter-resident kernel */
+    int32_t waves;         /* wavefronts per workgroup of the filter-ring kernel */
     int32_t wide_loads;    /* 1: the register-weight kernel loads its weights
                               through a buffer resource on one map group too */
     int32_t gemm_split;    /* -1: the dense GEMM never splits its reduction */

@@ -65,7 +65,7 @@ KERNEL_IDS = {"none": 0, "fused": 1, "resident": 2, "ring": 3, "generic": 4, "fu
 
 class Tuning(ctypes.Structure):
     """isc_tuning: per-call plan overrides (0 = the library chooses)."""
-    _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "rows", "cols", "maps_per_lane", "phases",
+    _fields_ = [(n, ctypes.c_int32) for n in ("kernel", "rows", "cols", "maps_per_lane", "phases", "waves",
                                                "wide_loads", "gemm_split", "reserved")]
 
 

@@ -216,6 +216,7 @@ hipError_t launch_sparse_fring(const SparseShape &sh, const float *x, const floa
 // The plan the on-the-fly kernels take for a shape (false: none takes it).
 bool sparse_fused_plan_info(const SparseShape &sh, isc_plan *out);
 bool sparse_fring_plan_info(const SparseShape &sh, isc_plan *out);
+int64_t sparse_fring_max_groups(const SparseShape &sh);
 // Upper bound of the workgroups of the on-the-fly kernels' launch for a
 // shape (the census slots their epilogue may write).
 int64_t sparse_fused_max_groups(const SparseShape &sh);

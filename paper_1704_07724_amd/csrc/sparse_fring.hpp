@@ -7,9 +7,12 @@
 // branch): the input is compacted on the fly as in the filter-resident kernel
 // (sparse_fused.hip), and the filter is streamed through LDS.
 //
-// The four wavefronts of a workgroup own TH consecutive output rows each (4*TH
-// rows of one image), TW columns and 64*KPL output maps in registers (tile
-// machinery in sparse_tile.hpp).  Input channels go in order through a ring
+// The output of every image is cut into TH x TW tiles, numbered image by
+// image, row band by row band; wavefront w of workgroup b owns tile 4b + w
+// (any image: the four wavefronts share only the channel's weights), with
+// 64*KPL output maps in registers (tile machinery in sparse_tile.hpp).  The
+// flat tile list leaves no wavefront idle on a ragged last band, except in
+// the launch's last workgroup.  Input channels go in order through a ring
 // of NBUF stages: stage c holds channel c's R*S*64*KPL weights (from the
 // K-contiguous repacked filter) and each wavefront's input window of the
 // channel -- (TH+R-1) rows x (TW+S-1) columns in leaf-key order, padding
@@ -31,40 +34,53 @@ namespace isc {
 namespace fring {
 
 using tile::kLanes;
-constexpr int kWaves = 4;
 constexpr size_t kLdsMax = 160 * 1024;
-constexpr size_t kLdsPair = kLdsMax / 2;  // two workgroups per CU
 
 struct FringArgs {
     const float *x;   // N x C x H x W
     const float *wt;  // [C][R][S][Kp], K contiguous, zero past K
     float *y;         // N x K x Ho x Wo
     int N, C, H, W, K, Kp, P, Ho, Wo;
-    int TWr;          // output columns per tile in use (<= TW)
-    int ctiles;       // column tiles per row
-    int bands;        // groups of kWaves * TH output rows
+    int ctiles;       // column tiles per row band, ceil(Wo / TW)
+    int rtiles;       // row bands per image, ceil(Ho / TH)
+    int ntiles;       // N * rtiles * ctiles
     int kgroups;      // groups of 64 * KPL output maps
     Decision dec;
     Epilogue epi;     // rectifier and census of y
 };
 
-// Register tiles instantiated: (KPL, TH) per filter size and tile width,
-// with TH * TW * KPL accumulators and R*S*KPL weights per lane.
+// A register tile: KPL maps per lane, TH x TW outputs, so TH * TW * KPL
+// accumulators and R*S*KPL weights per lane; NW wavefronts per workgroup
+// share each stage of the ring (4: two workgroups per CU, each with half
+// of the LDS; 8: one workgroup per CU with all of it, so a deeper ring and
+// half the weight traffic per wavefront).
 struct TileChoice {
-    int kpl, th;
+    int kpl, th, tw, nw;
 };
 
-constexpr int kMaxAcc = 112;      // accumulators per lane
-constexpr int kMaxRegs = 212;     // accumulators + weights per lane
+constexpr int kMaxAcc = 160;      // accumulators per lane
+constexpr int kMaxRegs = 216;     // accumulators + weights per lane
 
 constexpr bool fring_fits(int RS, int KPL, int TH, int TW) {
     return TH * TW * KPL <= kMaxAcc && TH * TW * KPL + RS * RS * KPL <= kMaxRegs;
 }
 
+// The tiles compiled for each filter size, the choice's candidates.  Tall
+// tiles feed every scanned nonzero to more outputs (R x S filters: up to
+// TH*TW*R*S / ((TH+R-1)(TW+S-1)) taps, times KPL maps per lane), which is
+// what the scan's scalar work per nonzero is paid against; narrow ones fit
+// the 13-, 14-, 27- and 28-column maps without ragged edges.
+constexpr TileChoice kTiles5[] = {{4, 4, 7, 4}, {4, 3, 9, 4}, {4, 1, 28, 4}, {2, 2, 28, 4}, {2, 1, 28, 4},
+                                  {1, 2, 28, 4}, {4, 1, 16, 4}, {2, 2, 16, 4}, {1, 2, 16, 4}, {4, 4, 7, 8}};
+constexpr TileChoice kTiles3[] = {{6, 2, 13, 4}, {4, 2, 16, 4}, {6, 1, 16, 4}, {2, 2, 28, 4}, {2, 1, 28, 4},
+                                  {4, 1, 28, 4}, {1, 2, 28, 4}, {1, 2, 16, 4}, {2, 4, 16, 4}, {2, 2, 28, 8}};
+constexpr TileChoice kTiles1[] = {{6, 2, 13, 4}, {6, 1, 16, 4}, {4, 2, 16, 4}, {4, 1, 28, 4}, {2, 2, 28, 4},
+                                  {1, 2, 16, 4}};
+
 // Launchers of the kernels of one filter size (sparse_fring_r{1,3,5}.hip).
-hipError_t launch_r1(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
-hipError_t launch_r3(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
-hipError_t launch_r5(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s);
+hipError_t launch_r1(const FringArgs &a, const TileChoice &tc, hipStream_t s);
+hipError_t launch_r3(const FringArgs &a, const TileChoice &tc, hipStream_t s);
+hipError_t launch_r5(const FringArgs &a, const TileChoice &tc, hipStream_t s);
 
 }  // namespace fring
 }  // namespace isc
@@ -74,31 +90,40 @@ namespace isc {
 namespace fring {
 namespace {
 
-template <int RS_, int KPL, int TH, int TW>
+template <int RS_, int KPL, int TH, int TW, int NW>
 struct FringShape {
     using T = tile::Shape<RS_, RS_, KPL, TH, TW>;
+    static constexpr int kWaves = NW;
     static constexpr int RS2 = RS_ * RS_;
     static constexpr int CHF = RS2 * T::KW;                  // floats of one channel's weights
     static constexpr int NDW = (CHF + 255) / 256;            // 1 KB direct-to-LDS blocks
     static constexpr int SLOT4 = NDW * kLanes;               // float4 per ring slot
     static constexpr size_t SLOTB = sizeof(float4) * SLOT4;  // bytes of one stage's weights
-    static constexpr int WIN4 = kWaves * T::EPL * kLanes / 4;             // float4 of its windows
+    static constexpr int WIN4 = NW * T::EPL * kLanes / 4;    // float4 of its windows
     static constexpr size_t WINB = sizeof(float4) * WIN4;
-    // stages: up to 4 for slots of <= 16 KB, 3 for <= 32 KB, else 2, and no
-    // more than leave room for two workgroups per CU
-    static constexpr int NPREF = SLOTB <= 16384 ? 4 : (SLOTB <= 32768 ? 3 : 2);
-    static constexpr int NBUF = NPREF >= 4 && 4 * (SLOTB + WINB) <= kLdsPair   ? 4
-                                : NPREF >= 3 && 3 * (SLOTB + WINB) <= kLdsPair ? 3
-                                                                               : 2;
-    static constexpr int DPW = (NDW + kWaves - 1) / kWaves;  // weight blocks per wavefront per stage
+    static constexpr int DPW = (NDW + NW - 1) / NW;          // weight blocks per wavefront per stage
     static constexpr int VPS = DPW + T::EPL;                 // vector-memory operations per stage
+    // stages: up to 4 for slots of <= 16 KB, 3 for <= 32 KB, else 2, within
+    // the workgroup's share of LDS (half of it for four wavefronts, so that
+    // two workgroups share a CU) and few enough that the wait for the stage
+    // consumed fits the vmcnt field.  Deeper rings measured slower: the LDS
+    // they take costs resident workgroups (six stages for the inception 3x3
+    // branch on 1 x 28 tiles: 0.205 -> 0.284 ms)
+    static constexpr size_t BUDGET = NW == 4 ? kLdsMax / 2 : kLdsMax;
+    static constexpr int NPREF = SLOTB <= 16384 ? 4 : (SLOTB <= 32768 ? 3 : 2);
+    static constexpr int NFIT = static_cast<int>(BUDGET / (SLOTB + WINB));
+    static constexpr int NVM = 63 / VPS + 2;
+    static constexpr int NCAP = NFIT < NVM ? NFIT : NVM;
+    static constexpr int NBUF = NPREF < NCAP ? NPREF : NCAP;
+    static_assert(NBUF >= 2, "ring needs two stages");
     static constexpr size_t lds = NBUF * (SLOTB + WINB);
 };
 
-template <int RS_, int KPL, int TH, int TW>
-__global__ __launch_bounds__(kWaves * kLanes)
+template <int RS_, int KPL, int TH, int TW, int NW>
+__global__ __launch_bounds__(NW * kLanes)
 void sparse_conv_fring_kernel(FringArgs a) {
-    using SH = FringShape<RS_, KPL, TH, TW>;
+    using SH = FringShape<RS_, KPL, TH, TW, NW>;
+    constexpr int kWaves = NW;
     using T = typename SH::T;
     constexpr int KW = T::KW, NDW = SH::NDW, NBUF = SH::NBUF, DPW = SH::DPW, EPL = T::EPL;
 
@@ -112,19 +137,21 @@ void sparse_conv_fring_kernel(FringArgs a) {
 
     const int lane = threadIdx.x & (kLanes - 1);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
-    int b = blockIdx.x;
-    const int kg = b % a.kgroups;
-    b /= a.kgroups;
-    const int ct = b % a.ctiles;
-    b /= a.ctiles;
-    const int band = b % a.bands;
-    const int n = b / a.bands;
-    const int oy0 = (band * kWaves + wave) * TH;
-    const int ox0 = ct * a.TWr;
+    const int kg = blockIdx.x % a.kgroups;
+    // this wavefront's tile (past the last tile: the last tile's addresses,
+    // nothing counted, nothing stored)
+    const int tile = (blockIdx.x / a.kgroups) * kWaves + wave;
+    const bool rows_ok = tile < a.ntiles;
+    int t = rows_ok ? tile : a.ntiles - 1;
+    const int ct = t % a.ctiles;
+    t /= a.ctiles;
+    const int band = t % a.rtiles;
+    const int n = t / a.rtiles;
+    const int oy0 = band * TH;
+    const int ox0 = ct * TW;
     const int kbase = kg * KW;
     const int C = a.C, H = a.H, W = a.W, P = a.P, Kp = a.Kp;
-    const bool rows_ok = oy0 < a.Ho;
-    const int tw = min(a.TWr, a.Wo - ox0);
+    const int tw = min(TW, a.Wo - ox0);
     const size_t HW = static_cast<size_t>(H) * W;
     const float *x_n = a.x + static_cast<size_t>(n) * C * HW;
 
@@ -225,38 +252,44 @@ void sparse_conv_fring_kernel(FringArgs a) {
     }
 }
 
-template <int RS_, int KPL, int TH, int TW>
+template <int RS_, int KPL, int TH, int TW, int NW>
 hipError_t launch_fring_t(const FringArgs &a, hipStream_t s) {
     if constexpr (!fring_fits(RS_, KPL, TH, TW)) {
         return hipErrorInvalidValue;
     } else {
-        using SH = FringShape<RS_, KPL, TH, TW>;
+        using SH = FringShape<RS_, KPL, TH, TW, NW>;
+        constexpr int kWaves = NW;
         static_assert(SH::lds <= kLdsMax, "weight ring exceeds LDS");
-        const int64_t grid = static_cast<int64_t>(a.N) * a.bands * a.ctiles * a.kgroups;
+        const int64_t grid = static_cast<int64_t>((a.ntiles + kWaves - 1) / kWaves) * a.kgroups;
         if (a.epi.census && census_slots_for(grid) > a.epi.cap) return hipErrorInvalidValue;
-        sparse_conv_fring_kernel<RS_, KPL, TH, TW><<<static_cast<unsigned>(grid), kWaves * kLanes, 0, s>>>(a);
+        sparse_conv_fring_kernel<RS_, KPL, TH, TW, NW><<<static_cast<unsigned>(grid), kWaves * kLanes, 0, s>>>(a);
         return hipGetLastError();
     }
 }
 
-template <int RS_, int KPL, int TW>
-hipError_t launch_fring_th(const FringArgs &a, int th, hipStream_t s) {
-    return th == 2 ? launch_fring_t<RS_, KPL, 2, TW>(a, s) : launch_fring_t<RS_, KPL, 1, TW>(a, s);
-}
-
-template <int RS_, int TW>
-hipError_t launch_fring_kpl(const FringArgs &a, const TileChoice &tc, hipStream_t s) {
-    switch (tc.kpl) {
-    case 6: return launch_fring_th<RS_, 6, TW>(a, tc.th, s);
-    case 4: return launch_fring_th<RS_, 4, TW>(a, tc.th, s);
-    case 2: return launch_fring_th<RS_, 2, TW>(a, tc.th, s);
-    default: return launch_fring_th<RS_, 1, TW>(a, tc.th, s);
+// The launcher of table entry I of TILES when it is the chosen tile, else
+// the next entry's.
+template <int RS_, const TileChoice *TILES, int I, int NT>
+hipError_t launch_fring_table(const FringArgs &a, const TileChoice &tc, hipStream_t s) {
+    if constexpr (I >= NT) {
+        return hipErrorInvalidValue;
+    } else {
+        constexpr TileChoice t = TILES[I];
+        if (tc.kpl == t.kpl && tc.th == t.th && tc.tw == t.tw && tc.nw == t.nw)
+            return launch_fring_t<RS_, t.kpl, t.th, t.tw, t.nw>(a, s);
+        return launch_fring_table<RS_, TILES, I + 1, NT>(a, tc, s);
     }
 }
 
 template <int RS_>
-hipError_t launch_fring_rs(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s) {
-    return tw == 16 ? launch_fring_kpl<RS_, 16>(a, tc, s) : launch_fring_kpl<RS_, 28>(a, tc, s);
+hipError_t launch_fring_rs(const FringArgs &a, const TileChoice &tc, hipStream_t s) {
+    if constexpr (RS_ == 5) {
+        return launch_fring_table<5, kTiles5, 0, sizeof(kTiles5) / sizeof(kTiles5[0])>(a, tc, s);
+    } else if constexpr (RS_ == 3) {
+        return launch_fring_table<3, kTiles3, 0, sizeof(kTiles3) / sizeof(kTiles3[0])>(a, tc, s);
+    } else {
+        return launch_fring_table<1, kTiles1, 0, sizeof(kTiles1) / sizeof(kTiles1[0])>(a, tc, s);
+    }
 }
 
 }  // namespace

@@ -6,8 +6,8 @@
 namespace isc {
 namespace fring {
 
-hipError_t launch_r1(const FringArgs &a, int tw, const TileChoice &tc, hipStream_t s) {
-    return launch_fring_rs<1>(a, tw, tc, s);
+hipError_t launch_r1(const FringArgs &a, const TileChoice &tc, hipStream_t s) {
+    return launch_fring_rs<1>(a, tc, s);
 }
 
 }  // namespace fring

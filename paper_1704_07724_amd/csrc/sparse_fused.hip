@@ -57,7 +57,13 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
     if (sh.R != sh.S || !(sh.R == 1 || sh.R == 3 || sh.R == 5)) return false;
     if (!(sh.T == 1 || (sh.T == 2 && sh.R > 1 && sh.Wo <= 8))) return false;
     if (sh.Wo > 28) return false;
-    if (sh.K > kLanes) return fused_wreg_plan(sh, plan);  // only the register-weight kernel takes K > 64
+    // beyond 64 maps only the register-weight kernel (one wavefront per 64
+    // maps and channel phase), where it takes the shape and the caller does
+    // not ask for the filter-ring kernel: at 13 x 13 and sparsity 0.95
+    // (AlexNet conv3-5) it beat every tile of the filter-ring kernel by
+    // 12-30 %, the ring's tiles of up to 384 maps leaving CUs idle or
+    // waiting on each channel's stage
+    if (sh.K > kLanes) return fused_wreg_plan(sh, plan);
     const int crs = sh.C * sh.R * sh.S;
     // a filter too large for LDS: only the register-weight kernel, which
     // keeps none of it there, takes it (one phase per wavefront)
@@ -96,12 +102,11 @@ bool fused_plan(const SparseShape &sh, FusedPlan *plan) {
 
 // The filter-resident kernel launches N * bands <= N * Ho workgroups; its
 // register-weight variant N * bands * map groups, with bands <= Ho; the
-// filter-ring kernel N * bands * column tiles * map groups, with bands <=
-// ceil(Ho / 4), column tiles <= ceil(Wo / 16) and map groups <= ceil(K / 64).
+// filter-ring kernel at most what its largest grid over its compiled tiles
+// is (sparse_fring_max_groups).
 int64_t sparse_fused_max_groups(const SparseShape &sh) {
-    const int64_t ring = static_cast<int64_t>((sh.Ho + 3) / 4) * ((sh.Wo + 15) / 16) * ((sh.K + 63) / 64);
-    const int64_t reg = static_cast<int64_t>(sh.Ho) * ((sh.K + 63) / 64);  // register-weight kernel
-    return static_cast<int64_t>(sh.N) * std::max(ring, reg);
+    const int64_t reg = static_cast<int64_t>(sh.N) * sh.Ho * ((sh.K + 63) / 64);  // register-weight kernel
+    return std::max(reg, sparse_fring_max_groups(sh));
 }
 
 bool sparse_fused_applies(const SparseShape &sh) {

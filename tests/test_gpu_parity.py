@@ -481,33 +481,36 @@ def test_fused_weight_placements_agree(torch, isc, case):
                                   (2, 7, 12, 12, 130, 5, 5, 1, 2, 0.9), (2, 40, 9, 9, 100, 1, 1, 1, 0, 0.9),
                                   (3, 33, 16, 16, 80, 1, 1, 1, 0, 0.8)])
 def test_register_kernel_map_groups(torch, isc, case):
-    """The register-weight kernel beyond 64 maps (one workgroup per group of
-    64, ragged last group included) and on 16-column tiles, every tile
-    height it takes: plain and rectified with the census, against the
-    oracle; and the filter-ring kernel (tuning kernel "fused_ring") on the same shape."""
+    """The register-weight kernel (tuning kernel "fused_reg") beyond 64 maps
+    (one workgroup per group of 64, ragged last group included) and on
+    16-column tiles, every tile height it takes: plain and rectified with the
+    census, against the oracle; and the filter-ring kernel (tuning kernel
+    "fused_ring") on the same shape."""
     N, C, H, W, K, R, S, T, P, sp = case
     note("register kernel map groups", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
-    assert isc.isc_sparse_kernel(desc) == "fused_reg"
+    reg = {"kernel": "fused_reg"}
+    assert isc.isc_sparse_kernel(desc, reg) == "fused_reg"
     x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=83 + sum(case[:9]))
     wt = isc.isc_repack_filter(to_dev(torch, w))
     want = oracle.conv2d_f64(x, w, T, P)
     Wo = want.shape[3]
     full = 4 if Wo <= 8 else 2
     for th in (full, full // 2):
-        assert isc.isc_sparse_plan(desc, {"rows": th})["rows"] == th
-        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning={"rows": th}).cpu().numpy()
+        tu = {"kernel": "fused_reg", "rows": th}
+        assert isc.isc_sparse_plan(desc, tu)["rows"] == th
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning=tu).cpu().numpy()
         assert_conv_close(y, want, "register kernel th%d %s" % (th, case))
     yc = isc.census(desc)
     z = isc.isc_conv2d_relu(to_dev(torch, x), to_dev(torch, w), T, P, path="sparse", y_census=yc,
-                            ws=isc.workspace(desc, "sparse")).cpu().numpy()
+                            ws=isc.workspace(desc, "sparse"), tuning=reg).cpu().numpy()
     want_relu, _ = oracle.relu_conv2d_f64(x, w, T, P)
     assert_conv_close(z, want_relu, "register kernel relu %s" % (case,))
     assert isc.isc_census_read(yc) == (z.size, int(np.count_nonzero(z)))
-    tu = {"kernel": "fused_ring"}
-    other = isc.isc_sparse_kernel(desc, tu)
+    ring = {"kernel": "fused_ring"}
+    other = isc.isc_sparse_kernel(desc, ring)
     assert other in ("fused", "fused_ring"), other
-    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning=tu).cpu().numpy()
+    y = isc.isc_sparse_conv_fused(to_dev(torch, x), wt, T, P, tuning=ring).cpu().numpy()
     assert_conv_close(y, want, "%s kernel %s" % (other, case))
 
 
@@ -558,3 +561,42 @@ def test_side_stream_parity(torch, isc):
     side.synchronize()
     for path, y in zip(("sparse", "dense", "auto"), outs):
         assert_conv_close(y.cpu().numpy(), want, "side stream %s" % path)
+
+
+def _ring_tiles():
+    """The filter-ring kernel's compiled tiles, read from its header:
+    (R, maps per lane, rows, cols, wavefronts per workgroup)."""
+    import os
+    import re
+    src = open(os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_1704_07724_amd",
+                            "csrc", "sparse_fring.hpp")).read()
+    out = []
+    for r in (1, 3, 5):
+        body = re.search(r"kTiles%d\[\] = \{(.*?)\};" % r, src, re.S).group(1)
+        for t in re.findall(r"\{(\d+), (\d+), (\d+), (\d+)\}", body):
+            out.append((r,) + tuple(int(v) for v in t))
+    return out
+
+
+@pytest.mark.parametrize("tile", _ring_tiles(), ids=lambda t: "R%d-kpl%d-%dx%d-w%d" % t)
+def test_every_ring_tile(torch, isc, tile):
+    """Every compiled tile of the filter-ring kernel, forced through the
+    per-call overrides, against the oracle on maps with ragged row bands and
+    column tiles, a ragged last map group and a partly filled last
+    workgroup; and bitwise on integer inputs."""
+    R, kpl, th, tw, nw = tile
+    tu = {"kernel": "fused_ring", "maps_per_lane": kpl, "rows": th, "cols": tw, "waves": nw}
+    for case in [(2, 5, 17, 19, 70, R, R, 1, R // 2, 0.85), (1, 3, 11, 30, 200, R, R, 1, R // 2, 0.9)]:
+        N, C, H, W, K, _, _, T, P, sp = case
+        note("ring tile", tile, case)
+        desc = isc.make_desc(N, C, H, W, K, R, R, T, P)
+        plan = isc.isc_sparse_plan(desc, tu)
+        assert (plan["kernel"], plan["maps_per_lane"], plan["rows"], plan["cols"], plan["waves"]) == \
+            ("fused_ring", kpl, th, tw, nw), plan
+        x, w = workloads.make_case(N, C, H, W, K, R, R, T, P, sp, seed=101 + sum(case[:5]) + kpl * 7 + th * 3 + tw)
+        y = isc.isc_sparse_conv_fused(to_dev(torch, x), isc.isc_repack_filter(to_dev(torch, w)), T, P,
+                                      tuning=tu).cpu().numpy()
+        assert_conv_close(y, oracle.conv2d_f64(x, w, T, P), "ring tile %s %s" % (tile, case))
+        xi, wi = workloads.integer_case(N, C, H, W, K, R, R, seed=5 + kpl + th + tw)
+        yi = isc.isc_sparse_conv_fused(to_dev(torch, xi), isc.isc_repack_filter(to_dev(torch, wi)), T, P, tuning=tu)
+        assert np.array_equal(yi.cpu().numpy().astype(np.float64), oracle.conv2d_f64(xi, wi, T, P))
