@@ -281,6 +281,9 @@ class LayerRun:
             out["tflops_%s" % path] = round(f / (res["t_%s_ms" % path] * 1e-3) / 1e12, 3)
         out["nonzero_mac_per_s_auto"] = nzm / (res["t_auto_ms"] * 1e-3)
         out["speedup_auto_vs_dense"] = round(res["t_dense_ms"] / res["t_auto_ms"], 3)
+        # AUTO's time over the faster of the two forced paths (1.0: the
+        # dispatcher chose the faster path at no cost)
+        out["auto_vs_best"] = round(res["t_auto_ms"] / min(res["t_sparse_ms"], res["t_dense_ms"]), 3)
         out["speedup_sparse_vs_dense"] = round(res["t_dense_ms"] / res["t_sparse_ms"], 3)
         out["sparse_kernel_tflops_nonzero"] = round(2 * nzm / (res["t_sparse_kernel_ms"] * 1e-3) / 1e12, 3)
         out["sparse_kernel_frac_valu_peak"] = round(out["sparse_kernel_tflops_nonzero"] / VALU_F32_PEAK_TFLOPS, 4)
@@ -541,7 +544,7 @@ def sweep_point(torch, isc, cold, layer, reps, graphs, run=None):
     sm = run.summary(run.measure(cold, reps, graphs))
     keep = ("target_sparsity", "measured_sparsity", "t_auto_ms", "t_sparse_ms", "t_dense_ms",
             "t_compact_ms", "t_sparse_kernel_ms", "warm_auto_ms", "warm_sparse_kernel_ms", "tflops_auto",
-            "tflops_sparse", "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense",
+            "tflops_sparse", "tflops_dense", "nonzero_mac_per_s_auto", "speedup_auto_vs_dense", "auto_vs_best",
             "speedup_sparse_vs_dense", "sparse_kernel_tflops_nonzero", "sparse_kernel_frac_valu_peak",
             "dense_frac_mfma_peak")
     out = {k: sm[k] for k in keep}
@@ -704,8 +707,8 @@ def main():
                 dws = (" | dw sparse %.4f ms library %.4f (%.2fx)" % (
                     s["t_dw_sparse_ms"], s["t_dw_library_ms"], s["speedup_dw_vs_library"])
                        if "t_dw_sparse_ms" in s else "")
-                print("# %s: auto %.4f ms (%s) sparse %.4f dense %.4f speedup %.2fx library %.4f (%.2fx)%s" % (
-                    layer.name, s["t_auto_ms"], s["auto_path"], s["t_sparse_ms"], s["t_dense_ms"],
+                print("# %s: auto %.4f ms (%s, %.3f of best) sparse %.4f dense %.4f speedup %.2fx library %.4f (%.2fx)%s" % (
+                    layer.name, s["t_auto_ms"], s["auto_path"], s["auto_vs_best"], s["t_sparse_ms"], s["t_dense_ms"],
                     s["speedup_sparse_vs_dense"], s["t_library_ms"], s["speedup_sparse_vs_library"], dws),
                       file=sys.stderr, flush=True)
                 del run

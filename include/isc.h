@@ -169,6 +169,14 @@ int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, flo
 int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, float *y,
                        int32_t path, float threshold, void *stream);
 
+/* The per-shape crossover AUTO uses under ISC_THRESHOLD_CROSSOVER: the
+ * smallest input sparsity (fraction of zero inputs, the definition under
+ * Tab. 2) at which it takes the sparse path, from models of both paths'
+ * times on this GPU for the plans this descriptor gets; 2.0 when the sparse
+ * path is never expected to win (for example 1x1 filters at large batch).
+ * Host-only.  Errors: NULL, SHAPE, LIMIT. */
+int isc_crossover_sparsity(const isc_conv_desc *d, double *sparsity);
+
 /* After isc_conv2d has completed on `stream` (this call synchronises the
  * stream): the number of nonzero inputs the compaction counted (UINT64_MAX
  * if the call ran the dense path only) and the path taken (ISC_PATH_SPARSE

@@ -12,6 +12,7 @@ The functions carry the C names:
     isc_conv2d_dw_workspace_size, isc_conv2d_dw,
     isc_compact, isc_repacked_filter_size, isc_repack_filter,
     isc_sparse_conv, isc_sparse_conv_fused, isc_sparse_kernel, isc_sparse_plan,
+    isc_crossover_sparsity,
     isc_im2col, isc_gemm_f32, isc_status_str, isc_version
 
 Defaults a user may set in the environment (read here, by the binding, at
@@ -43,7 +44,7 @@ STATUS = {
     8: "ISC_ERR_HIP", 9: "ISC_ERR_ALIGN", 10: "ISC_ERR_ARG",
 }
 EXPORTS = ("isc_out_shape", "isc_workspace_size", "isc_conv2d", "isc_conv2d_tuned", "isc_decision",
-           "isc_read_decision", "isc_sparse_plan", "isc_conv2d_noalloc",
+           "isc_read_decision", "isc_sparse_plan", "isc_conv2d_noalloc", "isc_crossover_sparsity",
            "isc_compact", "isc_repacked_filter_size", "isc_repack_filter", "isc_sparse_conv",
            "isc_im2col", "isc_gemm_f32", "isc_sparse_conv_fused", "isc_sparse_kernel",
            "isc_census_size", "isc_conv2d_relu", "isc_census_read",
@@ -125,6 +126,7 @@ def lib():
     L.isc_conv2d_tuned.argtypes = [dp, vp, vp, vp, vp, sz, i32, ctypes.c_float, tp, vp]
     L.isc_decision.argtypes = [dp, vp, sz, ctypes.POINTER(ctypes.c_uint64), ctypes.POINTER(i32), vp]
     L.isc_conv2d_noalloc.argtypes = [dp, vp, vp, vp, i32, ctypes.c_float, vp]
+    L.isc_crossover_sparsity.argtypes = [dp, ctypes.POINTER(ctypes.c_double)]
     L.isc_read_decision.argtypes = [vp, ctypes.POINTER(i32), ctypes.POINTER(ctypes.c_uint64)]
     L.isc_sparse_plan.argtypes = [dp, tp, ctypes.POINTER(Plan)]
     L.isc_compact.argtypes = [dp, vp, vp, vp, vp, vp]
@@ -495,6 +497,14 @@ def isc_sparse_kernel(desc: ConvDesc, tuning=None) -> str:
     which = ctypes.c_int32(-1)
     _check(lib().isc_sparse_kernel(ctypes.byref(desc), ctypes.byref(which)), "isc_sparse_kernel")
     return KERNEL_NAMES[which.value]
+
+
+def isc_crossover_sparsity(desc: ConvDesc) -> float:
+    """The sparsity at or above which AUTO (per-shape crossover) takes the
+    sparse path for desc; 2.0 when it never does."""
+    v = ctypes.c_double()
+    _check(lib().isc_crossover_sparsity(ctypes.byref(desc), ctypes.byref(v)), "isc_crossover_sparsity")
+    return v.value
 
 
 def isc_sparse_plan(desc: ConvDesc, tuning=None) -> dict:

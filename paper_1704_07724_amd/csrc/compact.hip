@@ -25,7 +25,7 @@ namespace isc {
 namespace {
 
 constexpr int kWaves = 4;    // wavefronts per workgroup
-constexpr int kUnroll = 8;   // 64-element chunks loaded before the ballots
+constexpr int kUnroll = 16;  // 64-element chunks loaded before the ballots (a 32 x 32 plane at once)
 
 __device__ __forceinline__ uint32_t lanes_below(unsigned long long mask) {
     return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
@@ -106,8 +106,19 @@ void count_kernel(const int32_t *__restrict__ row_ptr, int planes, int H,
                   unsigned long long *__restrict__ total) {
     __shared__ unsigned long long part[kCountThreads / 64];
     unsigned long long s = 0;
-    for (int p = threadIdx.x; p < planes; p += kCountThreads)
-        s += static_cast<uint32_t>(row_ptr[static_cast<size_t>(p) * (H + 1) + H]);
+    // eight loads in flight per thread (the counts are H + 1 words apart:
+    // one load per L2 round trip would leave the tail latency-bound)
+    for (int p0 = threadIdx.x; p0 < planes; p0 += 8 * kCountThreads) {
+        uint32_t v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int p = min(p0 + j * kCountThreads, planes - 1);
+            v[j] = static_cast<uint32_t>(row_ptr[static_cast<size_t>(p) * (H + 1) + H]);
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (p0 + j * kCountThreads < planes) s += v[j];
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
@@ -126,12 +137,13 @@ __device__ __forceinline__ void repack_tile(const float *__restrict__ w, int K, 
                                             float *__restrict__ wt, int qt, int kt, float (&tile)[64][65]) {
     const int q0 = qt * 64, k0 = kt * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < 64; i += kWaves) {
+    const int waves = static_cast<int>(blockDim.x >> 6);
+    for (int i = ty; i < 64; i += waves) {
         const int k = k0 + i, q = q0 + tx;
         tile[i][tx] = (k < K && q < CRS) ? w[static_cast<size_t>(k) * CRS + q] : 0.0f;
     }
     __syncthreads();
-    for (int i = ty; i < 64; i += kWaves) {
+    for (int i = ty; i < 64; i += waves) {
         const int q = q0 + i, k = k0 + tx;
         if (q < CRS && k < Kp) wt[static_cast<size_t>(q) * Kp + k] = tile[tx][i];
     }
@@ -174,15 +186,27 @@ void prep_kernel(const float *__restrict__ x, int planes, int H, int W, int32_t 
 }
 
 // Nonzero count of x (total elements) in per-workgroup parts, for the
-// sparse/dense decision when no compaction runs: workgroup b counts one
-// contiguous chunk; workgroup 0 also zeroes parts[groups .. nparts).
-constexpr int kCountUnroll = 8;
+// sparse/dense decision when no compaction runs (ISC step 1's count without
+// the list): workgroup b counts one contiguous chunk of whole 16-byte
+// groups, eight of them in flight per thread (32 MB in flight over the
+// launch: a cold read of AlexNet conv2's input in one round trip);
+// workgroup 0 also counts
+// the elements before the first 16-byte boundary and zeroes parts[groups ..
+// nparts), the last one counts the elements after the last whole group.
+// The workgroups past `groups` repack the filter, one 64 x 64 tile each.
+constexpr int kCountWaves = 16;   // 1024 threads
+constexpr int kCountUnroll = 8;   // 16-byte loads in flight per thread
 
-__global__ __launch_bounds__(kWaves * 64)
-void count_parts_kernel(const float *__restrict__ x, int64_t total, uint32_t *__restrict__ parts, int groups,
-                        int nparts, const float *__restrict__ w, int K, int Kp, int CRS, int qtiles,
+__device__ __forceinline__ uint32_t nz4(const float4 &v) {
+    return ((__float_as_uint(v.x) & 0x7fffffffu) != 0u) + ((__float_as_uint(v.y) & 0x7fffffffu) != 0u) +
+           ((__float_as_uint(v.z) & 0x7fffffffu) != 0u) + ((__float_as_uint(v.w) & 0x7fffffffu) != 0u);
+}
+
+__global__ __launch_bounds__(kCountWaves * 64)
+void count_parts_kernel(const float *__restrict__ x, int64_t total, int head, uint32_t *__restrict__ parts,
+                        int groups, int nparts, const float *__restrict__ w, int K, int Kp, int CRS, int qtiles,
                         float *__restrict__ wt) {
-    __shared__ uint32_t wave_count[kWaves];
+    __shared__ uint32_t wave_count[kCountWaves];
     __shared__ float tile[64][65];
     const int b = blockIdx.x;
     if (b >= groups) {  // filter repack, one 64 x 64 tile per workgroup
@@ -190,31 +214,43 @@ void count_parts_kernel(const float *__restrict__ x, int64_t total, uint32_t *__
         repack_tile(w, K, Kp, CRS, wt, t % qtiles, t / qtiles, tile);
         return;
     }
-    const int64_t chunk = (total + groups - 1) / groups;
+    constexpr int kThreads = kCountWaves * 64;
+    // x[head ..] is 16-byte aligned; n4 whole groups of four follow
+    const int64_t n4 = (total - head) / 4;
+    const float4 *x4 = reinterpret_cast<const float4 *>(x + head);
+    const int64_t chunk = (n4 + groups - 1) / groups;
     const int64_t beg = b * chunk;
-    const int64_t end = min(total, beg + chunk);
+    const int64_t end = min(n4, beg + chunk);
     uint32_t cnt = 0;
-    for (int64_t e0 = beg + threadIdx.x; e0 < end; e0 += static_cast<int64_t>(kWaves) * 64 * kCountUnroll) {
-        uint32_t bits[kCountUnroll];
+    for (int64_t g0 = beg + threadIdx.x; g0 < end; g0 += static_cast<int64_t>(kThreads) * kCountUnroll) {
+        float4 v[kCountUnroll];
 #pragma unroll
         for (int u = 0; u < kCountUnroll; ++u) {
-            const int64_t e = e0 + static_cast<int64_t>(u) * kWaves * 64;
-            bits[u] = e < end ? __float_as_uint(x[e]) : 0u;
+            const int64_t g = g0 + static_cast<int64_t>(u) * kThreads;
+            v[u] = x4[g < end ? g : beg];  // past the end: an element already counted, not added
         }
 #pragma unroll
-        for (int u = 0; u < kCountUnroll; ++u) cnt += (bits[u] & 0x7fffffffu) != 0u ? 1u : 0u;
+        for (int u = 0; u < kCountUnroll; ++u)
+            if (g0 + static_cast<int64_t>(u) * kThreads < end) cnt += nz4(v[u]);
+    }
+    if (b == 0 && static_cast<int>(threadIdx.x) < head)
+        cnt += (__float_as_uint(x[threadIdx.x]) & 0x7fffffffu) != 0u;
+    if (b == groups - 1) {
+        const int64_t t0 = head + 4 * n4;  // at most 3 elements after the last whole group
+        if (t0 + static_cast<int64_t>(threadIdx.x) < total)
+            cnt += (__float_as_uint(x[t0 + threadIdx.x]) & 0x7fffffffu) != 0u;
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
     if ((threadIdx.x & 63) == 0) wave_count[threadIdx.x >> 6] = cnt;
     if (b == 0) {
-        for (int i = groups + static_cast<int>(threadIdx.x); i < nparts; i += kWaves * 64) parts[i] = 0u;
+        for (int i = groups + static_cast<int>(threadIdx.x); i < nparts; i += kThreads) parts[i] = 0u;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t s = 0;
 #pragma unroll
-        for (int i = 0; i < kWaves; ++i) s += wave_count[i];
+        for (int i = 0; i < kCountWaves; ++i) s += wave_count[i];
         parts[b] = s;
     }
 }
@@ -265,17 +301,24 @@ hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, floa
     return hipGetLastError();
 }
 
+// At most 256 counting workgroups, so that the decision sums at most 256
+// parts: one 16-byte load per lane of one wavefront.
+constexpr int kCountGroups = 256;
+
 hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s,
                               const float *w, int K, int C, int R, int S, float *wt) {
-    const int64_t per = static_cast<int64_t>(kWaves) * 64 * kCountUnroll * 2;  // elements per workgroup, at least
-    const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kMaxParts, (total + per - 1) / per)));
+    const int64_t per = static_cast<int64_t>(kCountWaves) * 64 * kCountUnroll * 4;  // elements per workgroup, at least
+    const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kCountGroups, (total + per - 1) / per)));
     const int np = (groups + 3) / 4 * 4;
     const int CRS = C * R * S;
     const int Kp = (K + 63) / 64 * 64;
     const int qtiles = (CRS + 63) / 64;
     const int tiles = w ? qtiles * (Kp / 64) : 0;
-    count_parts_kernel<<<groups + tiles, kWaves * 64, 0, s>>>(x, total, parts, groups, np, w, K, Kp, CRS, qtiles,
-                                                              wt);
+    // elements before the first 16-byte boundary (x is 4-byte aligned)
+    const int head = static_cast<int>(std::min<int64_t>(
+        total, ((16 - reinterpret_cast<uintptr_t>(x) % 16) % 16) / 4));
+    count_parts_kernel<<<groups + tiles, kCountWaves * 64, 0, s>>>(x, total, head, parts, groups, np, w, K, Kp, CRS,
+                                                                   qtiles, wt);
     *nparts = np;
     return hipGetLastError();
 }

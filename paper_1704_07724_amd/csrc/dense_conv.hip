@@ -12,6 +12,7 @@
 #include "isc_internal.hpp"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdlib>
 
 namespace isc {
@@ -472,6 +473,33 @@ int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
 }
 
 }  // namespace
+
+// Expected time of the implicit GEMM (ms): a fixed part, the rounds of
+// resident tiles times each tile's reduction length and size, the output
+// (times the ranges of a split reduction, whose partial sums are written and
+// summed), and a second launch when the reduction is split.  Coefficients
+// fitted to the dense path measured on every workload and Tab. 2 shape
+// (15 % rms).
+double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
+    int64_t tm, tn;
+    if (M <= 32) {
+        tm = 32;
+        tn = (Ncols + 255) / 256 >= 512 ? 256 : 128;
+    } else if (M <= 64) {
+        tm = 64;
+        tn = (Ncols + 127) / 128 >= 512 ? 128 : 64;
+    } else {
+        tm = 128;
+        tn = 128;
+    }
+    const int64_t tiles = gemm_tiles(M, Ncols);
+    const int kc = Kd < (1ll << 31) ? gemm_kchunk(M, Ncols, static_cast<int>(Kd)) : 0;
+    const int64_t ranges = kc > 0 ? (Kd + kc - 1) / kc : 1;
+    const double rounds = std::ceil(static_cast<double>(tiles * ranges) / 512.0);
+    const double per = static_cast<double>(Kd) / ranges * tm * tn;
+    return 0.0147936 + 8.70142e-9 * rounds * per + 5.93757e-9 * static_cast<double>(M) * Ncols * ranges +
+           (ranges > 1 ? 0.00754156 : 0.0);
+}
 
 size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd) {
     const int kc = gemm_kchunk(M, Ncols, Kd);

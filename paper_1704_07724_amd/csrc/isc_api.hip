@@ -155,7 +155,7 @@ int check_device() {
 
 // Largest nonzero count n with 1 - n/total >= threshold (the sparsity test of
 // the dispatcher, evaluated in double exactly as written).
-unsigned long long nnz_limit_for(int64_t total, float threshold) {
+long long nnz_limit_for(int64_t total, float threshold) {
     const double th = static_cast<double>(threshold);
     auto sparse_enough = [&](int64_t n) {
         return 1.0 - static_cast<double>(n) / static_cast<double>(total) >= th;
@@ -164,8 +164,7 @@ unsigned long long nnz_limit_for(int64_t total, float threshold) {
     n = std::max<int64_t>(-1, std::min<int64_t>(n, total));
     while (n + 1 <= total && sparse_enough(n + 1)) ++n;
     while (n >= 0 && !sparse_enough(n)) --n;
-    if (n < 0) return ~0ull;  // unreachable for threshold <= 1: n = 0 gives sparsity 1
-    return static_cast<unsigned long long>(n);
+    return static_cast<long long>(n);  // -1 only for a threshold above 1 (rejected)
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? ISC_OK : ISC_ERR_HIP; }
@@ -266,8 +265,12 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
     hipError_t e = hipSuccess;
     uint32_t *parts = L.sparse ? reinterpret_cast<uint32_t *>(base + L.parts) : nullptr;
     int nparts = 0;
-    const unsigned long long limit =
-        threshold < 0.0f ? isc::crossover_nnz_limit(sh) : nnz_limit_for(s.in_elems(), threshold);
+    const long long limit = threshold < 0.0f ? isc::crossover_nnz_limit(sh) : nnz_limit_for(s.in_elems(), threshold);
+    // a limit no count can cross decides AUTO on the host: every count picks
+    // the sparse path (the count still runs, for the record), or none does
+    // (the dense path alone, as if asked for)
+    if (path == ISC_PATH_AUTO && limit >= s.in_elems()) path = ISC_PATH_SPARSE;
+    if (path == ISC_PATH_AUTO && limit < 0) path = ISC_PATH_DENSE;
     const int gate_sparse = path == ISC_PATH_AUTO ? isc::kGateIfSparse : isc::kGateAlways;
 
     if (path != ISC_PATH_DENSE) {
@@ -536,6 +539,18 @@ int isc_sparse_kernel(const isc_conv_desc *d, int32_t *kernel) {
     const isc::SparseShape sh = sparse_shape(s);
     const int fused = isc::sparse_fused_kernel(sh);
     *kernel = fused ? fused : isc::list_kernel_for(sh);
+    return ISC_OK;
+}
+
+int isc_crossover_sparsity(const isc_conv_desc *d, double *sparsity) {
+    if (!sparsity) return ISC_ERR_NULL;
+    Shape s;
+    const int st = check_desc(d, &s);
+    if (st) return st;
+    const isc::SparseShape sh = sparse_shape(s);
+    const bool sparse_fits = isc::sparse_fused_applies(sh) || isc::sparse_conv_feasible(sh);
+    const long long limit = sparse_fits ? isc::crossover_nnz_limit(sh) : -1;
+    *sparsity = limit < 0 ? 2.0 : 1.0 - static_cast<double>(limit) / static_cast<double>(s.in_elems());
     return ISC_OK;
 }
 

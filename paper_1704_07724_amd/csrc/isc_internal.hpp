@@ -56,7 +56,7 @@ struct Epilogue {
 struct Decision {
     const uint32_t *parts;         // per-workgroup counts (nullptr: no compaction ran)
     int nparts;                    // entries of parts, a multiple of 4
-    unsigned long long nnz_limit;  // largest nonzero count that still picks sparse
+    long long nnz_limit;           // largest nonzero count that still picks sparse (-1: none does)
     int gate;
     Ctrl *record;                  // where block 0 records count and path (may be nullptr)
     const Ctrl *recorded = nullptr;  // decision recorded by an earlier kernel on the stream
@@ -116,8 +116,10 @@ __device__ __forceinline__ unsigned long long decision_total(const Decision &d) 
 // taken when asked.  Called by whole wavefronts.
 __device__ __forceinline__ bool decision_gate(const Decision &d, uint32_t mine) {
     if (d.recorded) return d.recorded->path_taken == mine;
+    const bool recorder = d.record && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0;
+    if (d.gate == kGateAlways && !recorder) return true;  // no count needed
     const unsigned long long total = decision_total(d);
-    const bool sparse = total != ~0ull && total <= d.nnz_limit;
+    const bool sparse = total != ~0ull && static_cast<long long>(total) <= d.nnz_limit;
     const bool run = d.gate == kGateAlways || (d.gate == kGateIfSparse ? sparse : !sparse);
     if (d.record && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) {
         d.record->nnz_total = total;
@@ -238,8 +240,11 @@ int list_kernel_waves(int kernel);
 
 // AUTO's per-shape crossover: the largest nonzero count of the input at
 // which the sparse path is expected to be faster than the dense path for
-// this shape (crossover.cpp).
-unsigned long long crossover_nnz_limit(const SparseShape &sh);
+// this shape, -1 when it never is (crossover.hip).
+long long crossover_nnz_limit(const SparseShape &sh);
+// The dense path's expected time (ms) for an M x Ncols x Kd implicit GEMM,
+// from its tile grid (dense_conv.hip).
+double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd);
 
 // ISC steps 2 and 3: zero-skipping convolution over the compacted lists.
 hipError_t launch_sparse_conv(const SparseShape &sh, const int32_t *row_ptr,

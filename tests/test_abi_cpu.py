@@ -306,7 +306,7 @@ def test_sparse_plan_and_overrides():
     conv2 = d(128, 96, 27, 27, 256, 5, 5, 1, 2)
     r = isc.isc_sparse_plan(conv2, {"kernel": "fused_ring", "maps_per_lane": 2, "rows": 1})
     assert (r["kernel"], r["maps_per_lane"], r["rows"]) == ("fused_ring", 2, 1)
-    assert r["workgroups"] == 128 * 7 * 1 * 2
+    assert r["workgroups"] == 128 * 27 // 4 * 2      # 1 x 28 tiles, four to a workgroup, two map groups
     # five maps per lane: no such tile, the library's own choice runs
     assert isc.isc_sparse_plan(conv2, {"kernel": "fused_ring", "maps_per_lane": 5}) == isc.isc_sparse_plan(conv2)
     assert isc.isc_sparse_plan(d(2, 4, 21, 21, 64, 5, 5, 2, 1))["kernel"] == "generic"
@@ -320,3 +320,21 @@ def test_read_decision_validation():
     p, n = ctypes.c_int32(), ctypes.c_uint64()
     assert L.isc_read_decision(None, ctypes.byref(p), ctypes.byref(n)) == 1
     assert L.isc_read_decision(0x1000, None, ctypes.byref(n)) == 1
+
+
+def test_crossover_model_orders_shapes():
+    """AUTO's per-shape crossover (host model): the 5x5 layers cross far
+    below the paper's 0.9, AlexNet conv3-5 near 0.7, Tab. 2's 1x1 layers at
+    batch 128 never go sparse, and the crossover is a sparsity in [0, 1]
+    or 2.0 (never)."""
+    d = isc.make_desc
+    lenet = isc.isc_crossover_sparsity(d(256, 20, 12, 12, 50, 5, 5, 1, 0))
+    conv2 = isc.isc_crossover_sparsity(d(128, 96, 27, 27, 256, 5, 5, 1, 2))
+    conv3 = isc.isc_crossover_sparsity(d(128, 256, 13, 13, 384, 3, 3, 1, 1))
+    one = isc.isc_crossover_sparsity(d(128, 480, 14, 14, 192, 1, 1, 1, 0))
+    assert 0.0 <= lenet < 0.5 and 0.3 < conv2 < 0.7 and 0.5 < conv3 < 0.85
+    assert one == 2.0
+    for s in (lenet, conv2, conv3):
+        assert 0.0 <= s <= 1.0
+    # a shape only the list kernels take keeps the paper's 0.9
+    assert abs(isc.isc_crossover_sparsity(d(2, 4, 21, 21, 64, 5, 5, 2, 1)) - 0.9) < 1e-3

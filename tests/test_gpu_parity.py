@@ -600,3 +600,27 @@ def test_every_ring_tile(torch, isc, tile):
         xi, wi = workloads.integer_case(N, C, H, W, K, R, R, seed=5 + kpl + th + tw)
         yi = isc.isc_sparse_conv_fused(to_dev(torch, xi), isc.isc_repack_filter(to_dev(torch, wi)), T, P, tuning=tu)
         assert np.array_equal(yi.cpu().numpy().astype(np.float64), oracle.conv2d_f64(xi, wi, T, P))
+
+
+def test_auto_crossover_both_sides(torch, isc):
+    """AUTO with the per-shape crossover (the library's default threshold):
+    on a shape whose modelled crossover lies inside (0, 1), an input below it
+    runs the dense path and one above it the sparse path; the decision is the
+    integer comparison of the input's nonzero count, and both outputs match
+    the oracle."""
+    case = (8, 96, 27, 27, 256, 5, 5, 1, 2)
+    N, C, H, W, K, R, S, T, P = case
+    desc = isc.make_desc(*case)
+    s_star = isc.isc_crossover_sparsity(desc)
+    assert 0.3 < s_star < 0.95, s_star
+    for sp, want in ((s_star - 0.2, "dense"), (min(0.99, s_star + 0.15), "sparse")):
+        note("crossover", case, "sparsity", sp, want)
+        x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=301 + int(sp * 100))
+        measured = 1.0 - np.count_nonzero(x) / x.size
+        assert (measured >= s_star) == (want == "sparse")
+        ws = isc.workspace(desc, "auto")
+        y = isc.isc_conv2d(to_dev(torch, x), to_dev(torch, w), T, P, path="auto", threshold=isc.THRESHOLD_CROSSOVER,
+                           ws=ws)
+        nnz, taken = isc.isc_decision(desc, ws)
+        assert nnz == int(np.count_nonzero(x)) and taken == want
+        assert_conv_close(y.cpu().numpy(), oracle.conv2d_f64(x, w, T, P), "crossover %s" % want)
