@@ -202,16 +202,43 @@ __device__ __forceinline__ uint32_t nz4(const float4 &v) {
            ((__float_as_uint(v.z) & 0x7fffffffu) != 0u) + ((__float_as_uint(v.w) & 0x7fffffffu) != 0u);
 }
 
+// Cache warm-up: workgroup `blk` reads its 64 KiB of p[0 .. n4) with four
+// 16-byte loads in flight per thread.  The loaded words feed a value that
+// is stored (to a word nobody reads) only when it equals `key`, so the loads
+// are not dead code; what matters is that the lines end up cached.
+constexpr int kWarmThreads = 1024, kWarmLoads = 4;
+constexpr int64_t kWarmBytesPerGroup = static_cast<int64_t>(kWarmThreads) * kWarmLoads * 16;
+
+__device__ __forceinline__ void warm_lines(const uint4 *__restrict__ p, int64_t n4, int64_t blk, uint32_t key,
+                                           uint32_t *sink) {
+    const int64_t base = blk * kWarmThreads * kWarmLoads + threadIdx.x;
+    uint4 v[kWarmLoads];
+#pragma unroll
+    for (int j = 0; j < kWarmLoads; ++j) {
+        const int64_t i = base + static_cast<int64_t>(j) * kWarmThreads;
+        v[j] = p[i < n4 ? i : n4 - 1];
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < kWarmLoads; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
+    if (acc == key) *sink = acc;
+}
+
+constexpr uint32_t kWarmKey = 0x5bd1e995u;
+
 __global__ __launch_bounds__(kCountWaves * 64)
 void count_parts_kernel(const float *__restrict__ x, int64_t total, int head, uint32_t *__restrict__ parts,
                         int groups, int nparts, const float *__restrict__ w, int K, int Kp, int CRS, int qtiles,
-                        float *__restrict__ wt) {
+                        float *__restrict__ wt, const uint4 *__restrict__ warm, int64_t warm_n4, uint32_t *sink) {
     __shared__ uint32_t wave_count[kCountWaves];
     __shared__ float tile[64][65];
     const int b = blockIdx.x;
-    if (b >= groups) {  // filter repack, one 64 x 64 tile per workgroup
+    if (b >= groups) {  // filter repack, one 64 x 64 tile per workgroup; or cache warm-up
         const int t = b - groups;
-        repack_tile(w, K, Kp, CRS, wt, t % qtiles, t / qtiles, tile);
+        if (w)
+            repack_tile(w, K, Kp, CRS, wt, t % qtiles, t / qtiles, tile);
+        else
+            warm_lines(warm, warm_n4, t, kWarmKey, sink);
         return;
     }
     constexpr int kThreads = kCountWaves * 64;
@@ -255,6 +282,56 @@ void count_parts_kernel(const float *__restrict__ x, int64_t total, int head, ui
     }
 }
 
+
+// Workgroup 0 turns a census into the decision's parts: the census's counts
+// summed with 16-byte loads (a census of a few thousand workgroups is read
+// once, here, instead of by every wavefront of the next kernel); the other
+// workgroups warm the cache with `warm`.
+constexpr int kCensusThreads = kWarmThreads;
+
+__global__ __launch_bounds__(kCensusThreads)
+void census_parts_kernel(const CensusHeader *__restrict__ census, uint32_t cap, unsigned long long elems,
+                         uint32_t *__restrict__ parts, const uint4 *__restrict__ warm, int64_t warm_n4,
+                         uint32_t *sink) {
+    if (blockIdx.x > 0) {
+        warm_lines(warm, warm_n4, blockIdx.x - 1, kWarmKey, sink);
+        return;
+    }
+    __shared__ unsigned long long part[kCensusThreads / 64];
+    const CensusHeader h = *census;
+    const bool ok = h.elems == elems && h.nslots <= cap && h.nslots % 4 == 0;
+    unsigned long long s = 0;
+    if (ok) {
+        const uint4 *c4 = reinterpret_cast<const uint4 *>(census + 1);
+        const int n4 = static_cast<int>(h.nslots / 4);
+        for (int i0 = threadIdx.x; i0 < n4; i0 += 4 * kCensusThreads) {
+            uint4 v[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) v[j] = c4[min(i0 + j * kCensusThreads, n4 - 1)];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (i0 + j * kCensusThreads < n4)
+                    s += static_cast<unsigned long long>(v[j].x) + v[j].y + v[j].z + v[j].w;
+        }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long t = 0;
+#pragma unroll
+        for (int i = 0; i < kCensusThreads / 64; ++i) t += part[i];
+        // an unusable census, or (impossible for a real one) a total of 2^32
+        // or more: all ones, which the decision reads as an unknown count
+        const bool known = ok && t < (1ull << 32);
+        parts[0] = known ? static_cast<uint32_t>(t) : 0xffffffffu;
+        parts[1] = known ? 0u : 0xffffffffu;
+        parts[2] = 0u;
+        parts[3] = 0u;
+    }
+}
+
 // The output epilogue as a pass of its own, for the kernels over compacted
 // lists (which store y without one): y rectified in place and its nonzeros
 // counted into the census; workgroup b takes one contiguous chunk.
@@ -288,6 +365,17 @@ hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row
     return hipGetLastError();
 }
 
+hipError_t launch_census_parts(const CensusHeader *census, uint32_t cap, unsigned long long elems, uint32_t *parts,
+                               const void *warm, size_t warm_bytes, Ctrl *ctrl, hipStream_t s) {
+    // whole 16-byte words of the warmed range (a repacked filter is a
+    // multiple of 64 floats)
+    const int64_t n4 = warm ? static_cast<int64_t>(warm_bytes / 16) : 0;
+    const int64_t groups = (n4 * 16 + kWarmBytesPerGroup - 1) / kWarmBytesPerGroup;
+    census_parts_kernel<<<static_cast<unsigned>(1 + groups), kCensusThreads, 0, s>>>(
+        census, cap, elems, parts, static_cast<const uint4 *>(warm), n4, &ctrl->sink);
+    return hipGetLastError();
+}
+
 size_t repacked_filter_floats(int K, int C, int R, int S) {
     const size_t Kp = (static_cast<size_t>(K) + 63) / 64 * 64;
     return static_cast<size_t>(C) * R * S * Kp;
@@ -306,19 +394,23 @@ hipError_t launch_repack_filter(const float *w, int K, int C, int R, int S, floa
 constexpr int kCountGroups = 256;
 
 hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s,
-                              const float *w, int K, int C, int R, int S, float *wt) {
+                              const float *w, int K, int C, int R, int S, float *wt, const void *warm,
+                              size_t warm_bytes, Ctrl *ctrl) {
     const int64_t per = static_cast<int64_t>(kCountWaves) * 64 * kCountUnroll * 4;  // elements per workgroup, at least
     const int groups = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(kCountGroups, (total + per - 1) / per)));
     const int np = (groups + 3) / 4 * 4;
     const int CRS = C * R * S;
     const int Kp = (K + 63) / 64 * 64;
     const int qtiles = (CRS + 63) / 64;
-    const int tiles = w ? qtiles * (Kp / 64) : 0;
+    const int64_t warm_n4 = !w && warm && ctrl ? static_cast<int64_t>(warm_bytes / 16) : 0;
+    const int tiles = w ? qtiles * (Kp / 64)
+                        : static_cast<int>((warm_n4 * 16 + kWarmBytesPerGroup - 1) / kWarmBytesPerGroup);
     // elements before the first 16-byte boundary (x is 4-byte aligned)
     const int head = static_cast<int>(std::min<int64_t>(
         total, ((16 - reinterpret_cast<uintptr_t>(x) % 16) % 16) / 4));
-    count_parts_kernel<<<groups + tiles, kCountWaves * 64, 0, s>>>(x, total, head, parts, groups, np, w, K, Kp, CRS,
-                                                                   qtiles, wt);
+    count_parts_kernel<<<groups + tiles, kCountWaves * 64, 0, s>>>(
+        x, total, head, parts, groups, np, w, K, Kp, CRS, qtiles, wt, static_cast<const uint4 *>(warm), warm_n4,
+        ctrl ? &ctrl->sink : nullptr);
     *nparts = np;
     return hipGetLastError();
 }

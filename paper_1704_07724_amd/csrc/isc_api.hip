@@ -281,19 +281,29 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
             const float *wt = ch && ch->wt ? ch->wt : wt_ws;
             isc::Decision dec{parts, 0, limit, gate_sparse, ctrl};
             if (ch && ch->x_census) {
-                // the count comes from the census of x: no pass over x
+                // the count comes from the census of x, summed once into
+                // the parts: no pass over x
                 if (!ch->wt && (e = isc::launch_repack_filter(w, sh.K, sh.C, sh.R, sh.S, wt_ws, hs)) != hipSuccess)
                     return hip_status(e);
-                dec.parts = nullptr;
-                dec.census = ch->x_census;
-                dec.census_cap = ch->x_cap;
-                dec.census_elems = static_cast<unsigned long long>(s.in_elems());
+                // and a filter repacked by the caller, cold in cache, warmed
+                // in the same launch (the fused kernels read it a channel
+                // at a time, one dependent step after another)
+                const size_t wt_bytes =
+                    ch->wt ? isc::repacked_filter_floats(sh.K, sh.C, sh.R, sh.S) * sizeof(float) : 0;
+                if ((e = isc::launch_census_parts(ch->x_census, ch->x_cap, static_cast<unsigned long long>(s.in_elems()),
+                                                  parts, ch->wt, wt_bytes, ctrl, hs)) != hipSuccess)
+                    return hip_status(e);
+                dec.nparts = 4;
             } else {
                 // the count for the decision and the filter repack to
-                // K-contiguous in one launch, then steps 1-3 in one launch
+                // K-contiguous in one launch (or, with a filter the caller
+                // repacked, its cache warm-up), then steps 1-3 in one launch
                 const bool repack = !(ch && ch->wt);
+                const size_t wt_bytes =
+                    repack ? 0 : isc::repacked_filter_floats(sh.K, sh.C, sh.R, sh.S) * sizeof(float);
                 if ((e = isc::launch_count_parts(x, s.in_elems(), parts, &nparts, hs, repack ? w : nullptr, sh.K,
-                                                 sh.C, sh.R, sh.S, repack ? wt_ws : nullptr)) != hipSuccess)
+                                                 sh.C, sh.R, sh.S, repack ? wt_ws : nullptr, repack ? nullptr : ch->wt,
+                                                 wt_bytes, ctrl)) != hipSuccess)
                     return hip_status(e);
                 dec.nparts = nparts;
             }

@@ -19,7 +19,7 @@ struct alignas(8) NzEntry {
 struct alignas(16) Ctrl {
     unsigned long long nnz_total;  // nonzero inputs counted by the compaction
     uint32_t path_taken;           // 1 = sparse, 2 = dense (isc_path values)
-    uint32_t reserved;
+    uint32_t sink;                 // written (rarely) by cache warm-ups, never read
 };
 
 // Whether a kernel of one path runs unconditionally or only when the
@@ -60,12 +60,6 @@ struct Decision {
     int gate;
     Ctrl *record;                  // where block 0 records count and path (may be nullptr)
     const Ctrl *recorded = nullptr;  // decision recorded by an earlier kernel on the stream
-    // census of the input (used when parts is nullptr): counts must cover
-    // census_elems entries and fit in census_cap, else the count is unknown
-    // (all ones: the dense path)
-    const CensusHeader *census = nullptr;
-    uint32_t census_cap = 0;
-    unsigned long long census_elems = 0;
 };
 
 // Sum of n counts (n a multiple of 4), by the calling wavefront (every lane
@@ -100,15 +94,13 @@ __device__ __forceinline__ unsigned long long sum_counts(const uint32_t *counts,
 }
 
 // The input's nonzero count for the decision, by the calling wavefront;
-// all ones when neither a compaction nor a usable census gives it.
+// all ones when no count ran or the parts say "unknown" (a sum of 2^32 or
+// more: the census reduction's mark of an unusable census, as real counts
+// are below 2^31).
 __device__ __forceinline__ unsigned long long decision_total(const Decision &d) {
-    if (d.parts) return sum_counts(d.parts, d.nparts);
-    if (d.census) {
-        const CensusHeader h = *d.census;
-        if (h.elems == d.census_elems && h.nslots <= d.census_cap && h.nslots % 4 == 0)
-            return sum_counts(reinterpret_cast<const uint32_t *>(d.census + 1), static_cast<int>(h.nslots));
-    }
-    return ~0ull;
+    if (!d.parts) return ~0ull;
+    const unsigned long long s = sum_counts(d.parts, d.nparts);
+    return s >= (1ull << 32) ? ~0ull : s;
 }
 
 // Gate of a kernel on path `mine` (1 sparse, 2 dense): whether it runs.
@@ -138,17 +130,17 @@ __device__ __forceinline__ uint32_t nonzero_bit(float v) { return (__float_as_ui
 // The workgroup's census count: the sum of every thread's `cnt` into the
 // workgroup's slot; block 0 also writes the header and clears the tail
 // slots up to a multiple of 4.  Called by every thread of the workgroup
-// (uniformly: it synchronises); `sums` is LDS with one word per wavefront
-// that nothing else uses until the call returns.
-__device__ __forceinline__ void census_commit(const Epilogue &e, uint32_t cnt, uint32_t *sums) {
+// (uniformly: it synchronises); `sums` is LDS with one word per wavefront,
+// `stride` words apart, that nothing else touches until the call returns.
+__device__ __forceinline__ void census_commit(const Epilogue &e, uint32_t cnt, uint32_t *sums, int stride = 1) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) cnt += __shfl_xor(cnt, off);
     const int wave = threadIdx.x >> 6;
-    if ((threadIdx.x & 63) == 0) sums[wave] = cnt;
+    if ((threadIdx.x & 63) == 0) sums[wave * stride] = cnt;
     __syncthreads();
     if (threadIdx.x == 0) {
         uint32_t t = 0;
-        for (int i = 0; i < static_cast<int>(blockDim.x >> 6); ++i) t += sums[i];
+        for (int i = 0; i < static_cast<int>(blockDim.x >> 6); ++i) t += sums[i * stride];
         const uint32_t nblocks = gridDim.x * gridDim.y * gridDim.z;
         const uint32_t b = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
         uint32_t *slots = reinterpret_cast<uint32_t *>(e.census + 1);
@@ -174,13 +166,25 @@ inline uint32_t census_slots_for(int64_t blocks) { return static_cast<uint32_t>(
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s);
 
+// A census's total into parts[0 .. 4) (the decision's input for a layer
+// whose input carries a census): one workgroup sums the census's counts; a
+// census that does not cover exactly `elems` entries, or claims more counts
+// than `cap`, leaves all ones (a sum the decision reads as "unknown").
+// The same launch also reads `warm_bytes` bytes at `warm` (a filter the
+// next kernel streams in small dependent steps) with its other workgroups,
+// so that the kernel finds them in the last-level cache instead of HBM.
+hipError_t launch_census_parts(const CensusHeader *census, uint32_t cap, unsigned long long elems, uint32_t *parts,
+                               const void *warm, size_t warm_bytes, Ctrl *ctrl, hipStream_t s);
+
 // Nonzero count of x[0 .. total) as per-workgroup parts (the decision's input
 // when the sparse path compacts on the fly); with w, extra workgroups of the
 // same launch repack the K x C x R x S filter into wt (layout of
-// launch_repack_filter).
+// launch_repack_filter); without w, extra workgroups warm the cache with
+// warm_bytes bytes at `warm` (as launch_census_parts does).
 hipError_t launch_count_parts(const float *x, int64_t total, uint32_t *parts, int *nparts, hipStream_t s,
                               const float *w = nullptr, int K = 0, int C = 0, int R = 0, int S = 0,
-                              float *wt = nullptr);
+                              float *wt = nullptr, const void *warm = nullptr, size_t warm_bytes = 0,
+                              Ctrl *ctrl = nullptr);
 
 // The sparse path's first kernel: ISC step 1 with per-workgroup counts in
 // parts (kMaxParts entries; *nparts gets the number in use), and the filter

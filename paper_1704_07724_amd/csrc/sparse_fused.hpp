@@ -37,6 +37,7 @@ using tile::kLanes;
 constexpr int kWaves = 8;
 constexpr size_t kLdsMax = 160 * 1024;
 constexpr int kRPad = 65;        // LDS pitch of one tile position's output maps (reduction)
+static_assert(kRPad > kLanes, "the pad column holds the census sums");
 constexpr int kMaxTile = 64;     // accumulators per lane
 constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
 constexpr int kWPitch = 64;      // maps per filter column in the repacked layout (K <= 64)
@@ -233,8 +234,10 @@ void sparse_conv_fused_kernel(FusedArgs a) {
         dst[static_cast<size_t>(k) * plane_out] = sum;
     }
     if (a.epi.census) {
-        __syncthreads();  // every thread is done reading the phase tiles
-        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(lds));
+        // the wavefront sums in the pad word of the first phase-tile rows
+        // (column 64, which no tile store or read touches): no wait for the
+        // reads above
+        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(red + kLanes), kRPad);
     }
 }
 
@@ -379,10 +382,7 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
         cnt += nonzero_bit(sum);
         dst[static_cast<size_t>(k) * plane_out] = sum;
     }
-    if (a.epi.census) {
-        __syncthreads();
-        census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(lds));
-    }
+    if (a.epi.census) census_commit(a.epi, cnt, reinterpret_cast<uint32_t *>(red + kLanes), kRPad);
 }
 
 template <int RS_, int TH, int TW, bool WIDE>
