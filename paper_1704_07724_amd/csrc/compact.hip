@@ -16,7 +16,7 @@
 // transpose a 64 x 64 tile), and each compaction workgroup stores its own
 // nonzero count; the kernels after it add those counts for the sparse/dense
 // decision.  The stand-alone entry point instead sums the per-plane counts
-// with a one-workgroup kernel.
+// in a second launch spread over the CUs, one atomic add per workgroup.
 #include "isc_internal.hpp"
 
 #include <algorithm>
@@ -27,6 +27,19 @@ namespace {
 constexpr int kWaves = 4;    // wavefronts per workgroup
 constexpr int kUnroll = 16;  // 64-element chunks loaded before the ballots (a 32 x 32 plane at once)
 
+// Loads of data read once (the input's zero test): the non-temporal cache
+// policy.  Measured on a cold 36 MB input behind 512 MiB of dirty cache
+// lines, it halves the read time against the default policy, which
+// allocates the lines in L2 at the cost of evicting dirty ones.
+typedef float float4_nt __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float load_once(const float *p) { return __builtin_nontemporal_load(p); }
+
+__device__ __forceinline__ float4 load_once(const float4 *p) {
+    const float4_nt v = __builtin_nontemporal_load(reinterpret_cast<const float4_nt *>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ uint32_t lanes_below(unsigned long long mask) {
     return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
@@ -34,91 +47,158 @@ __device__ __forceinline__ uint32_t lanes_below(unsigned long long mask) {
 
 // Compact planes p = first, first + stride, ... (< planes) with the calling
 // wavefront; returns the number of nonzeros it listed (wave-uniform).
+//
+// Planes of at most kBatch elements (every workload layer's) take one batch
+// of kUnroll chunks each.  A lane's positions in the chunks are then the
+// same in every plane: the wavefront computes them once (packed row and
+// column, and which chunks start a row at the lane), so that listing a chunk
+// is the zero test, the ballot, the lane's slot (mbcnt), the entry store
+// and, at row starts, the row offset store.  The next plane's loads are
+// issued before the current plane is listed.  Larger planes take several
+// batches, with the positions stepped along.
+constexpr int kBatch = 64 * kUnroll;
+
 __device__ __forceinline__ uint32_t compact_planes(const float *__restrict__ x, int planes, int H, int W,
                                                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz,
                                                    int first, int stride) {
     const int lane = threadIdx.x & 63;
     const int HW = H * W;
-    // (row, column) of this lane's element in the first chunk, and the step
-    // that moves it 64 elements further in row-major order
-    const int y_first = lane / W;
-    const int x_first = lane - y_first * W;
-    const int dy = 64 / W;
-    const int dx = 64 - dy * W;
     uint32_t listed = 0;
+    if (first >= planes) return 0;
 
-    for (int p = first; p < planes; p += stride) {
+    auto load_batch = [&](int p, int e0, float (&v)[kUnroll]) {
         const float *xp = x + static_cast<size_t>(p) * HW;
-        NzEntry *np = nz + static_cast<size_t>(p) * HW;
-        int32_t *rp = row_ptr + static_cast<size_t>(p) * (H + 1);
-        uint32_t base = 0;  // nonzeros before the current chunk (wave-uniform)
-        int y = y_first, xc = x_first;
-        for (int e0 = 0; e0 < HW; e0 += 64 * kUnroll) {
-            float v[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int e = e0 + u * 64 + lane;
+            v[u] = e < HW ? load_once(xp + e) : 0.0f;  // past the plane: zero, never listed
+        }
+    };
+
+    if (HW <= kBatch) {
+        uint32_t yx[kUnroll];
+        uint32_t row_start = 0;  // bit u: the lane holds a row's first element in chunk u
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int e = u * 64 + lane;
+            const int yy = e / W, xx = e - (e / W) * W;
+            yx[u] = (static_cast<uint32_t>(yy) << 16) | static_cast<uint32_t>(xx);
+            row_start |= static_cast<uint32_t>(e < HW && xx == 0) << u;
+        }
+        float cur[kUnroll];
+        load_batch(first, 0, cur);
+        for (int p = first; p < planes; p += stride) {
+            float nxt[kUnroll];
+            if (p + stride < planes) load_batch(p + stride, 0, nxt);
+            NzEntry *np = nz + static_cast<size_t>(p) * HW;
+            int32_t *rp = row_ptr + static_cast<size_t>(p) * (H + 1);
+            uint32_t base = 0;  // nonzeros of the plane before the current chunk (wave-uniform)
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                const int e = e0 + u * 64 + lane;
-                v[u] = e < HW ? xp[e] : 0.0f;
-            }
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const int e = e0 + u * 64 + lane;
-                const bool inside = e < HW;
-                const uint32_t bits = __float_as_uint(v[u]);
-                const bool nonzero = inside && (bits & 0x7fffffffu) != 0u;
+                const bool nonzero = (__float_as_uint(cur[u]) & 0x7fffffffu) != 0u;
                 const unsigned long long mask = __ballot(nonzero);
                 const uint32_t slot = base + lanes_below(mask);
                 if (nonzero) {
                     NzEntry ent;
-                    ent.v = v[u];
-                    ent.yx = (static_cast<uint32_t>(y) << 16) | static_cast<uint32_t>(xc);
+                    ent.v = cur[u];
+                    ent.yx = yx[u];
                     np[slot] = ent;
                 }
-                if (inside && xc == 0) rp[y] = static_cast<int32_t>(slot);
+                if (row_start & (1u << u)) rp[yx[u] >> 16] = static_cast<int32_t>(slot);
                 base += static_cast<uint32_t>(__popcll(mask));
-                xc += dx;
-                y += dy;
-                if (xc >= W) {
-                    xc -= W;
-                    ++y;
-                }
+            }
+            if (lane == 0) rp[H] = static_cast<int32_t>(base);
+            listed += base;
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) cur[u] = nxt[u];
+        }
+        return listed;
+    }
+
+    // (row, column) of this lane's element in a plane's first chunk, and the
+    // step that moves it 64 elements further in row-major order
+    const int y_first = lane / W;
+    const int x_first = lane - y_first * W;
+    const int dy = 64 / W;
+    const int dx = 64 - dy * W;
+    int p = first, e0 = 0;
+    float cur[kUnroll];
+    load_batch(p, e0, cur);
+    uint32_t base = 0;
+    int y = y_first, xc = x_first;
+    for (;;) {
+        // the batch after this one: the next kBatch elements of this plane,
+        // else the first of the wavefront's next plane
+        int pn = p, en = e0 + kBatch;
+        if (en >= HW) {
+            en = 0;
+            pn = p + stride;
+        }
+        float nxt[kUnroll];
+        if (pn < planes) load_batch(pn, en, nxt);
+
+        NzEntry *np = nz + static_cast<size_t>(p) * HW;
+        int32_t *rp = row_ptr + static_cast<size_t>(p) * (H + 1);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int e = e0 + u * 64 + lane;
+            const bool inside = e < HW;
+            const bool nonzero = (__float_as_uint(cur[u]) & 0x7fffffffu) != 0u;
+            const unsigned long long mask = __ballot(nonzero);
+            const uint32_t slot = base + lanes_below(mask);
+            if (nonzero) {
+                NzEntry ent;
+                ent.v = cur[u];
+                ent.yx = (static_cast<uint32_t>(y) << 16) | static_cast<uint32_t>(xc);
+                np[slot] = ent;
+            }
+            if (inside && xc == 0) rp[y] = static_cast<int32_t>(slot);
+            base += static_cast<uint32_t>(__popcll(mask));
+            xc += dx;
+            y += dy;
+            if (xc >= W) {
+                xc -= W;
+                ++y;
             }
         }
-        if (lane == 0) rp[H] = static_cast<int32_t>(base);
-        listed += base;
+        if (pn != p) {  // the plane is done: its count, and a fresh walk
+            if (lane == 0) rp[H] = static_cast<int32_t>(base);
+            listed += base;
+            base = 0;
+            y = y_first;
+            xc = x_first;
+        }
+        if (pn >= planes) break;
+        p = pn;
+        e0 = en;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) cur[u] = nxt[u];
     }
     return listed;
 }
 
+// The stand-alone compaction; workgroup 0 also clears the total, which the
+// count kernel after it accumulates.
 __global__ __launch_bounds__(kWaves * 64)
 void compact_kernel(const float *__restrict__ x, int planes, int H, int W,
-                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz) {
+                    int32_t *__restrict__ row_ptr, NzEntry *__restrict__ nz, unsigned long long *__restrict__ total) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) *total = 0ull;
     const int wave = threadIdx.x >> 6;
     compact_planes(x, planes, H, W, row_ptr, nz, blockIdx.x * kWaves + wave, gridDim.x * kWaves);
 }
 
-// Total of the per-plane counts (row_ptr[p][H]) by one workgroup, written
-// to *total with a plain store: no counter to clear, no same-address atomics.
-constexpr int kCountThreads = 1024;
+// Total of the per-plane counts (row_ptr[p][H], H + 1 words apart): one
+// plane per thread over as many workgroups as it takes (every count in one
+// round trip, spread over the CUs), each workgroup adding its sum to *total
+// with one atomic (a few dozen atomics on one address in all).
+constexpr int kCountThreads = 256;
 
 __global__ __launch_bounds__(kCountThreads)
 void count_kernel(const int32_t *__restrict__ row_ptr, int planes, int H,
                   unsigned long long *__restrict__ total) {
     __shared__ unsigned long long part[kCountThreads / 64];
-    unsigned long long s = 0;
-    // eight loads in flight per thread (the counts are H + 1 words apart:
-    // one load per L2 round trip would leave the tail latency-bound)
-    for (int p0 = threadIdx.x; p0 < planes; p0 += 8 * kCountThreads) {
-        uint32_t v[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int p = min(p0 + j * kCountThreads, planes - 1);
-            v[j] = static_cast<uint32_t>(row_ptr[static_cast<size_t>(p) * (H + 1) + H]);
-        }
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (p0 + j * kCountThreads < planes) s += v[j];
-    }
+    const int p = blockIdx.x * kCountThreads + static_cast<int>(threadIdx.x);
+    unsigned long long s = p < planes ? static_cast<uint32_t>(row_ptr[static_cast<size_t>(p) * (H + 1) + H]) : 0u;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
     if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
@@ -127,7 +207,7 @@ void count_kernel(const int32_t *__restrict__ row_ptr, int planes, int H,
         unsigned long long t = 0;
 #pragma unroll
         for (int i = 0; i < kCountThreads / 64; ++i) t += part[i];
-        *total = t;
+        atomicAdd(total, t);
     }
 }
 
@@ -254,7 +334,7 @@ void count_parts_kernel(const float *__restrict__ x, int64_t total, int head, ui
 #pragma unroll
         for (int u = 0; u < kCountUnroll; ++u) {
             const int64_t g = g0 + static_cast<int64_t>(u) * kThreads;
-            v[u] = x4[g < end ? g : beg];  // past the end: an element already counted, not added
+            v[u] = load_once(x4 + (g < end ? g : beg));  // past the end: an element already counted, not added
         }
 #pragma unroll
         for (int u = 0; u < kCountUnroll; ++u)
@@ -352,16 +432,22 @@ void rectify_kernel(float *__restrict__ y, int64_t n, Epilogue epi, Decision dec
 }
 
 int compact_groups(int planes) {
-    // one wavefront per plane, enough workgroups to cover 256 CUs many times
-    return std::max(1, std::min((planes + kWaves - 1) / kWaves, 8192));
+    // one plane per wavefront while every wavefront can be resident at once
+    // (24 per CU on 256 CUs), else as many planes per wavefront as it takes
+    // (the loads of a wavefront's next plane fly while it lists the current
+    // one)
+    constexpr int kResidentWaves = 256 * 24;
+    const int per_wave = std::max(1, (planes + kResidentWaves - 1) / kResidentWaves);
+    const int waves = (planes + per_wave - 1) / per_wave;
+    return std::max(1, (waves + kWaves - 1) / kWaves);
 }
 
 }  // namespace
 
 hipError_t launch_compact(const float *x, int planes, int H, int W, int32_t *row_ptr,
                           NzEntry *nz, unsigned long long *counter, hipStream_t s) {
-    compact_kernel<<<compact_groups(planes), kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz);
-    count_kernel<<<1, kCountThreads, 0, s>>>(row_ptr, planes, H, counter);
+    compact_kernel<<<compact_groups(planes), kWaves * 64, 0, s>>>(x, planes, H, W, row_ptr, nz, counter);
+    count_kernel<<<(planes + kCountThreads - 1) / kCountThreads, kCountThreads, 0, s>>>(row_ptr, planes, H, counter);
     return hipGetLastError();
 }
 

@@ -75,6 +75,18 @@ def test_compact_bitexact(torch, isc, shape, sparsity):
     _check_compact(torch, isc, x)
 
 
+@pytest.mark.parametrize("shape", [(2, 3500, 33, 33), (1, 13000, 5, 5)])
+def test_compact_several_planes_per_wavefront(torch, isc, shape):
+    """More planes than wavefronts resident at once: each wavefront lists
+    several planes, loading the next while it lists the current one (planes
+    of two batches each in the first shape)."""
+    note("compact planes per wavefront", shape)
+    rng = np.random.default_rng(sum(shape))
+    x = np.abs(rng.standard_normal(shape)).astype(np.float32) + np.float32(0.5)
+    x[rng.random(shape) < 0.7] = 0.0
+    _check_compact(torch, isc, x)
+
+
 def test_compact_special_values(torch, isc):
     rng = np.random.default_rng(5)
     x = np.abs(rng.standard_normal((2, 3, 9, 11))).astype(np.float32)
