@@ -14,6 +14,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdlib>
+#include <type_traits>
 
 namespace isc {
 namespace {
@@ -337,6 +338,219 @@ void gemm_f32_kernel(GemmArgs g) {
     }
 }
 
+// ------------------------------------------- pipelined implicit-im2col GEMM --
+//
+// The convolution GEMM for M > 64 output maps: 128 x 128 workgroup tiles,
+// four wavefronts of 64 x 64 (2 x 2 blocks of v_mfma_f32_32x32x2_f32), 16-deep
+// K slices streamed through a ring of NST LDS stages NST-1 slices ahead.
+// Both operands go from global memory straight into LDS (buffer loads with
+// the LDS bit: no staging registers, no LDS stores), 64 consecutive LDS
+// words per instruction.  A (the K x CRS filter) is stored as it is laid out,
+// [m][k], with rows padded to 17 words so that the 32 rows an MFMA operand
+// read touches fall in distinct banks; an instruction covers 64 slots of
+// that layout, so each of its lanes reads within one 64-byte row segment and
+// pad slots read nothing.  B (the im2col gather) is stored [k][n], each
+// instruction one k row of 64 consecutive output columns.  A gather outside the
+// input (padding, past the last column, past C*R*S) gets an offset beyond the
+// buffer's range, which the hardware reads as zero, so the gather needs no
+// select and no zero fill; A rows past M and slices past C*R*S read zero the
+// same way.  A slice is consumed after an exact vmcnt wait for the wavefront's
+// own loads of it and one barrier (everyone's loads landed, everyone done with
+// the slot refilled next).  The ring slot of a slice is chosen by a static
+// branch so that the compiler can tell the slot read from the slots being
+// filled.
+constexpr int kConvBM = 128, kConvBN = 128, kConvBK = 16;
+constexpr int kConvAPitch = kConvBK + 1;                                   // LDS words per A row
+constexpr int kConvALoads = (kConvBM * kConvAPitch + 4 * 64 - 1) / (4 * 64);  // A loads per wavefront per slice
+// Two stages (the next slice in flight while the current one is multiplied)
+// and three workgroups per CU measured faster than deeper rings at two per
+// CU: AlexNet conv2 1.31 ms with 2 stages, 1.39 with 4, 1.48 with 3 (at three
+// workgroups per CU), 1.89 with 5 (one); the register-staged kernel 1.37.
+constexpr int kConvStages = 2;
+constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every buffer this kernel reads (< 2^31 bytes)
+constexpr int kGemmBufferFormat = 0x00020000;  // raw buffer, 32-bit data
+
+template <int B, int E, typename F>
+__device__ __forceinline__ void for_static(F &&f) {
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        for_static<B + 1, E>(f);
+    }
+}
+
+// s_waitcnt vmcnt(VM) (lgkmcnt and expcnt untouched)
+template <int VM>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(VM >= 0 && VM < 64, "vmcnt field");
+    constexpr int imm = (VM & 0xF) | ((VM >> 4) << 14) | (0xF << 8) | (0x7 << 4);
+    __builtin_amdgcn_s_waitcnt(imm);
+}
+
+// 4 bytes per lane at byte offset voff of the buffer into LDS at dst + 4 * lane
+// (dst wave-uniform).  A device function: the builtin has no host form.
+__device__ __forceinline__ void buffer_to_lds(__amdgpu_buffer_rsrc_t r, float *dst, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)dst, 4,
+                                             static_cast<int>(voff), 0, 0, 0);
+}
+
+template <int NST>
+__global__ __launch_bounds__(256, NST <= 3 ? 3 : 2)
+void gemm_conv_ring_kernel(GemmArgs g) {
+    if (!decision_gate(g.dec, 2u)) return;
+    constexpr int BM = kConvBM, BN = kConvBN, BK = kConvBK;
+    constexpr int AP = kConvAPitch, AL = kConvALoads;
+    constexpr int LOADS = AL + (BK / 4) * 2;  // vector-memory operations per wavefront per slice
+    constexpr int AW = AL * 4 * 64;           // LDS words of an A slot (>= BM * AP)
+    __shared__ __align__(16) float ring[NST][AW + BK * BN];  // [slot][A: m x AP | B: k x n]
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    const int m0 = blockIdx.y * BM;
+    const int n0 = blockIdx.x * BN;
+    const int M = g.M, N = g.N, Kd = g.Kd;
+    const int HW = g.H * g.W;
+
+    const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(g.a), 0, static_cast<int>(static_cast<int64_t>(M) * g.lda * 4), kGemmBufferFormat);
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(g.x), 0, static_cast<int>(static_cast<int64_t>(g.N / g.conv_hw) * g.C * HW * 4),
+        kGemmBufferFormat);
+
+    // this lane's A slots: slot q = (wave*AL + i)*64 + lane holds row q / AP,
+    // k offset q % AP of the slice (pad slots and rows past M read nothing)
+    uint32_t aoff[AL];
+    int akk[AL];
+#pragma unroll
+    for (int i = 0; i < AL; ++i) {
+        const int q = (wave * AL + i) * 64 + lane;
+        const int row = q / AP, kk = q - (q / AP) * AP;
+        const int m = m0 + row;
+        const bool ok = row < BM && kk < BK && m < M;
+        aoff[i] = ok ? (static_cast<uint32_t>(m) * static_cast<uint32_t>(g.lda) + static_cast<uint32_t>(kk)) * 4u
+                     : kOutOfRange;
+        akk[i] = ok ? kk : (1 << 30);  // past every C*R*S
+    }
+    // this lane's B columns (n0 + h*64 + lane)
+    int coff[2], iy0[2], ix0[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int j = n0 + h * 64 + lane;
+        if (j < N) {
+            const int img = j / g.conv_hw;
+            const int p = j - img * g.conv_hw;
+            const int oy = p / g.Wo;
+            const int ox = p - oy * g.Wo;
+            iy0[h] = oy * g.T - g.P;
+            ix0[h] = ox * g.T - g.P;
+            coff[h] = img * g.C * HW + iy0[h] * g.W + ix0[h];
+        } else {
+            iy0[h] = -(1 << 30);  // fails every bounds test
+            ix0[h] = 0;
+            coff[h] = 0;
+        }
+    }
+
+    // slice kt -> slot SLOT: wavefront w loads AL instructions of A slots and
+    // k rows 4w .. 4w+3 of B, both 64-wide halves of each
+    auto issue = [&](auto slot_c, int kt) {
+        constexpr int SLOT = decltype(slot_c)::value;
+        const int k0 = kt * BK;
+#pragma unroll
+        for (int i = 0; i < AL; ++i)
+            buffer_to_lds(ra, &ring[SLOT][(wave * AL + i) * 64],
+                          k0 + akk[i] < Kd ? aoff[i] + static_cast<uint32_t>(k0) * 4u : kOutOfRange);
+#pragma unroll
+        for (int i = 0; i < BK / 4; ++i) {
+            const int kk = wave * (BK / 4) + i;
+            const int k = kt * BK + kk;
+            const bool kin = k < Kd;
+            const int kc = kin ? k : 0;
+            const int c = divm(kc, g.RS, g.mRS);
+            const int rs = kc - c * g.RS;
+            const int r = divm(rs, g.S, g.mS);
+            const int sx = rs - r * g.S;
+            const int roff = (c * g.H + r) * g.W + sx;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int iy = iy0[h] + r, ix = ix0[h] + sx;
+                const bool in = kin && static_cast<unsigned>(iy) < static_cast<unsigned>(g.H) &&
+                                static_cast<unsigned>(ix) < static_cast<unsigned>(g.W);
+                buffer_to_lds(rx, &ring[SLOT][AW + kk * BN + h * 64],
+                              in ? static_cast<uint32_t>(coff[h] + roff) * 4u : kOutOfRange);
+            }
+        }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+    const int nk = (Kd + BK - 1) / BK;
+    for_static<0, NST - 1>([&](auto sl) { issue(sl, decltype(sl)::value); });
+    const int lrow = lane & 31;  // row (A) / column (B) within a 32-block
+    const int lk = lane >> 5;    // which of the two k of an MFMA step
+    for (int kt = 0; kt < nk; ++kt) {
+        for_static<0, NST>([&](auto sl) {
+            constexpr int SL = decltype(sl)::value;
+            if (kt % NST == SL) {
+                // slice kt landed for every wavefront; everyone is done with
+                // slice kt - 1, whose slot is refilled next
+                wait_vmcnt<(NST - 2) * LOADS>();
+                asm volatile("s_barrier" ::: "memory");
+                issue(std::integral_constant<int, (SL + NST - 1) % NST>{}, kt + NST - 1);
+#pragma unroll
+                for (int kk = 0; kk < BK; kk += 2) {
+                    float av[2], bv[2];
+#pragma unroll
+                    for (int i = 0; i < 2; ++i) av[i] = ring[SL][((wm * 2 + i) * 32 + lrow) * AP + kk + lk];
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) bv[j] = ring[SL][AW + (kk + lk) * BN + (wn * 2 + j) * 32 + lrow];
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+#pragma unroll
+                        for (int j = 0; j < 2; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+                }
+            }
+        });
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // no load into LDS may outlive the workgroup
+
+    // epilogue: accumulator register v of lane l holds row
+    // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32 x 32 block
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const int nn = n0 + (wn * 2 + j) * 32 + lrow;
+        if (nn >= N) continue;
+        const int img = nn / g.conv_hw;
+        const int p = nn - img * g.conv_hw;
+        const size_t col_off = static_cast<size_t>(img) * M * g.conv_hw + p;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int m = m0 + (wm * 2 + i) * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+                if (m < M) {
+                    const float o = epilogue_value(acc[i][j][v], g.epi.relu);
+                    cnt += nonzero_bit(o);
+                    g.c[col_off + static_cast<size_t>(m) * g.conv_hw] = o;
+                }
+            }
+        }
+    }
+    if (g.epi.census) {
+        __syncthreads();  // every wavefront is done with the ring
+        census_commit(g.epi, cnt, reinterpret_cast<uint32_t *>(&ring[0][0]));
+    }
+}
+
 // The split reduction's second pass: c = epilogue(sum over z of part[z]),
 // partials added in z order; each workgroup takes kReducePer consecutive
 // elements of the M x N result (consecutive threads on consecutive columns)
@@ -474,12 +688,12 @@ int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
 
 }  // namespace
 
-// Expected time of the implicit GEMM (ms): a fixed part, the rounds of
-// resident tiles times each tile's reduction length and size, the output
-// (times the ranges of a split reduction, whose partial sums are written and
-// summed), and a second launch when the reduction is split.  Coefficients
-// fitted to the dense path measured on every workload and Tab. 2 shape
-// (15 % rms).
+// Expected time of the implicit GEMM (ms): a fixed part, the tiles of the
+// busiest CU (workgroups spread over 256 CUs) times each tile's reduction
+// length and size, the output (times the ranges of a split reduction, whose
+// partial sums are written and summed), and a second launch when the
+// reduction is split.  Coefficients fitted to the dense path measured on
+// every workload and Tab. 2 shape (7.5 % rms, 19 % at most).
 double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
     int64_t tm, tn;
     if (M <= 32) {
@@ -495,10 +709,10 @@ double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
     const int64_t tiles = gemm_tiles(M, Ncols);
     const int kc = Kd < (1ll << 31) ? gemm_kchunk(M, Ncols, static_cast<int>(Kd)) : 0;
     const int64_t ranges = kc > 0 ? (Kd + kc - 1) / kc : 1;
-    const double rounds = std::ceil(static_cast<double>(tiles * ranges) / 512.0);
+    const double per_cu = std::ceil(static_cast<double>(tiles * ranges) / 256.0);
     const double per = static_cast<double>(Kd) / ranges * tm * tn;
-    return 0.0147936 + 8.70142e-9 * rounds * per + 5.93757e-9 * static_cast<double>(M) * Ncols * ranges +
-           (ranges > 1 ? 0.00754156 : 0.0);
+    return 0.0253300 + 5.70789e-9 * per_cu * per + 1.17338e-9 * static_cast<double>(M) * Ncols * ranges +
+           (ranges > 1 ? 0.00759 : 0.0);
 }
 
 size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd) {
@@ -529,6 +743,17 @@ hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int
     g.C = C; g.H = H; g.W = W; g.T = T; g.P = P; g.Wo = Wo; g.RS = R * S; g.S = S;
     g.mRS = div_magic(R * S);
     g.mS = div_magic(S);
+    // more than 64 output maps, no split, operands addressable by 31-bit
+    // byte offsets: the pipelined kernel
+    const int64_t x_bytes = static_cast<int64_t>(N) * C * H * W * 4;
+    const int64_t w_bytes = static_cast<int64_t>(K) * g.Kd * 4;
+    if (!g.part && K > 64 && x_bytes < (1ll << 31) && w_bytes < (1ll << 31)) {
+        dim3 grid((g.N + kConvBN - 1) / kConvBN, (g.M + kConvBM - 1) / kConvBM);
+        if (g.epi.census && census_slots_for(static_cast<int64_t>(grid.x) * grid.y) > g.epi.cap)
+            return hipErrorInvalidValue;
+        gemm_conv_ring_kernel<kConvStages><<<grid, 256, 0, s>>>(g);
+        return hipGetLastError();
+    }
     const bool a_vec = (g.lda % 4 == 0) && (reinterpret_cast<uintptr_t>(w) % 16 == 0);
     return launch_gemm_any(g, a_vec, false, true, s);
 }
