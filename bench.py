@@ -21,6 +21,9 @@ step is replayed from a HIP graph whose launches are queued behind that
 write, so host-side enqueue time never enters the interval.  `value` is the
 dense-equivalent rate at the median of the K cold steps (p10 / p90 beside
 it); the warm figures (back-to-back replays, caches hot) come alongside.
+Paths compared with each other (AUTO, sparse, dense, the compaction and the
+sparse kernel alone; the chain's three forms) take their cold reps
+interleaved, rep i of each before rep i + 1 of any.
 
 Prints ONE JSON line: value = dense-equivalent TFLOP/s of the step
 (2*N*K*C*R*S*Ho*Wo per step), speedup against the same GPU's dense path
@@ -109,6 +112,23 @@ class ColdTimer:
             evs.append((a, b))
         torch.cuda.synchronize()
         return [a.elapsed_time(b) for a, b in evs[warm:]]
+
+    def times_interleaved(self, fns: dict, reps: int, warm: int = 2) -> dict:
+        """times() of several functions with their reps interleaved (rep i of
+        every function before rep i + 1 of any), so that clock and cache
+        drift over the run falls on all of them alike."""
+        torch = self.torch
+        evs = {name: [] for name in fns}
+        for i in range(warm + reps):
+            for name, fn in fns.items():
+                self.flush()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                fn()
+                b.record()
+                evs[name].append((a, b))
+        torch.cuda.synchronize()
+        return {name: [a.elapsed_time(b) for a, b in ev[warm:]] for name, ev in evs.items()}
 
 
 def stats(ms) -> dict:
@@ -214,12 +234,13 @@ class LayerRun:
         res = {}
         fns = {"auto": self.conv("auto"), "sparse": self.conv("sparse"), "dense": self.conv("dense"),
                "compact": self.compact(), "sparse_kernel": self.sparse_kernel()}
-        for name, fn in fns.items():
-            if graphs:
-                fn = graph_of(torch, fn).replay
-            st = stats(cold.times(fn, reps))
+        if graphs:
+            fns = {name: graph_of(torch, fn).replay for name, fn in fns.items()}
+        for name, ms in cold.times_interleaved(fns, reps).items():
+            st = stats(ms)
             res["t_%s_ms" % name] = st["median"]
             res["t_%s" % name] = st
+        for name, fn in fns.items():
             res["warm_%s_ms" % name] = round(event_time_ms(torch, fn, max(20, reps)), 6)
         return res
 
@@ -354,13 +375,14 @@ class ChainRun:
     def measure(self, cold, reps, graphs=True):
         torch = self.torch
         res = {}
-        for name in ("fused", "separate", "dense"):
-            fn = getattr(self, name)()
-            if graphs:
-                fn = graph_of(torch, fn).replay
-            st = stats(cold.times(fn, reps))
+        fns = {name: getattr(self, name)() for name in ("fused", "separate", "dense")}
+        if graphs:
+            fns = {name: graph_of(torch, fn).replay for name, fn in fns.items()}
+        for name, ms in cold.times_interleaved(fns, reps).items():
+            st = stats(ms)
             res["t_chain_%s_ms" % name] = st["median"]
             res["t_chain_%s" % name] = st
+        for name, fn in fns.items():
             res["warm_chain_%s_ms" % name] = round(event_time_ms(torch, fn, max(20, reps)), 6)
         # the activations of the fused run (the last one timed wrote the
         # dense run's outputs, equal up to rounding): run it once more
