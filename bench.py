@@ -408,6 +408,75 @@ class ChainRun:
         return res
 
 
+# Tab. 3 of the paper: one image on one core of a Xeon E5-2630 v4 at 2.2 GHz,
+# ms for Caffe's GEMM convolution (MKL) and for ISC, and the speedup printed,
+# per Tab. 2 layer.
+PAPER_TAB3_MS = {
+    "tab2_lenet_conv2_n1": (0.854, 0.123, 6.96), "tab2_alexnetc_conv3_n1": (0.329, 0.122, 2.69),
+    "tab2_alexneti_conv4_n1": (4.874, 1.660, 2.94), "tab2_inception4a_1_n1": (1.795, 1.292, 1.39),
+    "tab2_inception4a_2_n1": (0.943, 0.558, 1.69), "tab2_inception4e_3_n1": (7.602, 4.782, 1.59),
+    "tab2_inception5a_1_n1": (1.912, 0.645, 2.97), "tab2_inception5a_2_n1": (0.742, 0.258, 2.87),
+    "tab2_inception5b_3_n1": (4.410, 0.931, 4.74), "tab2_inception5b_5_n1": (1.560, 0.220, 7.11),
+}
+
+
+def host_cpu_rows(budget_s: float = 1.0) -> list:
+    """The paper's CPU comparison on this machine's host: for every Tab. 2
+    layer at one image, ISC on one core (the host library: steps 1-3,
+    AVX2 FMAs over K, filter repacked beforehand as an inference engine holds
+    it) against the GEMM convolution on one core (im2col, then a BLAS sgemm
+    limited to one thread), and the oracle (fp64 direct convolution) on one
+    thread; medians over repeats filling about budget_s per method."""
+    import oracle
+    from paper_1704_07724_amd import host
+    from threadpoolctl import threadpool_limits
+
+    def med_ms(fn):
+        fn()
+        times, t_end = [], time.perf_counter() + budget_s
+        while time.perf_counter() < t_end or len(times) < 3:
+            t0 = time.perf_counter()
+            fn()
+            times.append((time.perf_counter() - t0) * 1e3)
+        return float(np.median(times)), len(times)
+
+    rows = []
+    saved = oracle.threads()
+    oracle.set_threads(1)
+    try:
+        with threadpool_limits(1):
+            for layer in workloads.WORKLOADS["paper_tab2_n1"].layers:
+                x, w = workloads.make_inputs(layer)
+                T, P = layer.T, layer.P
+                Ho, Wo = host.out_shape(layer.H, layer.W, layer.R, layer.S, T, P)
+                wt = host.repack(w)
+                wm = np.ascontiguousarray(w.reshape(layer.K, -1))
+                y = np.empty((1, layer.K, Ho, Wo), np.float32)
+                yg = np.empty((layer.K, Ho * Wo), np.float32)
+
+                def gemm():
+                    np.matmul(wm, host.im2col(x[0], layer.R, layer.S, T, P), out=yg)
+
+                t_isc, n_isc = med_ms(lambda: host.conv2d(x, wt, T, P, threads=1, out=y))
+                t_gemm, n_gemm = med_ms(gemm)
+                t_oracle, _ = med_ms(lambda: oracle.conv2d_f64(x, w, T, P))
+                err = float(np.max(np.abs(yg.reshape(y.shape) - y)))
+                paper = PAPER_TAB3_MS.get(layer.name)
+                rows.append({"layer": layer.name, "sparsity": round(float(1.0 - np.count_nonzero(x) / x.size), 4),
+                             "t_isc_ms": round(t_isc, 4), "t_gemm_ms": round(t_gemm, 4),
+                             "t_oracle_ms": round(t_oracle, 4), "speedup_isc_vs_gemm": round(t_gemm / t_isc, 3),
+                             "max_abs_isc_minus_gemm": err, "reps": [n_isc, n_gemm],
+                             "paper_gemm_ms": paper[0] if paper else None, "paper_isc_ms": paper[1] if paper else None,
+                             "paper_speedup": paper[2] if paper else None})
+                r = rows[-1]
+                print("# host %s: ISC %.3f ms, GEMM %.3f ms (%.2fx; paper %.2fx), oracle %.3f ms" % (
+                    layer.name, t_isc, t_gemm, r["speedup_isc_vs_gemm"], r["paper_speedup"] or 0, t_oracle),
+                    file=sys.stderr, flush=True)
+    finally:
+        oracle.set_threads(saved)
+    return rows
+
+
 def cpu_baseline(layer, budget_s=10.0):
     """The oracle (fp64 direct convolution) on the headline workload, timed on
     this host: with all its threads, repeated over the whole batch (or the
@@ -586,11 +655,26 @@ def main():
     ap.add_argument("--all", action="store_true", help="also measure every workload layer")
     ap.add_argument("--out", default=None, help="JSONL file for --all rows")
     ap.add_argument("--workload", default="alexnet_conv2", help="headline workload (a workloads.py layer name)")
+    ap.add_argument("--host-cpu", action="store_true",
+                    help="only the paper's CPU comparison on the host: ISC against im2col + BLAS "
+                         "on one core for every Tab. 2 layer at one image (no GPU needed)")
     ap.add_argument("--probe", type=int, default=0, metavar="N",
                     help="only launch each kernel of the headline layer N times, eagerly, after "
                          "a copy kernel of known size, and print their algorithmic bytes "
                          "(a short program for hardware-counter runs)")
     args = ap.parse_args()
+
+    if args.host_cpu:
+        rows = host_cpu_rows()
+        cpu = _cpu_model()
+        for r in rows:
+            r["cpu"] = cpu
+        if args.out:
+            with open(args.out, "a") as fh:
+                for r in rows:
+                    fh.write(json.dumps(r) + "\n")
+        print(json.dumps({"host_cpu": rows}))
+        return
 
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "

@@ -109,8 +109,7 @@ __device__ __forceinline__ uint32_t compact_planes(const float *__restrict__ x, 
             }
             if (lane == 0) rp[H] = static_cast<int32_t>(base);
             listed += base;
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) cur[u] = nxt[u];
+            __builtin_memcpy(cur, nxt, sizeof(cur));
         }
         return listed;
     }
@@ -171,8 +170,7 @@ __device__ __forceinline__ uint32_t compact_planes(const float *__restrict__ x, 
         if (pn >= planes) break;
         p = pn;
         e0 = en;
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) cur[u] = nxt[u];
+        __builtin_memcpy(cur, nxt, sizeof(cur));
     }
     return listed;
 }
