@@ -363,9 +363,10 @@ constexpr int kConvBM = 128, kConvBN = 128, kConvBK = 16;
 constexpr int kConvAPitch = kConvBK + 1;                                   // LDS words per A row
 constexpr int kConvALoads = (kConvBM * kConvAPitch + 4 * 64 - 1) / (4 * 64);  // A loads per wavefront per slice
 // Two stages (the next slice in flight while the current one is multiplied)
-// and three workgroups per CU measured faster than deeper rings at two per
-// CU: AlexNet conv2 1.31 ms with 2 stages, 1.39 with 4, 1.48 with 3 (at three
-// workgroups per CU), 1.89 with 5 (one); the register-staged kernel 1.37.
+// and four workgroups per CU measured faster than deeper rings at fewer per
+// CU: AlexNet conv2 1.24 ms with 2 stages at four per CU, 1.28-1.31 at
+// three, 1.36-1.48 with 3 stages, 1.39 with 4 (two per CU), 1.89 with 5
+// (one); the register-staged kernel 1.37.
 constexpr int kConvStages = 2;
 constexpr uint32_t kOutOfRange = 0x80000000u;  // beyond every buffer this kernel reads (< 2^31 bytes)
 constexpr int kGemmBufferFormat = 0x00020000;  // raw buffer, 32-bit data
@@ -394,7 +395,7 @@ __device__ __forceinline__ void buffer_to_lds(__amdgpu_buffer_rsrc_t r, float *d
 }
 
 template <int NST>
-__global__ __launch_bounds__(256, NST <= 3 ? 3 : 2)
+__global__ __launch_bounds__(256, NST <= 2 ? 4 : (NST == 3 ? 3 : 2))
 void gemm_conv_ring_kernel(GemmArgs g) {
     if (!decision_gate(g.dec, 2u)) return;
     constexpr int BM = kConvBM, BN = kConvBN, BK = kConvBK;
@@ -418,20 +419,6 @@ void gemm_conv_ring_kernel(GemmArgs g) {
         const_cast<float *>(g.x), 0, static_cast<int>(static_cast<int64_t>(g.N / g.conv_hw) * g.C * HW * 4),
         kGemmBufferFormat);
 
-    // this lane's A slots: slot q = (wave*AL + i)*64 + lane holds row q / AP,
-    // k offset q % AP of the slice (pad slots and rows past M read nothing)
-    uint32_t aoff[AL];
-    int akk[AL];
-#pragma unroll
-    for (int i = 0; i < AL; ++i) {
-        const int q = (wave * AL + i) * 64 + lane;
-        const int row = q / AP, kk = q - (q / AP) * AP;
-        const int m = m0 + row;
-        const bool ok = row < BM && kk < BK && m < M;
-        aoff[i] = ok ? (static_cast<uint32_t>(m) * static_cast<uint32_t>(g.lda) + static_cast<uint32_t>(kk)) * 4u
-                     : kOutOfRange;
-        akk[i] = ok ? kk : (1 << 30);  // past every C*R*S
-    }
     // this lane's B columns (n0 + h*64 + lane)
     int coff[2], iy0[2], ix0[2];
 #pragma unroll
@@ -458,9 +445,19 @@ void gemm_conv_ring_kernel(GemmArgs g) {
         constexpr int SLOT = decltype(slot_c)::value;
         const int k0 = kt * BK;
 #pragma unroll
-        for (int i = 0; i < AL; ++i)
+        for (int i = 0; i < AL; ++i) {
+            // slot q = (wave*AL + i)*64 + lane holds row q / AP, k offset
+            // q % AP of the slice (pad slots, rows past M and k past C*R*S
+            // read nothing); decoded per load, which keeps the registers
+            // for a fourth workgroup per CU
+            const int q = (wave * AL + i) * 64 + lane;
+            const int row = q / AP, kk = q - (q / AP) * AP;
+            const int m = m0 + row;
+            const bool ok = row < BM && kk < BK && m < M && k0 + kk < Kd;
             buffer_to_lds(ra, &ring[SLOT][(wave * AL + i) * 64],
-                          k0 + akk[i] < Kd ? aoff[i] + static_cast<uint32_t>(k0) * 4u : kOutOfRange);
+                          ok ? (static_cast<uint32_t>(m) * static_cast<uint32_t>(g.lda) + static_cast<uint32_t>(k0 + kk)) * 4u
+                             : kOutOfRange);
+        }
 #pragma unroll
         for (int i = 0; i < BK / 4; ++i) {
             const int kk = wave * (BK / 4) + i;
@@ -693,7 +690,7 @@ int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
 // length and size, the output (times the ranges of a split reduction, whose
 // partial sums are written and summed), and a second launch when the
 // reduction is split.  Coefficients fitted to the dense path measured on
-// every workload and Tab. 2 shape (7.5 % rms, 19 % at most).
+// every workload and Tab. 2 shape (8.1 % rms, 19 % at most).
 double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
     int64_t tm, tn;
     if (M <= 32) {
@@ -711,8 +708,8 @@ double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
     const int64_t ranges = kc > 0 ? (Kd + kc - 1) / kc : 1;
     const double per_cu = std::ceil(static_cast<double>(tiles * ranges) / 256.0);
     const double per = static_cast<double>(Kd) / ranges * tm * tn;
-    return 0.0253300 + 5.70789e-9 * per_cu * per + 1.17338e-9 * static_cast<double>(M) * Ncols * ranges +
-           (ranges > 1 ? 0.00759 : 0.0);
+    return 0.0257600 + 5.57801e-9 * per_cu * per + 0.98543e-9 * static_cast<double>(M) * Ncols * ranges +
+           (ranges > 1 ? 0.00803 : 0.0);
 }
 
 size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd) {
