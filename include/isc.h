@@ -302,9 +302,11 @@ int isc_sparse_conv(const isc_conv_desc *d, const int32_t *row_ptr, const isc_nz
  * each nonzero by the K-contiguous weight vectors of step 2, which it holds
  * in registers.  The filter is resident in LDS when it fits (K <= 64:
  * ISC_KERNEL_FUSED), streamed from L2 into each wavefront's registers at
- * stride 1 with at most 16 output columns, for any K (ISC_KERNEL_FUSED_REG,
- * one workgroup per group of 64 output maps), and streamed through LDS
- * otherwise (ISC_KERNEL_FUSED_RING).  The kernels isc_conv2d's sparse path runs when
+ * stride 1 with at most 16 output columns (ISC_KERNEL_FUSED_REG, one
+ * workgroup per group of 64 output maps: taken there when K > 64, when the
+ * filter does not fit in LDS, or when every wavefront of the resident plan
+ * would own its channels alone), and streamed through LDS otherwise
+ * (ISC_KERNEL_FUSED_RING).  The kernels isc_conv2d's sparse path runs when
  * isc_sparse_kernel reports either (isc_conv2d repacks the filter itself, in
  * the launch that counts the nonzeros); no sparse/dense decision here.
  *   x: device input as for isc_conv2d.
