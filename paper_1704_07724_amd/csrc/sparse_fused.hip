@@ -17,8 +17,9 @@ size_t fused_lds(int crs, int th, int tw) {
 
 // Plans whose wavefronts share no channel (every wavefront its own phase)
 // gain nothing from the filter in LDS: with the weights streamed to
-// registers, LDS holds only the phase tiles, and 32-position tiles let two
-// workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us).  The filter need not
+// registers, LDS holds only the reduction's tiles, and 32-position tiles let
+// two workgroups share a CU (LeNet conv2: 13.2 -> 9.5 us), four since the
+// tiles are summed in pairs (AlexNet conv3-5 10-12 % faster).  The filter need not
 // fit in LDS at all, and one workgroup per group of 64 maps takes any K
 // (AlexNet-ImageNet conv4 of Tab. 2 at batch 128: 259 us on the
 // filter-ring kernel -> 113 us).  Taken wherever eligible: stride 1, square
@@ -40,7 +41,7 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
     const int64_t kgroups = (sh.K + kLanes - 1) / kLanes;
     int th = static_cast<int64_t>(sh.N) * ((sh.Ho + full - 1) / full) * kgroups < kMinGroups ? full / 2 : full;
     if (sh.tu.rows == full || sh.tu.rows == full / 2) th = sh.tu.rows;
-    *plan = FusedPlan{th, tw, kWaves, sizeof(float) * kWaves * th * tw * kRPad, 1, true};
+    *plan = FusedPlan{th, tw, kWaves, sizeof(float) * kRegSlots * th * tw * kRPad, 1, true};
     return true;
 }
 

@@ -21,9 +21,9 @@
 // channel's R*S weights (64 output maps, one per lane) into registers.
 // Wavefront w owns a TH x TW output tile (tile machinery in sparse_tile.hpp)
 // of row group w / cs and the input channels c = (w mod cs) + i*cs.  The cs
-// partial tiles of a row group are then summed through LDS in phase order
-// and stored to NCHW (step 3) with consecutive threads on consecutive
-// columns of one output map.
+// partial tiles of a row group are then summed through LDS, phases p and
+// p + cs/2 first, then those pairs in order, and stored to NCHW (step 3)
+// with consecutive threads on consecutive columns of one output map.
 // Summation order per output is fixed for a given launch shape, so results
 // are deterministic.
 #pragma once
@@ -39,6 +39,7 @@ constexpr size_t kLdsMax = 160 * 1024;
 constexpr int kRPad = 65;        // LDS pitch of one tile position's output maps (reduction)
 static_assert(kRPad > kLanes, "the pad column holds the census sums");
 constexpr int kMaxTile = 64;     // accumulators per lane
+constexpr int kRegSlots = kWaves / 2;  // phase-pair tiles of the register-weight kernel's reduction
 constexpr int kMinGroups = 256;  // workgroups that fill the CUs once
 constexpr int kWPitch = 64;      // maps per filter column in the repacked layout (K <= 64)
 // Word 3 of a raw buffer resource on gfx9-family chips (gfx950 included):
@@ -192,7 +193,7 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     // with a padded pitch (conflict-free); then each thread takes one output
     // position of the workgroup and the maps k0, k0 + ostep, ..., so that
     // consecutive threads store consecutive positions of one map, and sums
-    // the phases of each output in phase order.
+    // the phases of each output in pairs.
     constexpr int TP = TH * TW;
     __syncthreads();  // every wavefront is done with its weights
     float *red = lds;
@@ -214,21 +215,28 @@ void sparse_conv_fused_kernel(FusedArgs a) {
     const size_t plane_out = static_cast<size_t>(a.Ho) * Wo;
     const float *src = red + ((g * cs) * TP + (oyl - g * TH) * TW + ox) * kRPad;
     float *dst = a.y + static_cast<size_t>(n) * a.K * plane_out + static_cast<size_t>(oyb) * Wo + pos;
-    // phase p's partial at src + p * TP * kRPad; phases past cs read the last
-    // one again (in bounds, no branches) and are not added
-    int poff[kWaves];
+    // phase p's partial at src + p * TP * kRPad.  Summed in pairs (p, p +
+    // cs/2), pairs in order -- the order of the register-weight kernel's
+    // reduction, so the two kernels agree bitwise where both apply.  Pairs
+    // past cs/2 read the last phase again (in bounds, no branches) and are
+    // not added.
+    const int h = cs > 1 ? cs / 2 : 0;
+    int pa[kRegSlots], pb[kRegSlots];
 #pragma unroll
-    for (int p = 0; p < kWaves; ++p) poff[p] = min(p, cs - 1) * TP * kRPad;
+    for (int i = 0; i < kRegSlots; ++i) {
+        pa[i] = min(i, cs - 1) * TP * kRPad;
+        pb[i] = min(i + h, cs - 1) * TP * kRPad;
+    }
     const int relu = a.epi.relu;
     uint32_t cnt = 0;
     // threads past ostep map groups have no output (k0 >= ostep)
     for (int k = k0 < ostep ? k0 : a.K; k < a.K; k += ostep) {
-        float part[kWaves];
+        float pair[kRegSlots];
 #pragma unroll
-        for (int p = 0; p < kWaves; ++p) part[p] = src[poff[p] + k];
-        float sum = part[0];
+        for (int i = 0; i < kRegSlots; ++i) pair[i] = h > 0 ? src[pa[i] + k] + src[pb[i] + k] : src[pa[i] + k];
+        float sum = pair[0];
 #pragma unroll
-        for (int p = 1; p < kWaves; ++p) sum += p < cs ? part[p] : 0.0f;
+        for (int i = 1; i < kRegSlots; ++i) sum += i < h ? pair[i] : 0.0f;
         sum = epilogue_value(sum, relu);
         cnt += nonzero_bit(sum);
         dst[static_cast<size_t>(k) * plane_out] = sum;
@@ -244,9 +252,9 @@ void sparse_conv_fused_kernel(FusedArgs a) {
 // Variant for plans whose wavefronts share no input channel (cs == kWaves:
 // one row group, every wavefront its own channels): each wavefront streams
 // its channels' weights from the repacked filter (through L2) into
-// registers, one channel ahead of its walk, so LDS holds only the phase
-// tiles -- for four-row tiles of 8 columns little enough for two
-// workgroups per CU, four wavefronts per SIMD.  One workgroup per group of
+// registers, one channel ahead of its walk, so LDS holds only the tiles of
+// the reduction -- one per pair of phases, for four-row tiles of 8 columns
+// little enough for four workgroups per CU.  One workgroup per group of
 // 64 output maps (kgroups), lanes over the maps of its group.  Stride 1;
 // otherwise as the kernel above.
 template <int RS_, int TH, int TW, bool WIDE>
@@ -254,7 +262,7 @@ __global__ __launch_bounds__(kWaves * kLanes, 4)
 void sparse_conv_fused_reg_kernel(FusedArgs a) {
     using T = tile::Shape<RS_, RS_, 1, TH, TW>;
     constexpr int RS2 = RS_ * RS_, EPL = T::EPL;
-    extern __shared__ float lds[];  // the phase tiles [wave][TH*TW][kRPad]
+    extern __shared__ float lds[];  // the phase-pair tiles [kRegSlots][TH*TW][kRPad]
 
     const int tid = threadIdx.x;
     const int lane = tid & (kLanes - 1);
@@ -348,14 +356,32 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
         tile::walk_scan<T>(mask, cur, acc, w);
     }
 
-    // step 3: the phase tiles summed through LDS in phase order and stored
-    // to NCHW, as in the kernel above (one row group)
+    // step 3: the phase tiles summed through LDS and stored to NCHW, as in
+    // the kernel above (one row group).  Half as many tiles as phases: the
+    // upper phases write theirs, each lower phase p adds phase p + 4's to its
+    // registers and writes the pair back into the same slot, and the store
+    // sums the four pairs in order -- a fixed order, so deterministic.  The
+    // smaller LDS footprint lets twice as many workgroups share a CU.
     constexpr int TP = TH * TW;
+    constexpr int kSlots = kRegSlots;
     float *red = lds;
+    const int slot = wave % kSlots;
+    if (wave >= kSlots) {
 #pragma unroll
-    for (int y = 0; y < TH; ++y)
+        for (int y = 0; y < TH; ++y)
 #pragma unroll
-        for (int x = 0; x < TW; ++x) red[(wave * TP + y * TW + x) * kRPad + lane] = acc[y][x][0];
+            for (int x = 0; x < TW; ++x) red[(slot * TP + y * TW + x) * kRPad + lane] = acc[y][x][0];
+    }
+    __syncthreads();
+    if (wave < kSlots) {
+#pragma unroll
+        for (int y = 0; y < TH; ++y)
+#pragma unroll
+            for (int x = 0; x < TW; ++x) {
+                float *r = red + (slot * TP + y * TW + x) * kRPad + lane;
+                *r = acc[y][x][0] + *r;
+            }
+    }
     __syncthreads();
     const int Wo = a.Wo;
     const int rows = min(TH, a.Ho - oy0);
@@ -372,12 +398,12 @@ void sparse_conv_fused_reg_kernel(FusedArgs a) {
     uint32_t cnt = 0;
     // k: map within this workgroup's group of 64
     for (int k = k0 < ostep ? k0 : kcnt; k < kcnt; k += ostep) {
-        float part[kWaves];
+        float part[kSlots];
 #pragma unroll
-        for (int p = 0; p < kWaves; ++p) part[p] = src[p * TP * kRPad + k];
+        for (int p = 0; p < kSlots; ++p) part[p] = src[p * TP * kRPad + k];
         float sum = part[0];
 #pragma unroll
-        for (int p = 1; p < kWaves; ++p) sum += part[p];
+        for (int p = 1; p < kSlots; ++p) sum += part[p];
         sum = epilogue_value(sum, relu);
         cnt += nonzero_bit(sum);
         dst[static_cast<size_t>(k) * plane_out] = sum;

@@ -471,7 +471,8 @@ def test_fused_weight_placements_agree(torch, isc, case):
     """Plans whose wavefronts share no channel stream the weights to
     registers by default; the filter-in-LDS kernel (tuning kernel "fused") on the
     same shapes: both against the oracle, and bitwise equal to each other
-    (the same channel order per phase and phase order per output)."""
+    (the same channel order per phase and the same pairing of the phases
+    per output)."""
     N, C, H, W, K, R, S, T, P, sp = case
     note("fused weight placement", case)
     x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=71 + sum(case[:9]))
