@@ -14,9 +14,11 @@
 // positions (F_scan: the scan's tests, the ring's LDS traffic), the window's
 // nonzeros times their work (F_nz: scalar dispatch plus taps times maps per
 // lane in multiply-adds), and the channels each wavefront walks in sequence
-// (F_chain: memory latency per channel on small grids).  The coefficients
-// of each kernel family were fitted to the sparse path measured on every
-// workload and Tab. 2 shape at sparsities 0.5 to 0.99 (5-11 % rms); the
+// (F_chain: memory latency per channel on small grids; for the
+// register-weight kernel times the rounds of resident workgroups).  The coefficients
+// of each kernel family (the register-weight kernel's per filter size) were
+// fitted to the sparse path measured on every workload and Tab. 2 shape at
+// sparsities 0.5 to 0.99 (5-9 % rms); the
 // dense path's model is in dense_conv.hip.  The limit handed to the device
 // is the largest nonzero count whose modelled sparse time does not exceed
 // the modelled dense time; the device compares integers only.
@@ -33,7 +35,15 @@ struct Fit {
 };
 
 constexpr Fit kRingFit{0.07996214, 1.82930381, 1.78868403, 0.0};
-constexpr Fit kRegFit{0.02229609, 2.02201313, 0.85251592, 0.25481821};
+// the register-weight kernel per filter size (1x1, 3x3, 5x5: its only
+// ones), whose chain feature counts the rounds of resident workgroups
+constexpr Fit kRegFit1{0.020853829, 0.9847653, 0.45193746, 0.30660876};
+constexpr Fit kRegFit3{0.024391336, 1.1026716, 0.46104798, 0.43310146};
+constexpr Fit kRegFit5{0.019387133, 2.2505374, 1.0093551, 0.87563861};
+// its workgroups per CU: eight wavefronts each, 60-66 VGPRs for 1x1 and 3x3
+// filters (eight wavefronts per SIMD, the 33 KB of reduction tiles four
+// times over), 80-98 for 5x5 (five per SIMD)
+inline int reg_workgroups_per_cu(int R) { return R == 5 ? 2 : 4; }
 constexpr Fit kResidentFit{0.01847326, 0.0, 1.77078063, 1.41836285};
 
 }  // namespace
@@ -45,7 +55,8 @@ long long crossover_nnz_limit(const SparseShape &sh) {
         // kernels over compacted lists: no model, the paper's 0.9
         return static_cast<long long>(std::floor(0.1 * static_cast<double>(total)));
     }
-    const Fit &f = p.kernel == ISC_KERNEL_FUSED_RING ? kRingFit : (p.kernel == ISC_KERNEL_FUSED_REG ? kRegFit : kResidentFit);
+    const Fit &freg = sh.R == 1 ? kRegFit1 : (sh.R == 3 ? kRegFit3 : kRegFit5);
+    const Fit &f = p.kernel == ISC_KERNEL_FUSED_RING ? kRingFit : (p.kernel == ISC_KERNEL_FUSED_REG ? freg : kResidentFit);
     const double wc = static_cast<double>(p.workgroups) * p.waves * sh.C / std::max(1, p.phases);
     const int wrows = (p.rows - 1) * sh.T + sh.R, wcols = (p.cols - 1) * sh.T + sh.S;
     const double pw = static_cast<double>(wrows) * wcols;
@@ -60,7 +71,12 @@ long long crossover_nnz_limit(const SparseShape &sh) {
     } else {
         scan = wc * pw * 1e-9;
     }
-    const double chain = static_cast<double>(sh.C) / std::max(1, p.phases) * 1e-3;
+    // channels each wavefront walks in sequence; for the register-weight
+    // kernel, whose wavefronts wait on their own chain of loads and scans,
+    // times the rounds of resident workgroups the grid takes
+    double chain = static_cast<double>(sh.C) / std::max(1, p.phases) * 1e-3;
+    if (p.kernel == ISC_KERNEL_FUSED_REG)
+        chain *= std::ceil(static_cast<double>(p.workgroups) / (256.0 * reg_workgroups_per_cu(sh.R)));
     const double fixed = f.c0 + f.c_scan * scan + f.c_chain * chain;
     const double per_density = f.c_nz * wc * pin * (10.0 + taps * kpl) * 1e-9;
     const double dense = dense_time_model(sh.K, static_cast<int64_t>(sh.N) * sh.Ho * sh.Wo,
