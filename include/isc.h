@@ -103,7 +103,9 @@ typedef struct isc_tuning {
     int32_t waves;         /* wavefronts per workgroup of the filter-ring kernel */
     int32_t wide_loads;    /* 1: the register-weight kernel loads its weights
                               through a buffer resource on one map group too */
-    int32_t gemm_split;    /* -1: the dense GEMM never splits its reduction */
+    int32_t gemm_split;    /* -1: the dense GEMM never splits its reduction,
+                              and ws needs no room for its partial sums
+                              (which isc_workspace_size counts) */
     int32_t reserved;      /* must be 0 */
 } isc_tuning;
 
@@ -119,8 +121,10 @@ int isc_out_shape(const isc_conv_desc *d, int32_t *Ho, int32_t *Wo);
 
 /* Bytes of device workspace isc_conv2d needs for this descriptor and path
  * (AUTO needs the sparse and dense buffers; the dense path needs an im2col
- * buffer only when C*R*S >= 2^16).  Host-only.  Errors: NULL,
- * SHAPE, LIMIT, PATH. */
+ * buffer only when C*R*S >= 2^16, and the partial sums of its GEMM's split
+ * reduction where the GEMM splits: small grids, and grids of 128 x 128
+ * tiles that a split spreads more evenly over the CUs).  Host-only.
+ * Errors: NULL, SHAPE, LIMIT, PATH. */
 int isc_workspace_size(const isc_conv_desc *d, int32_t path, size_t *bytes);
 
 /* The convolution of Eq. 1 (Sec. "Sparsity of ReLUs"), extended with batch,
@@ -162,8 +166,11 @@ int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, flo
  * synchronisation, or from several threads) race and must not be made; the
  * buffer needs no clearing (the path writes every word it reads).
  *   x, w, y, path, threshold, stream: as for isc_conv2d.
+ * Where the dense GEMM's split reduction would not fit in the buffer with
+ * the rest of the workspace, the GEMM runs unsplit (as with tuning
+ * gemm_split = -1).
  * Errors: as isc_conv2d (no WORKSPACE); LIMIT also when the workspace this
- * descriptor and path need (isc_workspace_size) exceeds
+ * descriptor and path need without the split reduction exceeds
  * ISC_NOALLOC_SCRATCH_BYTES. */
 #define ISC_NOALLOC_SCRATCH_BYTES (16u << 20)
 int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, float *y,

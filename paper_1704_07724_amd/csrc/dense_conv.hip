@@ -488,8 +488,12 @@ void gemm_conv_ring_kernel(GemmArgs g) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    const int nk = (Kd + BK - 1) / BK;
-    for_static<0, NST - 1>([&](auto sl) { issue(sl, decltype(sl)::value); });
+    // the K slices of this workgroup: all of them, or with a split
+    // reduction those of range blockIdx.z (kchunk a multiple of BK).
+    // Slices prefetched past the range are loaded and never used.
+    const int kt0 = g.part ? static_cast<int>(blockIdx.z) * (g.kchunk / BK) : 0;
+    const int nk = g.part ? min(g.kchunk / BK, (Kd + BK - 1) / BK - kt0) : (Kd + BK - 1) / BK;
+    for_static<0, NST - 1>([&](auto sl) { issue(sl, kt0 + decltype(sl)::value); });
     const int lrow = lane & 31;  // row (A) / column (B) within a 32-block
     const int lk = lane >> 5;    // which of the two k of an MFMA step
     for (int kt = 0; kt < nk; ++kt) {
@@ -500,7 +504,7 @@ void gemm_conv_ring_kernel(GemmArgs g) {
                 // slice kt - 1, whose slot is refilled next
                 wait_vmcnt<(NST - 2) * LOADS>();
                 asm volatile("s_barrier" ::: "memory");
-                issue(std::integral_constant<int, (SL + NST - 1) % NST>{}, kt + NST - 1);
+                issue(std::integral_constant<int, (SL + NST - 1) % NST>{}, kt0 + kt + NST - 1);
 #pragma unroll
                 for (int kk = 0; kk < BK; kk += 2) {
                     float av[2], bv[2];
@@ -521,6 +525,22 @@ void gemm_conv_ring_kernel(GemmArgs g) {
 
     // epilogue: accumulator register v of lane l holds row
     // 8*(v/4) + 4*(l/32) + v%4 and column l%32 of its 32 x 32 block
+    if (g.part) {  // a partial sum of the split reduction, stored raw
+        float *pz = g.part + static_cast<size_t>(blockIdx.z) * M * N;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int nn = n0 + (wn * 2 + j) * 32 + lrow;
+            if (nn >= N) continue;
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = m0 + (wm * 2 + i) * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+                    if (m < M) pz[static_cast<size_t>(m) * N + nn] = acc[i][j][v];
+                }
+        }
+        return;
+    }
     uint32_t cnt = 0;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -669,47 +689,80 @@ int64_t gemm_tiles(int64_t M, int64_t Ncols) {
     return (M + 127) / 128 * ((Ncols + 127) / 128);
 }
 
-// Reduction range per workgroup, 0 for no split: a grid of fewer than 128
-// tiles (small batches: AlexNet-ImageNet conv4 at batch 1 is 3 tiles, each
-// walking all 3456 of C*R*S) splits C*R*S into ranges of at least 256, a
-// multiple of 32 (every K-slice of a range is whole), for a grid of about
-// 256 workgroups, at most 16 ranges.  (A caller's gemm_split = -1 passes no
-// partial-sum buffer, which turns it off.)
-int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
-    const int64_t tiles = gemm_tiles(M, Ncols);
-    if (tiles >= 128) return 0;
-    const int64_t splits = std::min<int64_t>({16, (256 + tiles - 1) / tiles, Kd / 256});
-    if (splits < 2) return 0;
-    return static_cast<int>((Kd + splits - 1) / splits + 31) / 32 * 32;
+// Workgroup tile (rows x columns) of the kernel launch_gemm_any or the
+// pipelined kernel runs for an M x Ncols product.
+void gemm_tile_shape(int64_t M, int64_t Ncols, int64_t *tm, int64_t *tn) {
+    if (M <= 32) {
+        *tm = 32;
+        *tn = (Ncols + 255) / 256 >= 512 ? 256 : 128;
+    } else if (M <= 64) {
+        *tm = 64;
+        *tn = (Ncols + 127) / 128 >= 512 ? 128 : 64;
+    } else {
+        *tm = 128;
+        *tn = 128;
+    }
 }
 
-}  // namespace
-
-// Expected time of the implicit GEMM (ms): a fixed part, the tiles of the
-// busiest CU (workgroups spread over 256 CUs) times each tile's reduction
-// length and size, the output (times the ranges of a split reduction, whose
-// partial sums are written and summed), and a second launch when the
-// reduction is split.  Coefficients fitted to the dense path measured on
-// every workload and Tab. 2 shape (8.1 % rms, 19 % at most).
-double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
+// Expected time of the implicit GEMM (ms) with C*R*S cut into `ranges`
+// reduction ranges: a fixed part, the tiles of the busiest CU (workgroups
+// spread over 256 CUs) times each tile's reduction length and size, the
+// output (times the ranges of a split reduction, whose partial sums are
+// written and summed), and a second launch when the reduction is split.
+// Coefficients fitted to the dense path measured on every workload and
+// Tab. 2 shape (8.1 % rms, 19 % at most).
+double gemm_model(int64_t M, int64_t Ncols, int64_t Kd, int64_t ranges) {
     int64_t tm, tn;
-    if (M <= 32) {
-        tm = 32;
-        tn = (Ncols + 255) / 256 >= 512 ? 256 : 128;
-    } else if (M <= 64) {
-        tm = 64;
-        tn = (Ncols + 127) / 128 >= 512 ? 128 : 64;
-    } else {
-        tm = 128;
-        tn = 128;
-    }
+    gemm_tile_shape(M, Ncols, &tm, &tn);
     const int64_t tiles = gemm_tiles(M, Ncols);
-    const int kc = Kd < (1ll << 31) ? gemm_kchunk(M, Ncols, static_cast<int>(Kd)) : 0;
-    const int64_t ranges = kc > 0 ? (Kd + kc - 1) / kc : 1;
     const double per_cu = std::ceil(static_cast<double>(tiles * ranges) / 256.0);
     const double per = static_cast<double>(Kd) / ranges * tm * tn;
     return 0.0257600 + 5.57801e-9 * per_cu * per + 0.98543e-9 * static_cast<double>(M) * Ncols * ranges +
            (ranges > 1 ? 0.00803 : 0.0);
+}
+
+// Reduction range per workgroup, 0 for no split; ranges are at least 256
+// deep and a multiple of 32 (every K-slice of a range is whole).  A grid of
+// fewer than 128 tiles (small batches: AlexNet-ImageNet conv4 at batch 1 is
+// 3 tiles, each walking all 3456 of C*R*S) splits for a grid of about 256
+// workgroups, at most 16 ranges.  A larger grid of 128 x 128 tiles (more
+// than 64 maps) splits into 2-4 ranges where the model above says the
+// busiest CU's share shrinks by more than the partial sums cost: AlexNet
+// conv5 at batch 128 is 338 tiles, two on 82 CUs and one on the rest, and
+// three ranges make it 1014 workgroups, four on the busiest CU with a third
+// of the reduction each (0.65 -> 0.45 ms).  A split must gain 10 % in the
+// model: at 5 % (the inception 3x3 branch, two ranges) the measured time did
+// not move.  (A caller's gemm_split = -1 passes no partial-sum buffer, which
+// turns it off.)
+int gemm_kchunk(int64_t M, int64_t Ncols, int Kd) {
+    const int64_t tiles = gemm_tiles(M, Ncols);
+    if (tiles < 128) {
+        const int64_t splits = std::min<int64_t>({16, (256 + tiles - 1) / tiles, Kd / 256});
+        if (splits < 2) return 0;
+        return static_cast<int>((Kd + splits - 1) / splits + 31) / 32 * 32;
+    }
+    if (M <= 64) return 0;
+    int best = 0;
+    double best_t = 0.9 * gemm_model(M, Ncols, Kd, 1);
+    for (int sp = 2; sp <= 4; ++sp) {
+        const int kc = ((Kd + sp - 1) / sp + 31) / 32 * 32;
+        if (kc < 256) break;
+        const double t = gemm_model(M, Ncols, Kd, (Kd + kc - 1) / kc);
+        if (t < best_t) {
+            best = kc;
+            best_t = t;
+        }
+    }
+    return best;
+}
+
+}  // namespace
+
+// Expected time of the dense path's GEMM (ms), with the split the launch
+// takes.
+double dense_time_model(int64_t M, int64_t Ncols, int64_t Kd) {
+    const int kc = Kd < (1ll << 31) ? gemm_kchunk(M, Ncols, static_cast<int>(Kd)) : 0;
+    return gemm_model(M, Ncols, Kd, kc > 0 ? (Kd + kc - 1) / kc : 1);
 }
 
 size_t conv_gemm_split_floats(int M, int64_t Ncols, int Kd) {
@@ -740,12 +793,23 @@ hipError_t launch_conv_gemm(const float *x, const float *w, float *y, int N, int
     g.C = C; g.H = H; g.W = W; g.T = T; g.P = P; g.Wo = Wo; g.RS = R * S; g.S = S;
     g.mRS = div_magic(R * S);
     g.mS = div_magic(S);
-    // more than 64 output maps, no split, operands addressable by 31-bit
-    // byte offsets: the pipelined kernel
+    // more than 64 output maps, operands addressable by 31-bit byte
+    // offsets: the pipelined kernel, with or without a split reduction
     const int64_t x_bytes = static_cast<int64_t>(N) * C * H * W * 4;
     const int64_t w_bytes = static_cast<int64_t>(K) * g.Kd * 4;
-    if (!g.part && K > 64 && x_bytes < (1ll << 31) && w_bytes < (1ll << 31)) {
+    if (K > 64 && x_bytes < (1ll << 31) && w_bytes < (1ll << 31)) {
         dim3 grid((g.N + kConvBN - 1) / kConvBN, (g.M + kConvBM - 1) / kConvBM);
+        if (g.part) {
+            if (g.kchunk <= 0 || g.kchunk % 32 != 0) return hipErrorInvalidValue;
+            grid.z = static_cast<unsigned>((g.Kd + g.kchunk - 1) / g.kchunk);
+            const int64_t rgroups = (static_cast<int64_t>(g.M) * g.N + kReducePer - 1) / kReducePer;
+            if (g.epi.census && census_slots_for(rgroups) > g.epi.cap) return hipErrorInvalidValue;
+            gemm_conv_ring_kernel<kConvStages><<<grid, 256, 0, s>>>(g);
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            gemm_split_reduce_kernel<<<static_cast<unsigned>(rgroups), 256, 0, s>>>(g, static_cast<int>(grid.z));
+            return hipGetLastError();
+        }
         if (g.epi.census && census_slots_for(static_cast<int64_t>(grid.x) * grid.y) > g.epi.cap)
             return hipErrorInvalidValue;
         gemm_conv_ring_kernel<kConvStages><<<grid, 256, 0, s>>>(g);

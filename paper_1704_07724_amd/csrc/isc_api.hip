@@ -84,7 +84,9 @@ struct Layout {
     bool fused = false;     // sparse path compacts on the fly (no lists; the repacked filter only)
 };
 
-Layout layout_for(const Shape &s, int32_t path) {
+// split: room for the dense GEMM's split reduction when it takes one (a
+// caller's tuning gemm_split = -1 turns the split off and needs none).
+Layout layout_for(const Shape &s, int32_t path, bool split_ok = true) {
     Layout L;
     L.sparse = path != ISC_PATH_DENSE;
     L.dense = path != ISC_PATH_SPARSE;
@@ -111,10 +113,11 @@ Layout layout_for(const Shape &s, int32_t path) {
         L.col = off;
         off = align_up(off + sizeof(float) * static_cast<size_t>(s.crs() * s.ldcol()), kAlign);
     }
-    // the partial sums of the implicit GEMM's split reduction (small grids)
-    const size_t split = L.dense && L.implicit ? isc::conv_gemm_split_floats(static_cast<int>(s.K), s.ncols(),
-                                                                             static_cast<int>(s.crs()))
-                                               : 0;
+    // the partial sums of the implicit GEMM's split reduction (last, so the
+    // layout without it is a prefix of the layout with it)
+    const size_t split = split_ok && L.dense && L.implicit
+                             ? isc::conv_gemm_split_floats(static_cast<int>(s.K), s.ncols(), static_cast<int>(s.crs()))
+                             : 0;
     if (split > 0) {
         L.split = off;
         off = align_up(off + sizeof(float) * split, kAlign);
@@ -229,7 +232,7 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
     if (!(threshold >= 0.0f && threshold <= 1.0f) && !(threshold < 0.0f)) return ISC_ERR_ARG;
     if (!tuning_ok(tu)) return ISC_ERR_ARG;
     if (!aligned(x, 4) || !aligned(w, 4) || !aligned(y, 4) || !aligned(ws, kAlign)) return ISC_ERR_ALIGN;
-    const Layout L = layout_for(s, path);
+    const Layout L = layout_for(s, path, !(tu && tu->gemm_split < 0));
     if (ws_bytes < L.total) return ISC_ERR_WORKSPACE;
     const size_t xbytes = sizeof(float) * static_cast<size_t>(s.in_elems());
     const size_t ybytes = sizeof(float) * static_cast<size_t>(s.out_elems());
@@ -334,8 +337,7 @@ int conv_impl(const isc_conv_desc *d, const float *x, const float *w, float *y, 
                           path == ISC_PATH_DENSE ? ctrl : nullptr, path == ISC_PATH_AUTO ? ctrl : nullptr};
         if (L.implicit) {
             // one launch: the GEMM gathers the im2col matrix from x
-            float *part = L.split && !(tu && tu->gemm_split < 0) ? reinterpret_cast<float *>(base + L.split)
-                                                                  : nullptr;
+            float *part = L.split ? reinterpret_cast<float *>(base + L.split) : nullptr;
             if ((e = isc::launch_conv_gemm(x, w, y, sh.N, sh.C, sh.H, sh.W, sh.K, sh.R, sh.S, sh.T, sh.P, sh.Ho,
                                            sh.Wo, dec, hs, epi, part)) != hipSuccess)
                 return hip_status(e);
@@ -411,13 +413,20 @@ int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, f
     if (st) return st;
     if (!x || !w || !y) return ISC_ERR_NULL;
     if (!valid_path(path)) return ISC_ERR_PATH;
-    if (layout_for(s, path).total > kScratchBytes) return ISC_ERR_LIMIT;
+    // the dense GEMM's split reduction only where its partial sums fit too
+    isc_tuning nosplit{};
+    nosplit.gemm_split = -1;
+    const isc_tuning *tu = nullptr;
+    if (layout_for(s, path).total > kScratchBytes) {
+        if (layout_for(s, path, false).total > kScratchBytes) return ISC_ERR_LIMIT;
+        tu = &nosplit;
+    }
     st = check_device();
     if (st) return st;
     void *ws = nullptr;
     st = scratch_for_current_device(&ws);
     if (st) return st;
-    return conv_impl(d, x, w, y, ws, kScratchBytes, path, threshold, stream, nullptr, nullptr);
+    return conv_impl(d, x, w, y, ws, kScratchBytes, path, threshold, stream, nullptr, tu);
 }
 
 int isc_conv2d_tuned(const isc_conv_desc *d, const float *x, const float *w, float *y, void *ws,

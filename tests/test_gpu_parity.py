@@ -529,12 +529,15 @@ def test_register_kernel_map_groups(torch, isc, case):
 
 @pytest.mark.parametrize("case", [(1, 384, 5, 5, 384, 3, 3, 1, 1, 0.9), (1, 100, 9, 7, 70, 3, 3, 1, 1, 0.5),
                                   (2, 48, 7, 7, 128, 5, 5, 1, 2, 0.9), (1, 60, 6, 6, 20, 5, 5, 1, 2, 0.3),
-                                  (3, 800, 4, 4, 33, 1, 1, 1, 0, 0.6)])
+                                  (3, 800, 4, 4, 33, 1, 1, 1, 0, 0.6), (100, 128, 13, 13, 256, 3, 3, 1, 1, 0.5),
+                                  (60, 64, 14, 14, 320, 3, 3, 1, 1, 0.5)])
 def test_dense_split_reduction(torch, isc, case):
     """The dense path's GEMM with its reduction split over C*R*S (grids of
-    fewer than 128 tiles): plain, rectified with the census, and under AUTO,
-    against the oracle; and the unsplit GEMM (tuning gemm_split = -1) on the
-    same shape."""
+    fewer than 128 tiles, and the last two shapes: 266 and 276 tiles of
+    128 x 128, which the GEMM's model splits into four and two ranges to
+    even out the CUs' shares): plain, rectified with the census, and under
+    AUTO, against the oracle; and the unsplit GEMM (tuning gemm_split = -1)
+    on the same shape with a workspace that has no room for partial sums."""
     N, C, H, W, K, R, S, T, P, sp = case
     note("dense split", case)
     desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
@@ -554,6 +557,14 @@ def test_dense_split_reduction(torch, isc, case):
     u = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=isc.workspace(desc, "dense"),
                        tuning={"gemm_split": -1}).cpu().numpy()
     assert_conv_close(u, want, "dense unsplit %s" % (case,))
+    # the same with a workspace too small for the partial sums (the dense
+    # path's implicit GEMM, unsplit, needs only its decision record)
+    small = torch.empty(4096, dtype=torch.uint8, device="cuda")
+    assert small.numel() < isc.isc_workspace_size(desc, "dense")
+    with pytest.raises(isc.IscError):
+        isc.isc_conv2d(xd, wd, T, P, path="dense", ws=small)
+    v = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=small, tuning={"gemm_split": -1}).cpu().numpy()
+    assert np.array_equal(v.view(np.uint32), u.view(np.uint32))
 
 
 def test_side_stream_parity(torch, isc):

@@ -58,3 +58,30 @@ def test_noalloc_rejects_workspace_beyond_scratch():
     with pytest.raises(isc.IscError) as e:
         isc.isc_conv2d_noalloc(x, w, out, 2, 1, path="sparse")
     assert e.value.status == 3
+
+
+def test_noalloc_runs_the_gemm_unsplit_when_its_partial_sums_do_not_fit():
+    """AlexNet conv5 at batch 128 on the dense path: the GEMM's split
+    reduction wants 66 MB of partial sums, more than the scratch buffer, so
+    the allocation-free entry point runs the GEMM unsplit -- bit for bit the
+    output of isc_conv2d with tuning gemm_split = -1 -- and matches the
+    oracle."""
+    import torch
+    import paper_1704_07724_amd as isc
+    assert torch.cuda.is_available()
+    isc.lib()
+    case = (128, 384, 13, 13, 256, 3, 3, 1, 1, 0.5)
+    N, C, H, W, K, R, S, T, P, sp = case
+    note("noalloc unsplit", case)
+    desc = isc.make_desc(N, C, H, W, K, R, S, T, P)
+    assert isc.isc_workspace_size(desc, "dense") > isc.NOALLOC_SCRATCH_BYTES
+    x, w = workloads.make_case(N, C, H, W, K, R, S, T, P, sp, seed=777)
+    xd, wd = torch.from_numpy(x).cuda(), torch.from_numpy(w).cuda()
+    ref = isc.isc_conv2d(xd, wd, T, P, path="dense", ws=isc.workspace(desc, "dense"), tuning={"gemm_split": -1})
+    out = torch.full_like(ref, float("nan"))
+    isc.isc_conv2d_noalloc(xd, wd, out, T, P, path="dense")
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    want = oracle.conv2d_f64(x, w, T, P)
+    got = out.cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(got - want) <= TOL * (1.0 + np.abs(want)))
