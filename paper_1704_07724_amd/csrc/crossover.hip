@@ -83,7 +83,12 @@ long long crossover_nnz_limit(const SparseShape &sh) {
                                           static_cast<int64_t>(sh.C) * sh.R * sh.S);
     if (!(per_density > 0.0)) return dense >= fixed ? static_cast<long long>(total) : -1;
     const double dstar = (dense - fixed) / per_density;  // density at which the two meet
-    if (dstar < 0.0) return -1;
+    // a crossover past 0.97 sparsity counts as none: keeping the choice open
+    // (the count, and the gated launch of the path not taken) costs more on
+    // every call than the sparse path could save on the rare inputs past it
+    // (Tab. 2's inception 4a.1 at batch 128: crossover 0.99, AUTO 18 % over
+    // the dense path at 0.9 while it kept the choice)
+    if (dstar < 0.03) return -1;
     if (dstar >= 1.0) return static_cast<long long>(total);
     return static_cast<long long>(std::floor(dstar * static_cast<double>(total)));
 }
