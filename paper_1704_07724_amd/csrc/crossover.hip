@@ -37,9 +37,9 @@ struct Fit {
 constexpr Fit kRingFit{0.07996214, 1.82930381, 1.78868403, 0.0};
 // the register-weight kernel per filter size (1x1, 3x3, 5x5: its only
 // ones), whose chain feature counts the rounds of resident workgroups
-constexpr Fit kRegFit1{0.020853829, 0.9847653, 0.45193746, 0.30660876};
-constexpr Fit kRegFit3{0.024391336, 1.1026716, 0.46104798, 0.43310146};
-constexpr Fit kRegFit5{0.019387133, 2.2505374, 1.0093551, 0.87563861};
+constexpr Fit kRegFit1{0.020774588, 1.0001204, 0.45244511, 0.30880721};
+constexpr Fit kRegFit3{0.023252027, 1.112875, 0.44553699, 0.46230413};
+constexpr Fit kRegFit5{0.019268499, 2.1330448, 1.0296948, 0.91803993};
 // its workgroups per CU: eight wavefronts each, 60-66 VGPRs for 1x1 and 3x3
 // filters (eight wavefronts per SIMD, the 33 KB of reduction tiles four
 // times over), 80-98 for 5x5 (five per SIMD)
@@ -83,12 +83,13 @@ long long crossover_nnz_limit(const SparseShape &sh) {
                                           static_cast<int64_t>(sh.C) * sh.R * sh.S);
     if (!(per_density > 0.0)) return dense >= fixed ? static_cast<long long>(total) : -1;
     const double dstar = (dense - fixed) / per_density;  // density at which the two meet
-    // a crossover past 0.97 sparsity counts as none: keeping the choice open
+    // a crossover past 0.95 sparsity counts as none: keeping the choice open
     // (the count, and the gated launch of the path not taken) costs more on
     // every call than the sparse path could save on the rare inputs past it
-    // (Tab. 2's inception 4a.1 at batch 128: crossover 0.99, AUTO 18 % over
-    // the dense path at 0.9 while it kept the choice)
-    if (dstar < 0.03) return -1;
+    // (Tab. 2's inception 4a.1 at batch 128: modelled crossover 0.97-0.99,
+    // measured none up to 0.99; AUTO 18 % over the dense path at 0.9 while
+    // it kept the choice)
+    if (dstar < 0.05) return -1;
     if (dstar >= 1.0) return static_cast<long long>(total);
     return static_cast<long long>(std::floor(dstar * static_cast<double>(total)));
 }

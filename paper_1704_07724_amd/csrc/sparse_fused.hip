@@ -33,10 +33,13 @@ bool fused_wreg_plan(const SparseShape &sh, FusedPlan *plan) {
     const int64_t kp = (sh.K + kLanes - 1) / kLanes * kLanes;
     if (static_cast<int64_t>(sh.C) * sh.R * sh.S * kp * static_cast<int64_t>(sizeof(float)) >= (1ll << 31))
         return false;
-    // 4 x 8 or 2 x 16 tiles; half as many rows when full ones leave CUs
-    // without a workgroup (LeNet conv2 at batch 8: 7.7 -> 6.4 us; at batch
-    // 256 they cost 44 %).  A caller's tuning rows fixes the rows.
-    const int tw = sh.Wo <= 8 ? 8 : 16;
+    // 4 x 8 or 2 x 16 tiles, 2 x 13 and 2 x 14 on maps of exactly that width
+    // (AlexNet conv3-5, the 14 x 14 inception layers: the window loses the
+    // columns past the map and fits one ballot; conv3-5 5 % faster); half as
+    // many rows when full ones leave CUs without a workgroup (LeNet conv2 at
+    // batch 8: 7.7 -> 6.4 us; at batch 256 they cost 44 %).  A caller's
+    // tuning rows fixes the rows.
+    const int tw = sh.Wo <= 8 ? 8 : (sh.Wo == 13 || sh.Wo == 14 ? sh.Wo : 16);
     const int full = 32 / tw;
     const int64_t kgroups = (sh.K + kLanes - 1) / kLanes;
     int th = static_cast<int64_t>(sh.N) * ((sh.Ho + full - 1) / full) * kgroups < kMinGroups ? full / 2 : full;

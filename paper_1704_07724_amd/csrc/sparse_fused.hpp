@@ -466,7 +466,8 @@ hipError_t launch_fused_th(const FusedArgs &a, int th, size_t lds, hipStream_t s
 template <int RS_>
 hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s) {
     if (p.wreg) {
-        // 4 x 8, 2 x 8, 2 x 16 and 1 x 16 tiles, stride 1
+        // 4 x 8, 2 x 8, 2 x 16, 1 x 16 and the exact 13- and 14-column
+        // tiles, stride 1
         if (p.st != 1) return hipErrorInvalidValue;
         if (p.tw == 8) {
             return p.th == 4 ? launch_fused_reg_t<RS_, 4, 8>(a, p.lds, s)
@@ -475,6 +476,14 @@ hipError_t launch_fused_rs(const FusedArgs &a, const FusedPlan &p, hipStream_t s
         if (p.tw == 16) {
             return p.th == 2 ? launch_fused_reg_t<RS_, 2, 16>(a, p.lds, s)
                              : (p.th == 1 ? launch_fused_reg_t<RS_, 1, 16>(a, p.lds, s) : hipErrorInvalidValue);
+        }
+        if (p.tw == 13) {
+            return p.th == 2 ? launch_fused_reg_t<RS_, 2, 13>(a, p.lds, s)
+                             : (p.th == 1 ? launch_fused_reg_t<RS_, 1, 13>(a, p.lds, s) : hipErrorInvalidValue);
+        }
+        if (p.tw == 14) {
+            return p.th == 2 ? launch_fused_reg_t<RS_, 2, 14>(a, p.lds, s)
+                             : (p.th == 1 ? launch_fused_reg_t<RS_, 1, 14>(a, p.lds, s) : hipErrorInvalidValue);
         }
         return hipErrorInvalidValue;
     }
