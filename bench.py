@@ -543,6 +543,21 @@ def sparse_source_hash(kernel: str) -> str:
     return h.hexdigest()[:16]
 
 
+def kernel_symbol(isc, desc, R: int) -> str:
+    """The sparse path's main kernel as the kernel trace names it, with its
+    tile (the on-the-fly kernels; the plan's kernel name otherwise)."""
+    p = isc.isc_sparse_plan(desc)
+    k = p["kernel"]
+    if k == "fused_ring":
+        return "sparse_conv_fring_kernel<%d, %d, %d, %d, %d>" % (R, p["maps_per_lane"], p["rows"], p["cols"],
+                                                                p["waves"])
+    if k == "fused_reg":
+        return "sparse_conv_fused_reg_kernel<%d, %d, %d, ...>" % (R, p["rows"], p["cols"])
+    if k == "fused":
+        return "sparse_conv_fused_kernel<%d, %d, %d, ...>" % (R, p["rows"], p["cols"])
+    return "sparse kernel %s" % k
+
+
 def counted_traffic(workload: str, kernel: str):
     """HBM bytes per launch of the sparse kernel from the committed counter
     summary of the workload (FETCH_SIZE and WRITE_SIZE scaled by a copy
@@ -726,7 +741,7 @@ def main():
     t_kernel = res["t_sparse_kernel"]["mean"]
     achieved = 2.0 * head.nz_macs / (t_kernel * 1e-3) / 1e12
     traffic = counted_traffic(head_layer.name, head.kernel)
-    roofline = {"bound": "alu", "kernel": "sparse_conv_%s_kernel" % head.kernel,
+    roofline = {"bound": "alu", "kernel": kernel_symbol(isc, head.desc, head_layer.R),
                 "achieved": round(achieved, 3), "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / VALU_F32_PEAK_TFLOPS, 4),
                 "traffic": traffic["bytes"] if traffic else None, "traffic_detail": traffic,
