@@ -61,7 +61,9 @@ typedef struct isc_conv_desc {
 
 /* Which path isc_conv2d runs. */
 typedef enum isc_path {
-    ISC_PATH_AUTO = 0,   /* compact, then sparse if sparsity >= threshold else dense */
+    ISC_PATH_AUTO = 0,   /* count the nonzero inputs, then sparse if the count is
+                            within the limit (the per-shape crossover, or a
+                            caller's sparsity threshold), else dense */
     ISC_PATH_SPARSE = 1, /* compaction + zero-skipping convolution */
     ISC_PATH_DENSE = 2   /* MFMA GEMM of Fig. 3 (im2col gathered in the GEMM) */
 } isc_path;
@@ -180,8 +182,10 @@ int isc_conv2d_noalloc(const isc_conv_desc *d, const float *x, const float *w, f
  * smallest input sparsity (fraction of zero inputs, the definition under
  * Tab. 2) at which it takes the sparse path, from models of both paths'
  * times on this GPU for the plans this descriptor gets; 2.0 when the sparse
- * path is never expected to win (for example 1x1 filters at large batch).
- * Host-only.  Errors: NULL, SHAPE, LIMIT. */
+ * path is never expected to win, or only past a sparsity of 0.95, where
+ * keeping the choice open (the count and the gated launch of the path not
+ * taken, on every call) costs more than it could save (for example 1x1
+ * filters at large batch).  Host-only.  Errors: NULL, SHAPE, LIMIT. */
 int isc_crossover_sparsity(const isc_conv_desc *d, double *sparsity);
 
 /* After isc_conv2d has completed on `stream` (this call synchronises the
@@ -228,14 +232,15 @@ int isc_census_size(const isc_conv_desc *d, size_t *bytes);
  *     (never written, or written for another shape) leaves the count
  *     unknown and AUTO runs the dense path: y is right either way.  Shapes
  *     whose sparse path runs over compacted lists (isc_sparse_kernel not
- *     FUSED or FUSED_RING) count x while listing it and ignore x_census.
+ *     FUSED, FUSED_REG or FUSED_RING) count x while listing it and ignore
+ *     x_census.
  *   wt: the repacked filter of isc_repack_filter for K, C, R, S of d
  *     (16-byte aligned), or NULL to repack w into the workspace on every
  *     call.  Used by the on-the-fly sparse kernels.
  *   y_census, y_census_bytes: at least isc_census_size(d) bytes, 16-byte
  *     aligned, or NULL for no census.
  *   tuning: plan overrides, or NULL.
- * The filter-resident, filter-ring and GEMM kernels rectify and count as
+ * The on-the-fly sparse kernels and the GEMM kernels rectify and count as
  * they store y; after a kernel over compacted lists, one more launch
  * rectifies y in place and counts it.  y must not overlap x, w, wt, ws or a
  * census; y_census must not overlap any other argument.
