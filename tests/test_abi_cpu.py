@@ -278,8 +278,9 @@ def test_dw_entry_validation():
 def test_dense_split_workspace():
     """Host plan of the dense GEMM's split reduction: a grid under 128 tiles
     splits C*R*S into ranges of at least 256 (multiples of 32, at most 16)
-    and the workspace holds ranges x K x N*Ho*Wo partial sums; grids that
-    fill the chip, or short reductions, do not split."""
+    and the workspace holds ranges x K x N*Ho*Wo partial sums; short
+    reductions do not split; larger grids split only where that evens out
+    the CUs' shares enough."""
     d = isc.make_desc(1, 384, 5, 5, 384, 3, 3, 1, 1)     # 3 tiles, C*R*S 3456
     lenet = isc.make_desc(256, 20, 12, 12, 50, 5, 5, 1, 0)  # 256 tiles of 64 x 64: no split
     base = isc.isc_workspace_size(lenet, "dense")          # the control block alone
@@ -288,6 +289,16 @@ def test_dense_split_workspace():
     assert split - base == 12 * 384 * 25 * 4
     short = isc.make_desc(3, 500, 4, 4, 33, 1, 1, 1, 0)   # C*R*S 500 < 2 * 256
     assert isc.isc_workspace_size(short, "dense") == base
+    # grids of 128 x 128 tiles split where the GEMM's model gains 10 %: AlexNet
+    # conv5 at batch 128 (338 tiles, two on 82 CUs) in three ranges of 1152;
+    # conv3 (507 tiles, two on almost every CU) and the inception 3x3 branch
+    # (784 tiles, a modelled 5 %) not at all
+    conv5 = isc.make_desc(128, 384, 13, 13, 256, 3, 3, 1, 1)
+    assert isc.isc_workspace_size(conv5, "dense") - base == 3 * 256 * 128 * 169 * 4
+    conv3 = isc.make_desc(128, 256, 13, 13, 384, 3, 3, 1, 1)
+    inc3 = isc.make_desc(128, 96, 28, 28, 128, 3, 3, 1, 1)
+    assert isc.isc_workspace_size(conv3, "dense") == base
+    assert isc.isc_workspace_size(inc3, "dense") == base
 
 
 def test_sparse_plan_and_overrides():
